@@ -1,0 +1,337 @@
+"""Pins of the CPU oracle against what the method and the mathematics fix.
+
+Each test checks the oracle against something other than itself: hand-worked
+fixtures, brute force over tokens / pairs on tiny inputs, special cases that
+reduce to a known matrix, closed forms (Johnson-Lindenstrauss expectation,
+Marchenko-Pastur edges) and invariants.  A plausible mistake in the oracle
+(dropped term, wrong sign or index, transposed operand, wrong flatten order,
+wrong tie order) fails at least one of them.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+import synth
+
+
+def _load(golden_dir, name):
+    with open(os.path.join(golden_dir, name)) as f:
+        d = json.load(f)
+
+    def conv(v):
+        if isinstance(v, list):
+            return [conv(x) for x in v]
+        if isinstance(v, str):
+            return float(v)
+        return v
+    return {k: (conv(v) if k != "source" else v) for k, v in d.items()}
+
+
+# ----------------------------------------------------------------------------
+# projection
+# ----------------------------------------------------------------------------
+def test_projection_golden_hand_worked(golden_dir):
+    d = _load(golden_dir, "projection_k2.json")
+    a = np.array(d["a"], dtype=np.float32)[None]
+    g = np.array(d["g"], dtype=np.float32)[None]
+    R = np.array(d["R"], dtype=np.float32)
+    S = np.array(d["S"], dtype=np.float32)
+    for fn in (O.project_explicit, O.project):
+        P = fn(a, g, R, S, length=[d["length"]])
+        np.testing.assert_array_equal(P[0], np.array(d["P_flat"], dtype=np.float64))
+
+
+def _brute_gradient(a, g, L):
+    """Per-example weight gradient summed over tokens by explicit loops over
+    tokens and matrix entries (no matrix product)."""
+    d_out, d_in = g.shape[1], a.shape[1]
+    G = np.zeros((d_out, d_in))
+    for t in range(L):
+        for r in range(d_out):
+            for c in range(d_in):
+                G[r, c] += float(g[t, r]) * float(a[t, c])
+    return G
+
+
+def test_identity_projection_reproduces_full_gradient():
+    # k = d_in = d_out with R = S = I: P_i is the full per-example gradient.
+    rng = np.random.default_rng(11)
+    d, T, n = 8, 5, 3
+    a = rng.standard_normal((n, T, d)).astype(np.float32)
+    g = rng.standard_normal((n, T, d)).astype(np.float32)
+    eye = np.eye(d, dtype=np.float32)
+    L = [5, 3, 0]
+    for fn in (O.project_explicit, O.project):
+        P = fn(a, g, eye, eye, length=L)
+        for i in range(n):
+            np.testing.assert_allclose(P[i].reshape(d, d), _brute_gradient(a[i], g[i], L[i]),
+                                       rtol=1e-12, atol=1e-12)
+
+
+def test_identity_projection_k64_tiny_shape():
+    # The tiny workload's module is 64 -> 64, so k = 64 with identities
+    # reproduces its exact gradient; checked against a per-token outer sum.
+    rng = np.random.default_rng(12)
+    a = rng.standard_normal((2, 32, 64)).astype(np.float32)
+    g = rng.standard_normal((2, 32, 64)).astype(np.float32)
+    eye = np.eye(64, dtype=np.float32)
+    P = O.project(a, g, eye, eye)
+    for i in range(2):
+        G = sum(np.outer(g[i, t].astype(np.float64), a[i, t].astype(np.float64)) for t in range(32))
+        np.testing.assert_allclose(P[i].reshape(64, 64), G, rtol=1e-12, atol=1e-10)
+
+
+def test_selection_projection_picks_entries():
+    # R = I[:, r_idx], S = I[:, c_idx]  =>  P[r, c] = G[r_idx[r], c_idx[c]].
+    rng = np.random.default_rng(13)
+    d_in, d_out, T, k = 24, 20, 7, 16
+    a = rng.standard_normal((1, T, d_in)).astype(np.float32)
+    g = rng.standard_normal((1, T, d_out)).astype(np.float32)
+    r_idx = rng.permutation(d_out)[:k]
+    c_idx = rng.permutation(d_in)[:k]
+    R = np.eye(d_out, dtype=np.float32)[:, r_idx]
+    S = np.eye(d_in, dtype=np.float32)[:, c_idx]
+    G = _brute_gradient(a[0], g[0], T)
+    want = G[np.ix_(r_idx, c_idx)]
+    for fn in (O.project_explicit, O.project):
+        np.testing.assert_allclose(fn(a, g, R, S)[0].reshape(k, k), want, rtol=1e-12, atol=1e-12)
+
+
+def test_tiny_factored_equals_explicit():
+    x = synth.tiny_inputs()
+    P1 = O.project_explicit(x["a"][:32], x["g"][:32], x["R"], x["S"])
+    P2 = O.project(x["a"][:32], x["g"][:32], x["R"], x["S"])
+    assert np.max(np.abs(P1 - P2)) <= 1e-12 * np.max(np.abs(P1))
+
+
+def test_projection_bilinear_additive_and_padding_invariant():
+    rng = np.random.default_rng(14)
+    n, T, d_in, d_out, k = 2, 9, 32, 48, 16
+    a = rng.standard_normal((n, T, d_in)).astype(np.float32)
+    g = rng.standard_normal((n, T, d_out)).astype(np.float32)
+    R = rng.standard_normal((d_out, k)).astype(np.float32)
+    S = rng.standard_normal((d_in, k)).astype(np.float32)
+    P = O.project(a, g, R, S)
+    # bilinearity in (a, g)
+    P2 = O.project(a * np.float32(2.0), g * np.float32(-0.5), R, S)
+    np.testing.assert_allclose(P2, -1.0 * P, rtol=1e-12, atol=1e-12)
+    # token additivity: P(len 9) = P(first 4 tokens) + P(last 5 tokens)
+    Pa = O.project(a[:, :4], g[:, :4], R, S)
+    Pb = O.project(a[:, 4:], g[:, 4:], R, S)
+    np.testing.assert_allclose(Pa + Pb, P, rtol=1e-10, atol=1e-10)
+    # length L equals the first L tokens; NaN padding beyond L changes nothing
+    L = [4, 7]
+    an = np.stack([synth.nan_pad(a[i], L[i]) for i in range(n)])
+    gn = np.stack([synth.nan_pad(g[i], L[i]) for i in range(n)])
+    Pl = O.project(an, gn, R, S, length=L)
+    for i in range(n):
+        ref = O.project(a[i:i + 1, :L[i]], g[i:i + 1, :L[i]], R, S)[0]
+        np.testing.assert_array_equal(Pl[i], ref)
+    assert np.isfinite(O.project_explicit(an, gn, R, S, length=L)).all()
+
+
+def test_bf16_decoding_exact():
+    vals = np.array([1.0, -2.5, 3.140625, 0.0, 65280.0, 1e-2], dtype=np.float32)
+    bits = synth.to_bf16_bits(vals)
+    back = O.bf16_bits_to_f64(bits)
+    np.testing.assert_array_equal(back[:5], vals[:5].astype(np.float64))
+    # 1e-2 rounds to the nearest bf16 (8 significant bits): |err| <= 2^-8 relative
+    assert abs(back[5] - 1e-2) <= 1e-2 * 2.0 ** -8
+
+
+def test_projection_jl_expectation():
+    # Under R, S with i.i.d. N(0, 1/k) entries, E[R R^T] = I and E[S S^T] = I,
+    # so E <P_i, P_j> = <G_i, G_j>_F (unbiased inner products, the reason the
+    # projection preserves scores in expectation).  Mean over 400 draws, 5 sigma.
+    rng = np.random.default_rng(15)
+    T, d_in, d_out, k = 6, 12, 10, 16
+    a = rng.standard_normal((2, T, d_in)).astype(np.float32)
+    g = rng.standard_normal((2, T, d_out)).astype(np.float32)
+    Gi = _brute_gradient(a[0], g[0], T)
+    Gj = _brute_gradient(a[1], g[1], T)
+    target = float((Gi * Gj).sum())
+    samples = []
+    for s in range(400):
+        r = np.random.default_rng([77, s])
+        R = (r.standard_normal((d_out, k)) / math.sqrt(k)).astype(np.float32)
+        S = (r.standard_normal((d_in, k)) / math.sqrt(k)).astype(np.float32)
+        P = O.project(a, g, R, S)
+        samples.append(float(P[0] @ P[1]))
+    samples = np.array(samples)
+    se = samples.std(ddof=1) / math.sqrt(len(samples))
+    assert abs(samples.mean() - target) < 5 * se
+
+
+# ----------------------------------------------------------------------------
+# normalisation and preconditioning
+# ----------------------------------------------------------------------------
+def test_normalisation_golden_and_invariants(golden_dir):
+    d = _load(golden_dir, "precond_small.json")
+    np.testing.assert_allclose(O.unit_normalize(np.array(d["norm_in"])), np.array(d["norm_out"]),
+                               rtol=0, atol=1e-15)
+    X = np.random.default_rng(16).standard_normal((50, 33)) * 7.0
+    Y = O.unit_normalize(X)
+    assert np.allclose(np.linalg.norm(Y, axis=1), 1.0, atol=1e-14)
+    # direction preserved: every row is a positive multiple of the input row
+    ratio = Y / X
+    assert np.allclose(ratio, ratio[:, :1], rtol=1e-12) and (ratio > 0).all()
+
+
+def test_diag_finalize_golden(golden_dir):
+    d = _load(golden_dir, "precond_small.json")
+    m = O.finalize_diag(np.array(d["diag_h"], dtype=np.float64), d["diag_n"])
+    np.testing.assert_allclose(m, np.array(d["diag_m"]), rtol=0, atol=1e-15)
+
+
+def test_full_finalize_golden(golden_dir):
+    d = _load(golden_dir, "precond_small.json")
+    M, lam = O.finalize_full(np.array(d["full_H"], dtype=np.float64), d["full_n"])
+    np.testing.assert_allclose(M, np.array(d["full_M"]), rtol=0, atol=1e-14)
+    np.testing.assert_allclose(np.sort(lam), [1.0, 3.0], atol=1e-14)
+
+
+def test_accumulate_brute_force():
+    rng = np.random.default_rng(17)
+    X = rng.standard_normal((37, 9)).astype(np.float16)
+    h = O.accumulate_diag(X)
+    H = O.accumulate_full(X)
+    Hb = np.zeros((9, 9))
+    for i in range(37):
+        for p in range(9):
+            for q in range(9):
+                Hb[p, q] += float(X[i, p]) * float(X[i, q])
+    np.testing.assert_allclose(H, Hb, rtol=1e-13, atol=1e-12)
+    np.testing.assert_allclose(h, np.diag(Hb), rtol=1e-13)
+    assert np.array_equal(H, H.T)
+    assert np.linalg.eigvalsh(H).min() > -1e-9
+
+
+def test_diag_whitening_unit_second_moment():
+    # After the diagonal preconditioner every coordinate has mean square 1.
+    rng = np.random.default_rng(18)
+    X = rng.standard_normal((400, 20)) * rng.uniform(0.1, 30, size=20)
+    X[:, 3] = 0.0                     # a dead coordinate stays at zero
+    m = O.finalize_diag(O.accumulate_diag(X), X.shape[0])
+    Y = O.precond_apply(X, "diag", m, unit_norm=False)
+    ms = (Y * Y).mean(axis=0)
+    np.testing.assert_allclose(np.delete(ms, 3), 1.0, rtol=1e-12)
+    assert ms[3] == 0.0
+
+
+def test_full_finalize_identities():
+    rng = np.random.default_rng(19)
+    X = rng.standard_normal((300, 24)) @ rng.standard_normal((24, 24))
+    N = X.shape[0]
+    H = O.accumulate_full(X)
+    M, _ = O.finalize_full(H, N)
+    Hn = H / N
+    np.testing.assert_allclose(M @ Hn @ M, np.eye(24), atol=1e-8)
+    np.testing.assert_allclose(M @ M, np.linalg.inv(Hn), rtol=1e-7, atol=1e-8)
+    # end to end: the second moment of the whitened rows is N * I
+    Y = O.precond_apply(X, "full", M, unit_norm=False)
+    np.testing.assert_allclose(Y.T @ Y, N * np.eye(24), atol=1e-7 * N)
+
+
+def test_full_finalize_rank_deficient_is_pseudo_inverse():
+    rng = np.random.default_rng(20)
+    B = rng.standard_normal((200, 5))
+    X = B @ rng.standard_normal((5, 12))      # rank 5 in R^12
+    M, lam = O.finalize_full(O.accumulate_full(X), 200)
+    assert np.isfinite(M).all()
+    # M^2 is the Moore-Penrose pseudo-inverse of Hn
+    np.testing.assert_allclose(M @ M, np.linalg.pinv(X.T @ X / 200, rcond=1e-10), rtol=1e-6, atol=1e-8)
+
+
+def test_lowrank_spectrum_marchenko_pastur():
+    # G = Z F^T + 0.1 E: the D - r noise eigenvalues of G^T G / N fill the
+    # Marchenko-Pastur bulk 0.01 (1 +- sqrt((D - r)/N))^2 and the r signal
+    # eigenvalues sit near those of F F^T.  Scaled-down (D=256, r=8, N=8192).
+    D, r, N = 256, 8, 8192
+    F = synth.lowrank_factor(D, r, seed=3)
+    X = synth.lowrank_rows(0, N, D=D, rank=r, seed=3, chunk=4096, F=F)
+    lam = np.sort(np.linalg.eigvalsh(O.accumulate_full(X) / N))
+    noise = lam[:D - r]
+    ratio = (D - r) / N
+    lo, hi = 0.01 * (1 - math.sqrt(ratio)) ** 2, 0.01 * (1 + math.sqrt(ratio)) ** 2
+    assert abs(noise.min() - lo) / lo < 0.05 and abs(noise.max() - hi) / hi < 0.05
+    sig = lam[D - r:]
+    ff = np.sort(np.linalg.eigvalsh(F.T @ F))
+    np.testing.assert_allclose(sig, ff, rtol=0.1)
+
+
+# ----------------------------------------------------------------------------
+# scoring and top-k
+# ----------------------------------------------------------------------------
+def test_topk_golden(golden_dir):
+    d = _load(golden_dir, "topk_order.json")
+    Q, G = np.array(d["Q"]), np.array(d["G"])
+    s, i = O.score_topk(Q, G, 3)
+    np.testing.assert_array_equal(s[0], d["k3_scores"])
+    np.testing.assert_array_equal(i[0], d["k3_index"])
+    s, i = O.score_topk(Q, G, 6)
+    np.testing.assert_array_equal(s[0], d["k6_scores"])
+    np.testing.assert_array_equal(i[0], d["k6_index"])
+
+
+def test_topk_brute_force_all_pairs():
+    rng = np.random.default_rng(21)
+    nq, ng, D, k = 8, 256, 12, 5
+    Q = rng.integers(-3, 4, (nq, D)).astype(np.float16)    # small integers: many exact ties
+    G = rng.integers(-3, 4, (ng, D)).astype(np.float16)
+    s, idx = O.score_topk(Q, G, k, index_base=1000)
+    for q in range(nq):
+        pairs = []
+        for j in range(ng):
+            v = sum(float(Q[q, e]) * float(G[j, e]) for e in range(D))
+            pairs.append((v, j))
+        # selection by repeated extraction of the best remaining (max score,
+        # then smallest index)
+        chosen = []
+        remaining = list(pairs)
+        for _ in range(k):
+            best = max(remaining, key=lambda p: (p[0], -p[1]))
+            chosen.append(best)
+            remaining.remove(best)
+        assert [c[0] for c in chosen] == list(s[q])
+        assert [c[1] + 1000 for c in chosen] == list(idx[q])
+
+
+def test_self_cosine_and_symmetry():
+    x = synth.tiny_inputs()
+    P = O.project(x["a"], x["g"], x["R"], x["S"])
+    U = O.unit_normalize(P)
+    Sm = O.scores(U, U)
+    np.testing.assert_allclose(np.diag(Sm), 1.0, atol=1e-12)
+    np.testing.assert_allclose(Sm, Sm.T, atol=0)
+    assert (np.abs(Sm) <= 1 + 1e-12).all()
+    s, idx = O.score_topk(U[:8], U, 5)
+    assert (idx[:, 0] == np.arange(8)).all()
+
+
+def test_merge_equals_single_pass_and_is_associative():
+    rng = np.random.default_rng(22)
+    Q = rng.standard_normal((6, 16))
+    G = rng.standard_normal((500, 16))
+    G[100] = G[7]                     # an exact tie across chunks
+    k = 9
+    ref_s, ref_i = O.score_topk(Q, G, k)
+    s, i = O.score_topk(Q, G[:0], k)
+    assert (i == -1).all() and np.isneginf(s).all()
+    for lo in range(0, 500, 130):
+        hi = min(500, lo + 130)
+        cs, ci = O.score_topk(Q, G[lo:hi], k, index_base=lo)
+        s, i = O.merge_topk(s, i, cs, ci, k)
+    np.testing.assert_array_equal(s, ref_s)
+    np.testing.assert_array_equal(i, ref_i)
+
+
+def test_fewer_candidates_than_k_and_nan():
+    Q = np.array([[1.0, 0.0]])
+    G = np.array([[np.nan, 0.0], [2.0, 0.0]])
+    s, i = O.score_topk(Q, G, 4)
+    assert list(i[0]) == [1, -1, -1, -1]
+    assert s[0, 0] == 2.0 and np.isneginf(s[0, 1:]).all()
