@@ -1,0 +1,314 @@
+"""Python binding of libattr, the MI355X gradient-attribution hot path.
+
+Thin ctypes marshalling over the C ABI declared in ``include/attr.h``: the
+functions below carry the same names as the C entry points, take torch
+tensors that already live on the GPU, and pass their device pointers, sizes
+and the current HIP stream through unchanged.  Every arithmetic step runs in
+the library's HIP kernels; PyTorch only provides device memory and streams.
+The library must have been built (``python -m paper_2606_11660_amd.build``);
+importing this package without it raises, there is no fallback path.
+
+The one host-side step of the method is ``finalize_full`` / ``finalize_diag``:
+turning the accumulated second moment into H^{-1/2} (an fp64 eigendecomposition
+done once per store, outside the per-row hot path).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+__all__ = [
+    "AttrError", "ATTR_F32", "ATTR_BF16", "ATTR_F16", "PRECOND_NONE", "PRECOND_DIAG",
+    "PRECOND_FULL", "Module", "lib", "lib_path", "attr_project", "attr_precond_accumulate",
+    "attr_precond_apply", "attr_score_topk", "attr_project_workspace_size",
+    "attr_precond_accumulate_workspace_size", "attr_precond_apply_workspace_size",
+    "attr_score_topk_workspace_size", "finalize_diag", "finalize_full", "Workspace",
+]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libattr.so")
+
+ATTR_F32, ATTR_BF16, ATTR_F16 = 0, 1, 2
+PRECOND_NONE, PRECOND_DIAG, PRECOND_FULL = 0, 1, 2
+_STATUS = {0: "ATTR_OK", 1: "ATTR_ERR_INVALID_ARG", 2: "ATTR_ERR_UNSUPPORTED",
+           3: "ATTR_ERR_ALIGNMENT", 4: "ATTR_ERR_WORKSPACE", 5: "ATTR_ERR_DEVICE"}
+_TORCH_DTYPE = {torch.float32: ATTR_F32, torch.bfloat16: ATTR_BF16, torch.float16: ATTR_F16}
+
+
+class AttrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class _CModule(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_void_p), ("g", ctypes.c_void_p), ("R", ctypes.c_void_p),
+                ("S", ctypes.c_void_p), ("lda", ctypes.c_int64), ("ldg", ctypes.c_int64),
+                ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64), ("out_col", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load libattr.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2606_11660_amd.build`")
+    L = ctypes.CDLL(_LIB_PATH)
+    i64, i32, vp, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+    L.attr_last_error.restype = ctypes.c_char_p
+    L.attr_status_string.restype = ctypes.c_char_p
+    L.attr_status_string.argtypes = [ctypes.c_int]
+    L.attr_abi_version.restype = ctypes.c_int
+    L.attr_project_workspace_size.restype = sz
+    L.attr_project_workspace_size.argtypes = [ctypes.POINTER(_CModule), i32, ctypes.c_int, i64, i64, i32]
+    L.attr_project.restype = ctypes.c_int
+    L.attr_project.argtypes = [ctypes.POINTER(_CModule), i32, ctypes.c_int, i32, i64, i64, vp, vp,
+                               vp, i64, vp, sz, vp]
+    L.attr_precond_accumulate_workspace_size.restype = sz
+    L.attr_precond_accumulate_workspace_size.argtypes = [i64, i64, ctypes.c_int, ctypes.c_int]
+    L.attr_precond_accumulate.restype = ctypes.c_int
+    L.attr_precond_accumulate.argtypes = [vp, ctypes.c_int, i64, i64, i64, ctypes.c_int, vp, vp, sz, vp]
+    L.attr_precond_apply_workspace_size.restype = sz
+    L.attr_precond_apply_workspace_size.argtypes = [i64, i64, ctypes.c_int]
+    L.attr_precond_apply.restype = ctypes.c_int
+    L.attr_precond_apply.argtypes = [vp, ctypes.c_int, i64, i64, i64, ctypes.c_int, vp, i32, vp,
+                                     ctypes.c_int, i64, vp, sz, vp]
+    L.attr_score_topk_workspace_size.restype = sz
+    L.attr_score_topk_workspace_size.argtypes = [i64, i64, i64, i32]
+    L.attr_score_topk.restype = ctypes.c_int
+    L.attr_score_topk.argtypes = [vp, i64, i64, vp, i64, i64, ctypes.c_int, i64, i32, i64, i32, vp,
+                                  vp, vp, sz, vp]
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise AttrError(status, lib().attr_last_error().decode(errors="replace"))
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype not in _TORCH_DTYPE:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return _TORCH_DTYPE[t.dtype]
+
+
+def _rows(t: torch.Tensor) -> Tuple[int, int, int]:
+    """(rows, width, row stride) of a tensor whose last dim is contiguous."""
+    if t.dim() < 2 or t.stride(-1) != 1:
+        raise ValueError("expected a tensor with a contiguous last dimension")
+    width, ld = t.shape[-1], t.stride(-2)
+    rows = 1
+    for d in range(t.dim() - 1):
+        rows *= t.shape[d]
+    for d in range(t.dim() - 2):
+        if t.stride(d) != t.stride(d + 1) * t.shape[d + 1]:
+            raise ValueError("leading dimensions must be packed")
+    return rows, width, ld
+
+
+class Workspace:
+    """Grow-only device scratch buffer handed to the library calls."""
+
+    def __init__(self, device=None):
+        self.device = torch.device(device or "cuda")
+        self.buf: Optional[torch.Tensor] = None
+
+    def get(self, nbytes: int) -> Tuple[Optional[int], int]:
+        if nbytes == 0:
+            return None, 0
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(int(nbytes), dtype=torch.uint8, device=self.device)
+        return self.buf.data_ptr(), self.buf.numel()
+
+
+_default_ws: Dict[str, Workspace] = {}
+
+
+def _ws(ws: Optional[Workspace], device) -> Workspace:
+    if ws is not None:
+        return ws
+    key = str(device)
+    if key not in _default_ws:
+        _default_ws[key] = Workspace(device)
+    return _default_ws[key]
+
+
+# ----------------------------------------------------------------------------
+# (1) projection
+# ----------------------------------------------------------------------------
+class Module:
+    """One linear module's inputs for ``attr_project``.
+
+    a: [..., d_in] activations, g: [..., d_out] output gradients (token rows,
+    last dim contiguous); R: [d_out, k], S: [d_in, k] contiguous; out_col:
+    first column of the module's k*k block in the output row.
+    """
+
+    def __init__(self, a: torch.Tensor, g: torch.Tensor, R: torch.Tensor, S: torch.Tensor,
+                 out_col: int):
+        self.a, self.g, self.R, self.S, self.out_col = a, g, R, S, int(out_col)
+
+    def c(self) -> _CModule:
+        _, d_in, lda = _rows(self.a)
+        _, d_out, ldg = _rows(self.g)
+        if not (self.R.is_contiguous() and self.S.is_contiguous()):
+            raise ValueError("R and S must be contiguous")
+        return _CModule(self.a.data_ptr(), self.g.data_ptr(), self.R.data_ptr(), self.S.data_ptr(),
+                        lda, ldg, d_in, d_out, self.out_col)
+
+
+def _cmods(mods: Sequence[Module]):
+    arr = (_CModule * len(mods))(*[m.c() for m in mods])
+    return arr
+
+
+def attr_project_workspace_size(mods: Sequence[Module], in_dtype: int, n_examples: int, T: int,
+                                k: int) -> int:
+    return int(lib().attr_project_workspace_size(_cmods(mods), len(mods), in_dtype, n_examples, T, k))
+
+
+def attr_project(mods: Sequence[Module], k: int, n_examples: int, T: int,
+                 out: torch.Tensor, row_offset: Optional[torch.Tensor] = None,
+                 length: Optional[torch.Tensor] = None, ws: Optional[Workspace] = None,
+                 stream=None) -> torch.Tensor:
+    """P_{i,m} = sum_{t < len_i} (R^T g_t)(S^T a_t)^T into out[i, out_col:out_col+k*k]."""
+    if not mods:
+        raise ValueError("need at least one module")
+    in_dtype = _dtype(mods[0].a)
+    cm = _cmods(mods)
+    L = lib()
+    if out.dtype != torch.float32 or out.dim() != 2 or out.stride(1) != 1:
+        raise ValueError("out must be fp32 [n, ldo] with contiguous rows")
+    need = L.attr_project_workspace_size(cm, len(mods), in_dtype, n_examples, T, k)
+    wsp, wsn = _ws(ws, out.device).get(need)
+    if row_offset is not None and (row_offset.dtype != torch.int64 or not row_offset.is_contiguous()):
+        raise ValueError("row_offset must be contiguous int64")
+    if length is not None and (length.dtype != torch.int32 or not length.is_contiguous()):
+        raise ValueError("length must be contiguous int32")
+    _check(L.attr_project(cm, len(mods), in_dtype, k, n_examples, T, _ptr(row_offset), _ptr(length),
+                          out.data_ptr(), out.stride(0), wsp, wsn, _stream(stream)))
+    return out
+
+
+# ----------------------------------------------------------------------------
+# (2) preconditioning
+# ----------------------------------------------------------------------------
+def attr_precond_accumulate_workspace_size(n_rows: int, D: int, x_dtype: int, mode: int) -> int:
+    return int(lib().attr_precond_accumulate_workspace_size(n_rows, D, x_dtype, mode))
+
+
+def attr_precond_accumulate(X: torch.Tensor, mode: int, H: torch.Tensor,
+                            ws: Optional[Workspace] = None, stream=None) -> torch.Tensor:
+    """H += diag(X^T X) (DIAG, H [D]) or the upper triangle of X^T X (FULL, H [D, D])."""
+    n, D, ldx = _rows(X)
+    xd = _dtype(X)
+    if H.dtype != torch.float32 or not H.is_contiguous():
+        raise ValueError("H must be contiguous fp32")
+    L = lib()
+    need = L.attr_precond_accumulate_workspace_size(n, D, xd, mode)
+    wsp, wsn = _ws(ws, X.device).get(need)
+    _check(L.attr_precond_accumulate(X.data_ptr(), xd, n, D, ldx, mode, H.data_ptr(), wsp, wsn,
+                                     _stream(stream)))
+    return H
+
+
+def attr_precond_apply_workspace_size(n_rows: int, D: int, mode: int) -> int:
+    return int(lib().attr_precond_apply_workspace_size(n_rows, D, mode))
+
+
+def attr_precond_apply(X: torch.Tensor, mode: int, M: Optional[torch.Tensor], unit_normalize: bool,
+                       Y: torch.Tensor, ws: Optional[Workspace] = None, stream=None) -> torch.Tensor:
+    """Y = unit_normalise(precondition(X)) cast to Y's dtype."""
+    n, D, ldx = _rows(X)
+    ny, Dy, ldy = _rows(Y)
+    if (ny, Dy) != (n, D):
+        raise ValueError("X and Y shapes differ")
+    if M is not None and (M.dtype != torch.float32 or not M.is_contiguous()):
+        raise ValueError("M must be contiguous fp32")
+    L = lib()
+    need = L.attr_precond_apply_workspace_size(n, D, mode)
+    wsp, wsn = _ws(ws, X.device).get(need)
+    _check(L.attr_precond_apply(X.data_ptr(), _dtype(X), n, D, ldx, mode, _ptr(M),
+                                1 if unit_normalize else 0, Y.data_ptr(), _dtype(Y), ldy, wsp, wsn,
+                                _stream(stream)))
+    return Y
+
+
+def finalize_diag(h: torch.Tensor, n_rows: int) -> torch.Tensor:
+    """m = (h / N)^{-1/2} (0 where h is 0), computed in fp64 on the host."""
+    hn = h.detach().double().cpu().numpy() / float(n_rows)
+    m = np.zeros_like(hn)
+    pos = hn > 0
+    m[pos] = 1.0 / np.sqrt(hn[pos])
+    return torch.from_numpy(m.astype(np.float32)).to(h.device)
+
+
+def finalize_full(H: torch.Tensor, n_rows: int) -> torch.Tensor:
+    """M = (H / N)^{-1/2} from the upper triangle of H, in fp64 on the host.
+
+    The eigendecomposition of the symmetrised H / N runs once per store
+    (LAPACK syevd through numpy); eigenvalues at or below
+    lam_max * D * eps64 are dropped (pseudo-inverse square root).
+    """
+    Hu = np.triu(H.detach().double().cpu().numpy())
+    Hs = (Hu + np.triu(Hu, 1).T) / float(n_rows)
+    lam, V = np.linalg.eigh(Hs)
+    floor = max(lam.max(), 0.0) * Hs.shape[0] * np.finfo(np.float64).eps
+    f = np.where(lam > floor, 1.0 / np.sqrt(np.maximum(lam, floor)), 0.0)
+    M = (V * f) @ V.T
+    M = 0.5 * (M + M.T)
+    return torch.from_numpy(M.astype(np.float32)).to(H.device)
+
+
+# ----------------------------------------------------------------------------
+# (3) scoring
+# ----------------------------------------------------------------------------
+def attr_score_topk_workspace_size(n_q: int, n_g: int, D: int, k: int) -> int:
+    return int(lib().attr_score_topk_workspace_size(n_q, n_g, D, k))
+
+
+def attr_score_topk(Q: torch.Tensor, G: torch.Tensor, k: int, top_score: torch.Tensor,
+                    top_index: torch.Tensor, index_base: int = 0, merge: bool = False,
+                    ws: Optional[Workspace] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Exact top-k of <Q_q, G_j> per query, merged with top_* when merge is set."""
+    nq, D, ldq = _rows(Q)
+    ng, Dg, ldg = _rows(G)
+    if Dg != D:
+        raise ValueError("Q and G widths differ")
+    if Q.dtype != G.dtype:
+        raise ValueError("Q and G dtypes differ")
+    if top_score.dtype != torch.float32 or top_index.dtype != torch.int64:
+        raise ValueError("top_score must be fp32 and top_index int64")
+    if not (top_score.is_contiguous() and top_index.is_contiguous()):
+        raise ValueError("top_score / top_index must be contiguous")
+    L = lib()
+    need = L.attr_score_topk_workspace_size(nq, ng, D, k)
+    wsp, wsn = _ws(ws, Q.device).get(need)
+    _check(L.attr_score_topk(Q.data_ptr(), nq, ldq, G.data_ptr(), ng, ldg, _dtype(Q), D, k,
+                             index_base, 1 if merge else 0, top_score.data_ptr(),
+                             top_index.data_ptr(), wsp, wsn, _stream(stream)))
+    return top_score, top_index

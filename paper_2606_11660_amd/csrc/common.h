@@ -1,0 +1,80 @@
+// Shared device helpers for the gfx950 (CDNA4) kernels: vector types, MFMA
+// fragment wrappers, range-checked buffer loads and wave reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace attr {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+// Raw (stride 0) buffer resource for the gfx9 family: 32-bit element format,
+// range checking against num_records on every lane.
+constexpr int kRsrcWord3 = 0x00020000;
+// Cache policy bit "nt": data streamed once, do not keep it hot in L2/MALL.
+constexpr int kAuxStream = 2;
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           kRsrcWord3);
+}
+
+// 16-byte load through a buffer resource; lanes whose offset is outside the
+// resource's range read zeros (no memory access is made for them).
+__device__ inline i32x4 load16_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kAuxStream);
+}
+__device__ inline i32x4 load16_cached(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+// One 16-byte A fragment times one 16-byte B fragment on the matrix cores,
+// accumulated into a 16x16 fp32 tile.  For bf16/fp16 a fragment is 8 values
+// of K (one 16x16x32 MFMA); for fp32 it is 4 values of K (four 16x16x4
+// MFMAs).  A and B fragments must use the same lane -> K assignment.
+struct Bf16Tag {};
+struct F16Tag {};
+struct F32Tag {};
+
+__device__ inline f32x4 mma16(Bf16Tag, i32x4 a, i32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ inline f32x4 mma16(F16Tag, i32x4 a, i32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+__device__ inline f32x4 mma16(F32Tag, i32x4 a, i32x4 b, f32x4 c) {
+  // Bit-cast whole vectors: a bit-cast of a single vector element is not
+  // reliable in this compiler (it reads element 0).
+  const f32x4 af = __builtin_bit_cast(f32x4, a);
+  const f32x4 bf = __builtin_bit_cast(f32x4, b);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(af.x, bf.x, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(af.y, bf.y, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(af.z, bf.z, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(af.w, bf.w, c, 0, 0, 0);
+  return c;
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ inline double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+}  // namespace attr

@@ -1,0 +1,73 @@
+// Internal interface between the C-ABI layer (api.cpp) and the HIP kernels.
+// Nothing here is exported from the shared library.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace attr {
+
+// ---------------------------------------------------------------------------
+// projection
+// ---------------------------------------------------------------------------
+// One module slot of the projection's device-side table (slots are in
+// launch order, largest modules first).
+struct ProjTab {
+  const void* a;
+  const void* g;
+  const void* pk;     // packed S fragments, then packed R fragments
+  int64_t lda, ldg, out_col;
+  int32_t d_in, d_out;
+};
+
+// Host -> device upload of module descriptors travels in kernel arguments.
+struct PackEntry {
+  const void* a;
+  const void* g;
+  const void* R;
+  const void* S;
+  int64_t lda, ldg, out_col, pk_off;
+  int32_t d_in, d_out;
+};
+constexpr int kPackMax = 24;
+struct PackArgs {
+  PackEntry e[kPackMax];
+  int32_t n;
+  int32_t slot0;
+};
+
+// Tokens handled by one workgroup of the projection for fragment width nk
+// (k = 16 * nk).
+int project_chunk_tokens(int nk);
+// Bytes of packed S and R for one module.
+size_t project_packed_bytes(int64_t d_in, int64_t d_out, int k, int elem_bytes);
+
+hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab* tab,
+                               char* pk_base, hipStream_t s);
+hipError_t launch_project_main(bool bf16, int nk, const ProjTab* tab, int n_slots,
+                               int n_chunks, int64_t n_ex, int64_t T,
+                               const int64_t* row_offset, const int32_t* length,
+                               float* partial, hipStream_t s);
+hipError_t launch_project_reduce(int nk, const ProjTab* tab, int n_slots, int n_chunks,
+                                 int64_t n_ex, int64_t T, const int32_t* length,
+                                 const float* partial, float* out, int64_t ldo,
+                                 hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// row-wise preconditioning / normalisation (NONE and DIAG)
+// ---------------------------------------------------------------------------
+// x_dtype / y_dtype: 0 = fp32, 2 = fp16 (attr_dtype values).
+hipError_t launch_rowscale(int x_dtype, int y_dtype, const void* X, int64_t ldx,
+                           int64_t n_rows, int64_t D, const float* m, int unit,
+                           const float* row_ss, int64_t n_ss, void* Y, int64_t ldy,
+                           hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// diagonal accumulate
+// ---------------------------------------------------------------------------
+int colsumsq_panels(int64_t n_rows, int64_t D);
+hipError_t launch_colsumsq(int x_dtype, const void* X, int64_t ldx, int64_t n_rows,
+                           int64_t D, float* H, double* part, hipStream_t s);
+
+}  // namespace attr

@@ -1,0 +1,365 @@
+// Per-example double-sided random projection of linear-layer gradients
+// (Figure 1 caption; Appendix B, paragraph "Gradients"):
+//     P_i = sum_{t < len_i} (R^T g_t)(S^T a_t)^T,   k x k per module,
+// computed from the token rows a_t, g_t without forming the d_out x d_in
+// per-example gradient.
+//
+// Design (HBM-bound: every a/g element is read once and used for 2k flops):
+//  * One workgroup (4 waves) owns one (module, token chunk, example) item;
+//    each wave owns 16*TT consecutive tokens.  Items are enumerated module
+//    slot major (largest modules first), then chunk, then example, so the
+//    dispatcher hands out the most expensive items first.
+//  * Stage 1 runs on the matrix cores: A_tile (16 tokens x K) times the
+//    packed S fragment gives 16 tokens x 16 projected columns.  Every lane
+//    loads 16 contiguous bytes of one token row per step through a
+//    range-checked buffer resource sized to the valid tokens, so padded or
+//    missing tokens read as exact zeros (NaN padding never enters).
+//  * Stage 2 contracts the two 16x16 fp32 tiles over tokens with fp32 MFMA:
+//    the C layout of stage 1 (lane = column + 16 * (token / 4), register =
+//    token % 4) is directly the A/B operand layout of the 16x16x4 fp32 MFMA
+//    when register q is fed as step q, so no data moves between lanes.
+//  * The four wave partials are summed in LDS in a fixed order and written
+//    as one fp32 k x k partial per item; a second kernel sums the chunks of
+//    each (module, example) in chunk order into the output row
+//    (deterministic, no atomics).
+#include "common.h"
+#include "kernels.h"
+
+namespace attr {
+namespace {
+
+template <bool BF16>
+struct ElemT;
+template <>
+struct ElemT<true> {
+  using tag = Bf16Tag;
+  static constexpr int bytes = 2;
+};
+template <>
+struct ElemT<false> {
+  using tag = F32Tag;
+  static constexpr int bytes = 4;
+};
+
+// Token tiles (16 tokens) per wave for fragment width NK (k = 16 NK).
+template <int NK>
+struct Tiles {
+  static constexpr int TT = NK == 1 ? 4 : (NK == 2 ? 2 : 1);
+};
+
+// ---------------------------------------------------------------------------
+// pack: S [d_in, k] and R [d_out, k] (row-major) into MFMA B fragments.
+// Fragment (step ks, column tile ct) is 64 lanes x 16 bytes; lane
+// (j = lane % 16, grp = lane / 16) holds rows KS*ks + E*grp + e (e < E) of
+// column 16*ct + j, where E = 16 / elem_bytes and KS = 4 E.
+// ---------------------------------------------------------------------------
+template <bool BF16, int NK>
+__global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTab* tab,
+                                                           char* pk_base) {
+  using E_t = ElemT<BF16>;
+  constexpr int E = 16 / E_t::bytes;
+  constexpr int KS = 4 * E;
+  constexpr int K = 16 * NK;
+  const int j = blockIdx.x;
+  if (j >= args.n) return;
+  const PackEntry pe = args.e[j];
+  char* pk = pk_base + pe.pk_off;
+  if (threadIdx.x == 0) {
+    ProjTab t;
+    t.a = pe.a;
+    t.g = pe.g;
+    t.pk = pk;
+    t.lda = pe.lda;
+    t.ldg = pe.ldg;
+    t.out_col = pe.out_col;
+    t.d_in = pe.d_in;
+    t.d_out = pe.d_out;
+    tab[args.slot0 + j] = t;
+  }
+  for (int side = 0; side < 2; ++side) {
+    const int d = side == 0 ? pe.d_in : pe.d_out;
+    const char* src = (const char*)(side == 0 ? pe.S : pe.R);
+    char* dst = pk + (side == 0 ? 0 : (size_t)pe.d_in * K * E_t::bytes);
+    const int n_frag16 = (d / KS) * NK * kWave;  // 16-byte fragments
+    for (int f = threadIdx.x; f < n_frag16; f += blockDim.x) {
+      const int lane = f % kWave;
+      const int ct = (f / kWave) % NK;
+      const int ks = f / (kWave * NK);
+      const int col = 16 * ct + (lane & 15);
+      const int row0 = KS * ks + E * (lane >> 4);
+      i32x4 v;
+      if (E_t::bytes == 2) {
+        uint16_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          h[e] = *(const uint16_t*)(src + ((size_t)(row0 + e) * K + col) * 2);
+        v.x = (int32_t)(h[0] | ((uint32_t)h[1] << 16));
+        v.y = (int32_t)(h[2] | ((uint32_t)h[3] << 16));
+        v.z = (int32_t)(h[4] | ((uint32_t)h[5] << 16));
+        v.w = (int32_t)(h[6] | ((uint32_t)h[7] << 16));
+      } else {
+        int32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          w[e] = *(const int32_t*)(src + ((size_t)(row0 + e) * K + col) * 4);
+        v.x = w[0];
+        v.y = w[1];
+        v.z = w[2];
+        v.w = w[3];
+      }
+      *(i32x4*)(dst + (size_t)f * 16) = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// main projection kernel
+// ---------------------------------------------------------------------------
+// Accumulate one side: acc[tt][ct] += X_tile(tt) * B(ct) over d / KS steps.
+template <typename Tag, int E, int NK, int TT>
+__device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int d,
+                                    const i32x4* __restrict__ pk, int lane,
+                                    f32x4 (&acc)[TT][NK]) {
+  constexpr int KS = 4 * E;
+  constexpr int EB = 16 / E;  // element bytes
+  const int row = lane & 15, grp = lane >> 4;
+  // Byte offset of this lane's fragment for token tile 0, step 0.
+  const uint32_t base = (uint32_t)(((int64_t)row * ld + E * grp) * EB);
+  const uint32_t tile_stride = (uint32_t)(16 * ld * EB);
+  const int n_ks = d / KS;
+
+  i32x4 a_cur[TT], b_cur[NK];
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt) a_cur[tt] = load16_stream(rsrc, base + tt * tile_stride);
+#pragma unroll
+  for (int ct = 0; ct < NK; ++ct) b_cur[ct] = pk[ct * kWave + lane];
+
+  for (int ks = 0; ks < n_ks; ++ks) {
+    i32x4 a_nxt[TT], b_nxt[NK];
+    const bool more = ks + 1 < n_ks;
+    if (more) {
+      const uint32_t off = base + (uint32_t)((ks + 1) * KS * EB);
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt) a_nxt[tt] = load16_stream(rsrc, off + tt * tile_stride);
+#pragma unroll
+      for (int ct = 0; ct < NK; ++ct) b_nxt[ct] = pk[((ks + 1) * NK + ct) * kWave + lane];
+    }
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+      for (int ct = 0; ct < NK; ++ct) acc[tt][ct] = mma16(Tag{}, a_cur[tt], b_cur[ct], acc[tt][ct]);
+    if (more) {
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt) a_cur[tt] = a_nxt[tt];
+#pragma unroll
+      for (int ct = 0; ct < NK; ++ct) b_cur[ct] = b_nxt[ct];
+    }
+  }
+}
+
+template <bool BF16, int NK>
+__global__ __launch_bounds__(256) void project_main_kernel(
+    const ProjTab* __restrict__ tab, int n_chunks, int64_t n_ex, int64_t T,
+    const int64_t* __restrict__ row_offset, const int32_t* __restrict__ length,
+    float* __restrict__ partial) {
+  using E_t = ElemT<BF16>;
+  using Tag = typename E_t::tag;
+  constexpr int EB = E_t::bytes;
+  constexpr int E = 16 / EB;
+  constexpr int KS = 4 * E;
+  constexpr int TT = Tiles<NK>::TT;
+  constexpr int TPW = 16 * TT;  // tokens per wave
+  constexpr int CT = 4 * TPW;   // tokens per workgroup
+  constexpr int KK = 256 * NK * NK;
+
+  // Work-item decode in 32-bit scalar arithmetic (the host keeps the grid
+  // below 2^24 items and n_examples below 2^31).
+  const uint32_t blk = blockIdx.x;
+  const uint32_t nex = (uint32_t)n_ex;
+  const uint32_t i = blk % nex;
+  const uint32_t rest = blk / nex;
+  const int c = (int)(rest % (uint32_t)n_chunks);
+  const int s = (int)(rest / (uint32_t)n_chunks);
+
+  int64_t len = length ? (int64_t)length[i] : T;
+  len = len < 0 ? 0 : (len > T ? T : len);
+  const int64_t t0 = (int64_t)c * CT;
+  if (t0 >= len) return;  // uniform over the workgroup
+
+  const ProjTab md = tab[s];
+  // The wave index is uniform per wave; readfirstlane lets the compiler keep
+  // everything derived from it (token range, buffer resources) in SGPRs.
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63;
+  const int64_t wt0 = t0 + (int64_t)wave * TPW;
+  int64_t ntok = len - wt0;
+  ntok = ntok < 0 ? 0 : (ntok > TPW ? TPW : ntok);
+
+  f32x4 P[NK][NK];
+#pragma unroll
+  for (int rt = 0; rt < NK; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < NK; ++ct) P[rt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (ntok > 0) {
+    const int64_t row0 = (row_offset ? row_offset[i] : (int64_t)i * T) + wt0;
+    const char* a_ptr = (const char*)md.a + row0 * md.lda * EB;
+    const char* g_ptr = (const char*)md.g + row0 * md.ldg * EB;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_ptr, (uint32_t)(ntok * md.lda * EB));
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(g_ptr, (uint32_t)(ntok * md.ldg * EB));
+    const i32x4* pkS = (const i32x4*)md.pk;
+    const i32x4* pkR = pkS + (size_t)(md.d_in / KS) * NK * kWave;
+
+    f32x4 At[TT][NK], Gt[TT][NK];
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+      for (int ct = 0; ct < NK; ++ct) {
+        At[tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+        Gt[tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    project_side<Tag, E, NK, TT>(ra, md.lda, md.d_in, pkS, lane, At);
+    project_side<Tag, E, NK, TT>(rg, md.ldg, md.d_out, pkR, lane, Gt);
+
+    // P[r][c] += sum_tokens Gt[token][r] * At[token][c]; register q of the
+    // stage-1 tiles holds token 4 * (lane / 16) + q, column lane % 16.
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+      for (int rt = 0; rt < NK; ++rt)
+#pragma unroll
+        for (int ct = 0; ct < NK; ++ct)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            P[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(Gt[tt][rt][q], At[tt][ct][q],
+                                                             P[rt][ct], 0, 0, 0);
+  }
+
+  // Fixed-order reduction of the four wave partials: waves 1..3 park their
+  // tiles in LDS, wave 0 adds them in wave order and writes the item.
+  __shared__ float red[3][KK];
+  if (wave > 0) {
+#pragma unroll
+    for (int rt = 0; rt < NK; ++rt)
+#pragma unroll
+      for (int ct = 0; ct < NK; ++ct)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) red[wave - 1][((rt * NK + ct) * 4 + q) * kWave + lane] = P[rt][ct][q];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    float* dst = partial + (int64_t)blk * KK;
+#pragma unroll
+    for (int rt = 0; rt < NK; ++rt)
+#pragma unroll
+      for (int ct = 0; ct < NK; ++ct)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int e = ((rt * NK + ct) * 4 + q) * kWave + lane;
+          float v = P[rt][ct][q];
+          v += red[0][e];
+          v += red[1][e];
+          v += red[2][e];
+          dst[e] = v;
+        }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// reduce: out[i, out_col + r*k + c] = sum over chunks of the item partials.
+// Partial element e = ((rt*NK + ct)*4 + q)*64 + lane holds
+// r = 16 rt + 4 (lane / 16) + q, c = 16 ct + lane % 16.
+// ---------------------------------------------------------------------------
+template <int NK>
+__global__ __launch_bounds__(256) void project_reduce_kernel(
+    const ProjTab* __restrict__ tab, int n_chunks, int64_t n_ex, int64_t T, int CT,
+    const int32_t* __restrict__ length, const float* __restrict__ partial,
+    float* __restrict__ out, int64_t ldo) {
+  constexpr int K = 16 * NK;
+  constexpr int KK = K * K;
+  const int64_t i = blockIdx.x % n_ex;
+  const int s = (int)(blockIdx.x / n_ex);
+  int64_t len = length ? (int64_t)length[i] : T;
+  len = len < 0 ? 0 : (len > T ? T : len);
+  const int nck = (int)((len + CT - 1) / CT);
+  const int64_t out_col = tab[s].out_col;
+  for (int e = threadIdx.x; e < KK; e += blockDim.x) {
+    float v = 0.f;
+    for (int c = 0; c < nck; ++c) v += partial[((((int64_t)s * n_chunks + c) * n_ex) + i) * KK + e];
+    const int lane = e & 63;
+    const int q = (e >> 6) & 3;
+    const int tile = e >> 8;
+    const int rt = tile / NK, ct = tile % NK;
+    const int r = 16 * rt + 4 * (lane >> 4) + q;
+    const int cc = 16 * ct + (lane & 15);
+    out[i * ldo + out_col + r * K + cc] = v;
+  }
+}
+
+}  // namespace
+
+int project_chunk_tokens(int nk) {
+  return 64 * (nk == 1 ? 4 : (nk == 2 ? 2 : 1));
+}
+
+size_t project_packed_bytes(int64_t d_in, int64_t d_out, int k, int elem_bytes) {
+  return (size_t)(d_in + d_out) * (size_t)k * (size_t)elem_bytes;
+}
+
+hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab* tab,
+                               char* pk_base, hipStream_t s) {
+  dim3 grid(args.n), block(256);
+#define ATTR_PACK(B, N) \
+  hipLaunchKernelGGL((project_pack_kernel<B, N>), grid, block, 0, s, args, tab, pk_base)
+  if (bf16) {
+    if (nk == 1) ATTR_PACK(true, 1);
+    else if (nk == 2) ATTR_PACK(true, 2);
+    else ATTR_PACK(true, 4);
+  } else {
+    if (nk == 1) ATTR_PACK(false, 1);
+    else if (nk == 2) ATTR_PACK(false, 2);
+    else ATTR_PACK(false, 4);
+  }
+#undef ATTR_PACK
+  return hipGetLastError();
+}
+
+hipError_t launch_project_main(bool bf16, int nk, const ProjTab* tab, int n_slots,
+                               int n_chunks, int64_t n_ex, int64_t T,
+                               const int64_t* row_offset, const int32_t* length,
+                               float* partial, hipStream_t s) {
+  const int64_t nblk = (int64_t)n_slots * n_chunks * n_ex;
+  dim3 grid((unsigned)nblk), block(256);
+#define ATTR_MAIN(B, N)                                                                    \
+  hipLaunchKernelGGL((project_main_kernel<B, N>), grid, block, 0, s, tab, n_chunks, n_ex, T, \
+                     row_offset, length, partial)
+  if (bf16) {
+    if (nk == 1) ATTR_MAIN(true, 1);
+    else if (nk == 2) ATTR_MAIN(true, 2);
+    else ATTR_MAIN(true, 4);
+  } else {
+    if (nk == 1) ATTR_MAIN(false, 1);
+    else if (nk == 2) ATTR_MAIN(false, 2);
+    else ATTR_MAIN(false, 4);
+  }
+#undef ATTR_MAIN
+  return hipGetLastError();
+}
+
+hipError_t launch_project_reduce(int nk, const ProjTab* tab, int n_slots, int n_chunks,
+                                 int64_t n_ex, int64_t T, const int32_t* length,
+                                 const float* partial, float* out, int64_t ldo,
+                                 hipStream_t s) {
+  dim3 grid((unsigned)((int64_t)n_slots * n_ex)), block(256);
+  const int CT = project_chunk_tokens(nk);
+#define ATTR_RED(N)                                                                          \
+  hipLaunchKernelGGL((project_reduce_kernel<N>), grid, block, 0, s, tab, n_chunks, n_ex, T, CT, \
+                     length, partial, out, ldo)
+  if (nk == 1) ATTR_RED(1);
+  else if (nk == 2) ATTR_RED(2);
+  else ATTR_RED(4);
+#undef ATTR_RED
+  return hipGetLastError();
+}
+
+}  // namespace attr

@@ -1,0 +1,116 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library must load, export every function declared in include/attr.h and
+reject bad arguments on the host with the documented status before any
+device work is enqueued.  Only calls that fail validation are made here, so
+no kernel is ever launched.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_11660_amd as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+OK, INVALID, UNSUPPORTED, ALIGN, WORKSPACE, DEVICE = 0, 1, 2, 3, 4, 5
+FAKE = 1 << 40          # 16-byte aligned fake device address, never dereferenced
+
+
+@pytest.fixture(scope="module")
+def L():
+    return P.lib()
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "attr.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = set(re.findall(r"\b(attr_[a-z_]+)\s*\(", src))
+    return sorted(names)
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared_functions()
+    assert len(names) >= 11
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings(L):
+    assert L.attr_abi_version() == 1
+    assert L.attr_status_string(0) == b"ATTR_OK"
+    assert L.attr_status_string(4) == b"ATTR_ERR_WORKSPACE"
+    assert L.attr_last_error() == b""
+
+
+def _mod(d_in=64, d_out=64, lda=None, ldg=None, out_col=0, a=FAKE, g=FAKE, R=FAKE, S=FAKE):
+    return P._CModule(a, g, R, S, lda or d_in, ldg or d_out, d_in, d_out, out_col)
+
+
+def _project(L, mods, dtype=P.ATTR_BF16, k=16, n=4, T=32, out=FAKE, ldo=256, ws=None, wsb=0):
+    arr = (P._CModule * len(mods))(*mods)
+    return L.attr_project(arr, len(mods), dtype, k, n, T, None, None, out, ldo, ws, wsb, None)
+
+
+def test_project_validation(L):
+    assert _project(L, [_mod()], k=24) == UNSUPPORTED
+    assert _project(L, [_mod()], dtype=P.ATTR_F16) == UNSUPPORTED
+    assert b"in_dtype" in L.attr_last_error()
+    assert _project(L, [_mod(d_in=48)]) == ALIGN                   # not a multiple of 32 (bf16)
+    assert _project(L, [_mod(d_in=48)], dtype=P.ATTR_F32) != ALIGN   # fine for fp32 (16)
+    assert _project(L, [_mod(a=0)]) == INVALID
+    assert _project(L, [_mod(a=FAKE + 2)]) == ALIGN
+    assert _project(L, [_mod(lda=32)]) == INVALID
+    assert _project(L, [_mod(lda=68)]) == ALIGN
+    assert _project(L, [_mod(out_col=1)]) == INVALID               # 1 + 256 > ldo
+    assert _project(L, [_mod(), _mod(out_col=128)], ldo=512) == INVALID   # overlapping blocks
+    assert _project(L, [_mod()], n=-1) == INVALID
+    assert _project(L, [_mod()], T=0) == INVALID
+    assert _project(L, [_mod()], out=0) == INVALID
+    assert _project(L, [_mod()], ldo=100) == INVALID
+    # all arguments valid, no workspace: rejected before any launch
+    assert _project(L, [_mod()], ws=None, wsb=0) == WORKSPACE
+    need = L.attr_project_workspace_size((P._CModule * 1)(_mod()), 1, P.ATTR_BF16, 4, 32, 16)
+    assert need > 0
+    assert _project(L, [_mod()], ws=FAKE, wsb=need - 1) == WORKSPACE
+    assert _project(L, [_mod()], ws=FAKE + 16, wsb=need) == ALIGN   # workspace not 256-aligned
+    # zero examples: valid no-op that touches nothing
+    assert _project(L, [_mod()], n=0) == OK
+
+
+def test_project_workspace_size_grows_with_batch(L):
+    mods = (P._CModule * 2)(_mod(768, 2304), _mod(3072, 768, out_col=256))
+    s1 = L.attr_project_workspace_size(mods, 2, P.ATTR_BF16, 8, 512, 16)
+    s2 = L.attr_project_workspace_size(mods, 2, P.ATTR_BF16, 16, 512, 16)
+    assert 0 < s1 < s2
+    assert L.attr_project_workspace_size(mods, 2, P.ATTR_BF16, 8, 512, 24) == 0
+
+
+def test_accumulate_and_apply_validation(L):
+    acc = L.attr_precond_accumulate
+    H = FAKE + (1 << 30)
+    assert acc(FAKE, P.ATTR_F16, 10, 64, 64, 7, H, None, 0, None) == UNSUPPORTED
+    assert acc(FAKE, P.ATTR_F16, -1, 64, 64, P.PRECOND_DIAG, H, None, 0, None) == INVALID
+    assert acc(FAKE, P.ATTR_F16, 10, 60, 64, P.PRECOND_DIAG, H, None, 0, None) == ALIGN
+    assert acc(FAKE, P.ATTR_F16, 10, 64, 32, P.PRECOND_DIAG, H, None, 0, None) == INVALID
+    assert acc(FAKE, P.ATTR_F16, 10, 64, 64, P.PRECOND_DIAG, 0, None, 0, None) == INVALID
+    assert acc(FAKE, P.ATTR_F16, 10, 64, 64, P.PRECOND_DIAG, H, None, 0, None) == WORKSPACE
+    assert acc(FAKE, P.ATTR_F16, 10, 64, 64, P.PRECOND_DIAG, FAKE + 64, None, 0, None) == INVALID  # H inside X
+    assert acc(FAKE, P.ATTR_F16, 0, 64, 64, P.PRECOND_DIAG, H, None, 0, None) == OK
+    app = L.attr_precond_apply
+    Y = FAKE + (1 << 30)
+    assert app(FAKE, P.ATTR_BF16, 4, 64, 64, P.PRECOND_NONE, None, 1, Y, P.ATTR_F16, 64, None, 0, None) == UNSUPPORTED
+    assert app(FAKE, P.ATTR_F32, 4, 64, 64, P.PRECOND_DIAG, None, 1, Y, P.ATTR_F16, 64, None, 0, None) == INVALID
+    assert app(FAKE, P.ATTR_F32, 4, 64, 64, P.PRECOND_NONE, FAKE, 1, Y, P.ATTR_F16, 64, None, 0, None) == INVALID
+    assert app(FAKE, P.ATTR_F32, 4, 64, 64, P.PRECOND_NONE, None, 1, FAKE + 8 * 64, P.ATTR_F16, 64, None, 0, None) == INVALID
+    assert app(FAKE, P.ATTR_F32, 4, 12, 64, P.PRECOND_NONE, None, 1, Y, P.ATTR_F16, 64, None, 0, None) == ALIGN
+    assert app(FAKE, P.ATTR_F32, 0, 64, 64, P.PRECOND_NONE, None, 1, Y, P.ATTR_F16, 64, None, 0, None) == OK
+
+
+def test_error_message_is_thread_local_and_cleared(L):
+    _project(L, [_mod()], k=24)
+    assert L.attr_last_error() != b""
+    assert _project(L, [_mod()], n=0) == OK
+    assert L.attr_last_error() == b""

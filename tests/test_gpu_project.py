@@ -1,0 +1,211 @@
+"""GPU parity of attr_project against the fp64 oracle (same seeded inputs).
+
+Bar: per-row relative L2 error <= 1e-5 for fp32 inputs and <= 2e-2 for
+bf16 inputs.  The bf16 path multiplies exact bf16 values and accumulates in
+fp32, so its error is also checked against a 1e-4 design bound.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2606_11660_amd as P
+import synth
+from tests._util import dev, host, row_rel_l2, say
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL, F32_TOL, BF16_DESIGN = 2e-2, 1e-5, 1e-4
+
+
+def _run_project(mods_host, k, n, T, length=None, row_offset=None, dtype="bf16", ldo=None,
+                 extra_cols=0, nan_pad=True):
+    """mods_host: list of (a [n*T or rows, d_in], g, R, S) numpy arrays."""
+    D = len(mods_host) * k * k
+    ldo = ldo or D + extra_cols
+    out = torch.full((n, ldo), -7.0, dtype=torch.float32, device="cuda")
+    mods = []
+    for m, (a, g, R, S) in enumerate(mods_host):
+        mods.append(P.Module(dev(a), dev(g), dev(R), dev(S), out_col=m * k * k))
+    L = None if length is None else torch.from_numpy(np.asarray(length, dtype=np.int32)).cuda()
+    ro = None if row_offset is None else torch.from_numpy(np.asarray(row_offset, dtype=np.int64)).cuda()
+    P.attr_project(mods, k, n, T, out, row_offset=ro, length=L)
+    torch.cuda.synchronize()
+    return host(out)
+
+
+def _oracle(mods_host, k, n, T, length=None, row_offset=None):
+    blocks = []
+    for (a, g, R, S) in mods_host:
+        if row_offset is None:
+            a3 = a.reshape(n, T, -1)
+            g3 = g.reshape(n, T, -1)
+        else:
+            a3 = np.stack([a[row_offset[i]:row_offset[i] + T] for i in range(n)])
+            g3 = np.stack([g[row_offset[i]:row_offset[i] + T] for i in range(n)])
+        blocks.append(O.project(a3, g3, R, S, length=length))
+    return O.project_concat(blocks)
+
+
+def test_tiny_fp32_parity():
+    say("case: tiny fp32 k=16 n=256 T=32")
+    x = synth.tiny_inputs()
+    a = x["a"].reshape(-1, 64)
+    g = x["g"].reshape(-1, 64)
+    got = _run_project([(a, g, x["R"], x["S"])], 16, 256, 32, dtype="f32")
+    ref = O.project(x["a"], x["g"], x["R"], x["S"])
+    err = row_rel_l2(got, ref)
+    say("tiny max row rel-L2", err.max())
+    assert err.max() <= F32_TOL
+
+
+def _random_modules(shapes, n, T, k, dtype, seed, lengths=None):
+    rng = np.random.default_rng(seed)
+    out = []
+    for (d_in, d_out) in shapes:
+        a = rng.standard_normal((n * T, d_in))
+        g = rng.standard_normal((n * T, d_out)) * 1e-2
+        R = rng.standard_normal((d_out, k)) / np.sqrt(k)
+        S = rng.standard_normal((d_in, k)) / np.sqrt(k)
+        if dtype == "bf16":
+            cast = synth.to_bf16_bits
+        else:
+            cast = lambda v: v.astype(np.float32)
+        a, g, R, S = cast(a), cast(g), cast(R), cast(S)
+        if lengths is not None:
+            for i, L in enumerate(lengths):
+                a[i * T:(i + 1) * T] = synth.nan_pad(a[i * T:(i + 1) * T], L)
+                g[i * T:(i + 1) * T] = synth.nan_pad(g[i * T:(i + 1) * T], L)
+        out.append((a, g, R, S))
+    return out
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("k", [16, 32, 64])
+def test_ragged_lengths_nan_padding(dtype, k):
+    n, T = 7, 300                     # T spans two 256-token chunks, not a multiple of 16
+    lengths = [0, 1, 17, 255, 256, 257, 300]
+    shapes = [(64, 96), (128, 32), (32, 64)]
+    say(f"case: ragged dtype={dtype} k={k} n={n} T={T}")
+    mods = _random_modules(shapes, n, T, k, dtype, seed=100 + k, lengths=lengths)
+    got = _run_project(mods, k, n, T, length=lengths, dtype=dtype)
+    ref = _oracle(mods, k, n, T, length=lengths)
+    assert np.isfinite(got).all()
+    assert (got[0] == 0).all()        # len 0 -> zero row
+    err = row_rel_l2(got, ref)
+    say("max row rel-L2", err.max())
+    assert err.max() <= (BF16_DESIGN if dtype == "bf16" else F32_TOL)
+
+
+def test_untouched_columns_and_row_offset():
+    n, T, k = 5, 40, 16
+    say("case: row_offset packed layout, extra output columns")
+    shapes = [(96, 64), (64, 128)]
+    lengths = [40, 3, 0, 33, 16]
+    # packed rows: example i starts at row_offset[i]; rows between are garbage
+    row_offset = [0, 50, 60, 61, 120]
+    rows = 200
+    rng = np.random.default_rng(7)
+    mods = []
+    for (d_in, d_out) in shapes:
+        a = synth.to_bf16_bits(rng.standard_normal((rows, d_in)))
+        g = synth.to_bf16_bits(rng.standard_normal((rows, d_out)))
+        R = synth.to_bf16_bits(rng.standard_normal((d_out, k)) / 4)
+        S = synth.to_bf16_bits(rng.standard_normal((d_in, k)) / 4)
+        mods.append((a, g, R, S))
+    got = _run_project(mods, k, n, T, length=lengths, row_offset=row_offset, extra_cols=24)
+    ref = _oracle(mods, k, n, T, length=lengths, row_offset=row_offset)
+    err = row_rel_l2(got[:, :2 * k * k], ref)
+    say("max row rel-L2", err.max())
+    assert err.max() <= BF16_DESIGN
+    assert (got[:, 2 * k * k:] == -7.0).all()
+
+
+def test_gpt2_shaped_two_examples():
+    wl = synth.GPT2
+    n, T, k = 2, wl.T, wl.k
+    say("case: gpt2 48 modules n=2 T=512")
+    mods, blocks = [], []
+    for m in range(len(wl.modules)):
+        R, S = synth.projection_pair(wl, m)
+        a = np.concatenate([synth.module_example(wl, m, i)[0] for i in range(n)])
+        g = np.concatenate([synth.module_example(wl, m, i)[1] for i in range(n)])
+        mods.append((a, g, R, S))
+    got = _run_project(mods, k, n, T)
+    ref = _oracle(mods, k, n, T)
+    err = row_rel_l2(got, ref)
+    say("gpt2 max row rel-L2", err.max())
+    assert err.max() <= BF16_DESIGN
+
+
+def test_llama1b_shaped_lengths():
+    wl = synth.LLAMA1B
+    n, T, k = 3, wl.T, wl.k
+    lengths = synth.example_lengths(wl.n_examples)[:n]
+    say(f"case: 1B-shaped modules q/gate/down n=3 T=2048 lengths={list(lengths)}")
+    picks = [0, 4, 6]                  # q (2048->2048), gate (2048->8192), down (8192->2048)
+    mods = []
+    for m in picks:
+        R, S = synth.projection_pair(wl, m)
+        a = np.concatenate([synth.nan_pad(synth.module_example(wl, m, i)[0], lengths[i]) for i in range(n)])
+        g = np.concatenate([synth.nan_pad(synth.module_example(wl, m, i)[1], lengths[i]) for i in range(n)])
+        mods.append((a, g, R, S))
+    got = _run_project(mods, k, n, T, length=lengths)
+    ref = _oracle(mods, k, n, T, length=lengths)
+    err = row_rel_l2(got, ref)
+    say("1B max row rel-L2", err.max())
+    assert err.max() <= BF16_DESIGN
+
+
+def test_deterministic_bitwise():
+    n, T, k = 9, 520, 16
+    say("case: determinism")
+    mods = _random_modules([(256, 512), (512, 256)], n, T, k, "bf16", seed=5)
+    a = _run_project(mods, k, n, T)
+    b = _run_project(mods, k, n, T)
+    assert np.array_equal(a, b)
+
+
+def test_zero_examples_is_noop():
+    k = 16
+    mods = _random_modules([(64, 64)], 1, 16, k, "bf16", seed=6)
+    out = torch.full((1, 256), 3.0, device="cuda")
+    m = [P.Module(dev(mods[0][0]), dev(mods[0][1]), dev(mods[0][2]), dev(mods[0][3]), 0)]
+    P.attr_project(m, k, 0, 16, out)
+    torch.cuda.synchronize()
+    assert (host(out) == 3.0).all()
+
+
+def test_bench_launch_full_batch_sampled():
+    """The bench's launch: 64 GPT-2 examples x 48 modules x 512 tokens in one
+    call (9.7 GB of bf16 inputs); examples 0, 31 and 63 hold the seeded synth
+    inputs and are checked row by row against the oracle."""
+    wl = synth.GPT2
+    n, T, k = 64, wl.T, wl.k
+    sampled = [0, 31, 63]
+    say("case: gpt2 full batch n=64 (bench launch), sampled rows", sampled)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1234)
+    mods, host_mods = [], []
+    for m, md in enumerate(wl.modules):
+        a = torch.randn((n * T, md.d_in), generator=gen, device="cuda").to(torch.bfloat16)
+        g = (torch.randn((n * T, md.d_out), generator=gen, device="cuda") * 1e-2).to(torch.bfloat16)
+        R, S = synth.projection_pair(wl, m)
+        ha, hg = [], []
+        for i in sampled:
+            ai, gi = synth.module_example(wl, m, i)
+            a[i * T:(i + 1) * T] = dev(ai)
+            g[i * T:(i + 1) * T] = dev(gi)
+            ha.append(ai)
+            hg.append(gi)
+        mods.append(P.Module(a, g, dev(R), dev(S), m * k * k))
+        host_mods.append((np.stack(ha), np.stack(hg), R, S))
+    out = torch.empty((n, wl.D), dtype=torch.float32, device="cuda")
+    P.attr_project(mods, k, n, T, out)
+    torch.cuda.synchronize()
+    got = host(out)[sampled]
+    ref = O.project_concat([O.project(a, g, R, S) for (a, g, R, S) in host_mods])
+    err = row_rel_l2(got, ref)
+    say("full-batch sampled max row rel-L2", err.max())
+    assert err.max() <= BF16_DESIGN
+    assert np.isfinite(host(out)).all()
