@@ -77,7 +77,7 @@ typedef struct {
   const void* R;     /* [d_out, k] row-major, same dtype as a/g (output-side projection) */
   const void* S;     /* [d_in,  k] row-major, same dtype as a/g (input-side projection) */
   int64_t lda, ldg;  /* row strides in elements, >= d_in / d_out, multiples of 8 */
-  int64_t d_in, d_out;  /* multiples of 32 (bf16) or 16 (fp32); at most 65536 */
+  int64_t d_in, d_out;  /* multiples of 64 (bf16) or 32 (fp32); at most 65536 */
   int64_t out_col;   /* first column of this module's k*k block in `out` */
 } attr_module;
 

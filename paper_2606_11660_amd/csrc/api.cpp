@@ -104,7 +104,8 @@ attr_status project_validate(const attr_module* mods, int32_t n_mods, attr_dtype
   if (n_ex > 0 && !out) return fail(ATTR_ERR_INVALID_ARG, "out is NULL");
   if (!aligned16(out)) return fail(ATTR_ERR_ALIGNMENT, "out must be 16-byte aligned");
   const int eb = dtype_bytes(in_dtype);
-  const int KS = in_dtype == ATTR_BF16 ? 32 : 16;
+  // Rows are streamed in 128-byte groups: 64 bf16 or 32 fp32 values.
+  const int KS = in_dtype == ATTR_BF16 ? 64 : 32;
   const int ld_mult = 16 / eb;
   const int64_t kk = (int64_t)k * k;
   if (ldo < kk) return fail(ATTR_ERR_INVALID_ARG, "ldo=%lld < k*k", (long long)ldo);
@@ -124,7 +125,7 @@ attr_status project_validate(const attr_module* mods, int32_t n_mods, attr_dtype
       return fail(ATTR_ERR_ALIGNMENT, "module %d: lda/ldg must be multiples of %d elements", j, ld_mult);
     if (!aligned16(m.a) || !aligned16(m.g) || !aligned16(m.R) || !aligned16(m.S))
       return fail(ATTR_ERR_ALIGNMENT, "module %d: pointers must be 16-byte aligned", j);
-    if (m.lda * 64 * eb >= (1ll << 31) || m.ldg * 64 * eb >= (1ll << 31))
+    if (m.lda * 256 * eb >= (1ll << 31) || m.ldg * 256 * eb >= (1ll << 31))
       return fail(ATTR_ERR_UNSUPPORTED, "module %d: row stride too large", j);
     if (m.out_col < 0 || m.out_col + kk > ldo)
       return fail(ATTR_ERR_INVALID_ARG, "module %d: out_col=%lld + k*k exceeds ldo=%lld", j,

@@ -41,10 +41,18 @@ struct ElemT<false> {
   static constexpr int bytes = 4;
 };
 
-// Token tiles (16 tokens) per wave for fragment width NK (k = 16 NK).
+// Token tiles (16 tokens) per wave and load steps kept in flight, per
+// fragment width NK (k = 16 NK).
+#ifndef ATTR_PROJ_TT1
+#define ATTR_PROJ_TT1 4
+#endif
+#ifndef ATTR_PROJ_PD
+#define ATTR_PROJ_PD 3
+#endif
 template <int NK>
 struct Tiles {
-  static constexpr int TT = NK == 1 ? 4 : (NK == 2 ? 2 : 1);
+  static constexpr int TT = NK == 1 ? ATTR_PROJ_TT1 : (NK == 2 ? 2 : 1);
+  static constexpr int PD = ATTR_PROJ_PD;
 };
 
 // ---------------------------------------------------------------------------
@@ -115,44 +123,82 @@ __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTa
 // ---------------------------------------------------------------------------
 // main projection kernel
 // ---------------------------------------------------------------------------
-// Accumulate one side: acc[tt][ct] += X_tile(tt) * B(ct) over d / KS steps.
-template <typename Tag, int E, int NK, int TT>
+// Accumulate one side: acc[tt][ct] += X_tile(tt) * B(ct) over d.
+//
+// The token rows are read in K-groups of 128 bytes per row (two MFMA steps).
+// Global loads are line-coalesced: 8 consecutive lanes read one full 128-byte
+// row segment, so one instruction covers 8 rows.  The MFMA operand layout
+// wants 16 different rows per quarter-wave instead, so each group passes
+// through a per-wave 2 KB LDS tile: written with an XOR swizzle (chunk ^
+// row % 8) and read back as MFMA fragments, both conflict-free.  PD groups
+// of loads are kept in flight in a register ring (the loop is unrolled by
+// PD so ring slots are compile-time registers).
+template <typename Tag, int E, int NK, int TT, int PD>
 __device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int d,
                                     const i32x4* __restrict__ pk, int lane,
-                                    f32x4 (&acc)[TT][NK]) {
-  constexpr int KS = 4 * E;
+                                    i32x4* __restrict__ xp, f32x4 (&acc)[TT][NK]) {
+  constexpr int KS = 4 * E;   // K elements per MFMA step (one 16-byte fragment)
   constexpr int EB = 16 / E;  // element bytes
-  const int row = lane & 15, grp = lane >> 4;
-  // Byte offset of this lane's fragment for token tile 0, step 0.
-  const uint32_t base = (uint32_t)(((int64_t)row * ld + E * grp) * EB);
+  constexpr int KG = 2 * KS;  // K elements per group = 128 bytes per row
+  const int lrow = lane >> 3, lch = lane & 7;
+  const uint32_t ld_base = (uint32_t)((int64_t)lrow * ld * EB + lch * 16);
+  const uint32_t half_stride = (uint32_t)(8 * ld * EB);
   const uint32_t tile_stride = (uint32_t)(16 * ld * EB);
-  const int n_ks = d / KS;
+  const int wslot = lrow * 8 + (lch ^ lrow);
+  const int ri = lane & 15, rgrp = lane >> 4;
+  const int rslot0 = ri * 8 + (rgrp ^ (ri & 7));
+  const int rslot1 = ri * 8 + ((4 + rgrp) ^ (ri & 7));
+  const int n_g = d / KG;
 
-  i32x4 a_cur[TT], b_cur[NK];
+  // Token-row loads run PD groups ahead (HBM latency); the projection
+  // fragments (L2 resident) run one group ahead.
+  i32x4 abuf[PD][TT][2], bcur[2][NK], bnxt[2][NK];
+  auto issue = [&](int grp, i32x4 (&ab)[TT][2]) {
+    const uint32_t off = ld_base + (uint32_t)grp * 128u;
 #pragma unroll
-  for (int tt = 0; tt < TT; ++tt) a_cur[tt] = load16_stream(rsrc, base + tt * tile_stride);
-#pragma unroll
-  for (int ct = 0; ct < NK; ++ct) b_cur[ct] = pk[ct * kWave + lane];
-
-  for (int ks = 0; ks < n_ks; ++ks) {
-    i32x4 a_nxt[TT], b_nxt[NK];
-    const bool more = ks + 1 < n_ks;
-    if (more) {
-      const uint32_t off = base + (uint32_t)((ks + 1) * KS * EB);
-#pragma unroll
-      for (int tt = 0; tt < TT; ++tt) a_nxt[tt] = load16_stream(rsrc, off + tt * tile_stride);
-#pragma unroll
-      for (int ct = 0; ct < NK; ++ct) b_nxt[ct] = pk[((ks + 1) * NK + ct) * kWave + lane];
+    for (int tt = 0; tt < TT; ++tt) {
+      ab[tt][0] = load16_stream(rsrc, off + tt * tile_stride);
+      ab[tt][1] = load16_stream(rsrc, off + tt * tile_stride + half_stride);
     }
+  };
+  auto issue_b = [&](int grp, i32x4 (&bb)[2][NK]) {
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt)
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
-      for (int ct = 0; ct < NK; ++ct) acc[tt][ct] = mma16(Tag{}, a_cur[tt], b_cur[ct], acc[tt][ct]);
-    if (more) {
+      for (int ct = 0; ct < NK; ++ct) bb[s][ct] = pk[((2 * grp + s) * NK + ct) * kWave + lane];
+  };
 #pragma unroll
-      for (int tt = 0; tt < TT; ++tt) a_cur[tt] = a_nxt[tt];
+  for (int u = 0; u < PD - 1; ++u)
+    if (u < n_g) issue(u, abuf[u]);
+  issue_b(0, bcur);
+
+  for (int g0 = 0; g0 < n_g; g0 += PD) {
 #pragma unroll
-      for (int ct = 0; ct < NK; ++ct) b_cur[ct] = b_nxt[ct];
+    for (int u = 0; u < PD; ++u) {
+      const int grp = g0 + u;
+      if (grp + PD - 1 < n_g) issue(grp + PD - 1, abuf[(u + PD - 1) % PD]);
+      if (grp < n_g) {
+        if (grp + 1 < n_g) issue_b(grp + 1, bnxt);
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) {
+          xp[tt * 128 + wslot] = abuf[u][tt][0];
+          xp[tt * 128 + 64 + wslot] = abuf[u][tt][1];
+        }
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) {
+          const i32x4 f0 = xp[tt * 128 + rslot0];
+          const i32x4 f1 = xp[tt * 128 + rslot1];
+#pragma unroll
+          for (int ct = 0; ct < NK; ++ct) {
+            acc[tt][ct] = mma16(Tag{}, f0, bcur[0][ct], acc[tt][ct]);
+            acc[tt][ct] = mma16(Tag{}, f1, bcur[1][ct], acc[tt][ct]);
+          }
+        }
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+          for (int ct = 0; ct < NK; ++ct) bcur[s][ct] = bnxt[s][ct];
+      }
     }
   }
 }
@@ -187,6 +233,7 @@ __global__ __launch_bounds__(256) void project_main_kernel(
   if (t0 >= len) return;  // uniform over the workgroup
 
   const ProjTab md = tab[s];
+  __shared__ i32x4 xpose[4][TT * 128];
   // The wave index is uniform per wave; readfirstlane lets the compiler keep
   // everything derived from it (token range, buffer resources) in SGPRs.
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -218,8 +265,9 @@ __global__ __launch_bounds__(256) void project_main_kernel(
         At[tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
         Gt[tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
-    project_side<Tag, E, NK, TT>(ra, md.lda, md.d_in, pkS, lane, At);
-    project_side<Tag, E, NK, TT>(rg, md.ldg, md.d_out, pkR, lane, Gt);
+    i32x4* xp = &xpose[wave][0];
+    project_side<Tag, E, NK, TT, Tiles<NK>::PD>(ra, md.lda, md.d_in, pkS, lane, xp, At);
+    project_side<Tag, E, NK, TT, Tiles<NK>::PD>(rg, md.ldg, md.d_out, pkR, lane, xp, Gt);
 
     // P[r][c] += sum_tokens Gt[token][r] * At[token][c]; register q of the
     // stage-1 tiles holds token 4 * (lane / 16) + q, column lane % 16.
@@ -299,7 +347,7 @@ __global__ __launch_bounds__(256) void project_reduce_kernel(
 }  // namespace
 
 int project_chunk_tokens(int nk) {
-  return 64 * (nk == 1 ? 4 : (nk == 2 ? 2 : 1));
+  return 64 * (nk == 1 ? ATTR_PROJ_TT1 : (nk == 2 ? 2 : 1));
 }
 
 size_t project_packed_bytes(int64_t d_in, int64_t d_out, int k, int elem_bytes) {

@@ -58,8 +58,9 @@ def test_project_validation(L):
     assert _project(L, [_mod()], k=24) == UNSUPPORTED
     assert _project(L, [_mod()], dtype=P.ATTR_F16) == UNSUPPORTED
     assert b"in_dtype" in L.attr_last_error()
-    assert _project(L, [_mod(d_in=48)]) == ALIGN                   # not a multiple of 32 (bf16)
-    assert _project(L, [_mod(d_in=48)], dtype=P.ATTR_F32) != ALIGN   # fine for fp32 (16)
+    assert _project(L, [_mod(d_in=96)]) == ALIGN                   # not a multiple of 64 (bf16)
+    assert _project(L, [_mod(d_in=96)], dtype=P.ATTR_F32) != ALIGN   # fine for fp32 (32)
+    assert _project(L, [_mod(d_in=48)], dtype=P.ATTR_F32) == ALIGN
     assert _project(L, [_mod(a=0)]) == INVALID
     assert _project(L, [_mod(a=FAKE + 2)]) == ALIGN
     assert _project(L, [_mod(lda=32)]) == INVALID

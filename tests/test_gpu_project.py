@@ -85,7 +85,7 @@ def _random_modules(shapes, n, T, k, dtype, seed, lengths=None):
 def test_ragged_lengths_nan_padding(dtype, k):
     n, T = 7, 300                     # T spans two 256-token chunks, not a multiple of 16
     lengths = [0, 1, 17, 255, 256, 257, 300]
-    shapes = [(64, 96), (128, 32), (32, 64)]
+    shapes = [(64, 192), (128, 64), (64, 128)]
     say(f"case: ragged dtype={dtype} k={k} n={n} T={T}")
     mods = _random_modules(shapes, n, T, k, dtype, seed=100 + k, lengths=lengths)
     got = _run_project(mods, k, n, T, length=lengths, dtype=dtype)
@@ -100,7 +100,7 @@ def test_ragged_lengths_nan_padding(dtype, k):
 def test_untouched_columns_and_row_offset():
     n, T, k = 5, 40, 16
     say("case: row_offset packed layout, extra output columns")
-    shapes = [(96, 64), (64, 128)]
+    shapes = [(192, 64), (64, 128)]
     lengths = [40, 3, 0, 33, 16]
     # packed rows: example i starts at row_offset[i]; rows between are garbage
     row_offset = [0, 50, 60, 61, 120]
