@@ -182,9 +182,10 @@ attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows
  * written to memory (exact top-k lookup, section "Attribution Pipelines").
  *
  *   Q, ldq       device [n_q, D];  G, ldg: device [n_g, D]; both `dtype`
- *                (ATTR_F16 or ATTR_F32); D multiple of 32
- *   k            1..256
- *   index_base   added to the local row index j (store offset of G)
+ *                (ATTR_F16 or ATTR_F32); D a multiple of 64 (fp16) or 32
+ *                (fp32); n_q, n_g below 2^31
+ *   k            1..128
+ *   index_base   added to the local row index j (store offset of G), >= 0
  *   merge        0: overwrite top_*;  1: top_* hold a previous sorted
  *                result which is merged with this chunk (streaming over
  *                stores larger than one call)

@@ -336,23 +336,79 @@ attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows
 }
 
 // ---------------------------------------------------------------------------
+struct ScoreLayout {
+  size_t off_s, off_i, total;
+};
+
+static ScoreLayout score_layout(int64_t n_q, int64_t n_g, int32_t k) {
+  ScoreLayout L{0, 0, 0};
+  if (n_q <= 0 || n_g <= 0) return L;
+  int parts = attr::score_parts(n_q, n_g);
+  const int64_t rpp = attr::score_rows_per_part(n_g, parts);
+  parts = (int)((n_g + rpp - 1) / rpp);
+  const size_t n = (size_t)n_q * (size_t)parts * (size_t)k;
+  L.off_s = 0;
+  L.off_i = align_up(n * sizeof(float));
+  L.total = L.off_i + align_up(n * sizeof(int64_t));
+  return L;
+}
+
 size_t attr_score_topk_workspace_size(int64_t n_q, int64_t n_g, int64_t D, int32_t k) {
-  (void)n_q;
-  (void)n_g;
   (void)D;
-  (void)k;
-  return 0;
+  if (n_q < 0 || n_g < 0 || k < 1 || k > 128) return 0;
+  return score_layout(n_q, n_g, k).total;
 }
 
 attr_status attr_score_topk(const void* Q, int64_t n_q, int64_t ldq, const void* G, int64_t n_g,
                             int64_t ldg, attr_dtype dtype, int64_t D, int32_t k, int64_t index_base,
                             int32_t merge, float* top_score, int64_t* top_index, void* ws,
                             size_t ws_bytes, void* stream) {
-  (void)Q; (void)n_q; (void)ldq; (void)G; (void)n_g; (void)ldg; (void)dtype; (void)D; (void)k;
-  (void)index_base; (void)merge; (void)top_score; (void)top_index; (void)ws; (void)ws_bytes;
-  (void)stream;
-  g_err.clear();
-  return fail(ATTR_ERR_UNSUPPORTED, "attr_score_topk is not built in this library");
+  try {
+    g_err.clear();
+    if (dtype != ATTR_F16 && dtype != ATTR_F32)
+      return fail(ATTR_ERR_UNSUPPORTED, "attr_score_topk: dtype must be ATTR_F16 or ATTR_F32");
+    if (k < 1 || k > 128) return fail(ATTR_ERR_UNSUPPORTED, "attr_score_topk: k=%d must be in [1, 128]", k);
+    if (n_q < 0 || n_g < 0) return fail(ATTR_ERR_INVALID_ARG, "n_q / n_g is negative");
+    if (n_q > (1ll << 31) - 1 || n_g > (1ll << 31) - 1)
+      return fail(ATTR_ERR_UNSUPPORTED, "n_q and n_g must be below 2^31 per call");
+    if (D < 1) return fail(ATTR_ERR_INVALID_ARG, "D must be >= 1");
+    const int eb = dtype_bytes(dtype);
+    const int grp = dtype == ATTR_F16 ? 64 : 32;
+    if (D % grp) return fail(ATTR_ERR_ALIGNMENT, "D=%lld must be a multiple of %d", (long long)D, grp);
+    if (ldq < D || ldg < D) return fail(ATTR_ERR_INVALID_ARG, "ldq/ldg < D");
+    if (ldq % (16 / eb) || ldg % (16 / eb))
+      return fail(ATTR_ERR_ALIGNMENT, "ldq/ldg must keep rows 16-byte aligned");
+    if (ldq * 64 * eb >= (1ll << 31) || ldg * 32 * eb >= (1ll << 31))
+      return fail(ATTR_ERR_UNSUPPORTED, "row stride too large");
+    if (merge != 0 && merge != 1) return fail(ATTR_ERR_INVALID_ARG, "merge must be 0 or 1");
+    if (index_base < 0 || index_base > (1ll << 62))
+      return fail(ATTR_ERR_INVALID_ARG, "index_base must be in [0, 2^62]");
+    if (n_q > 0 && (!Q || !top_score || !top_index))
+      return fail(ATTR_ERR_INVALID_ARG, "Q / top_score / top_index is NULL");
+    if (n_g > 0 && !G) return fail(ATTR_ERR_INVALID_ARG, "G is NULL");
+    if (!aligned16(Q) || !aligned16(G) || !aligned16(top_score) || !aligned16(top_index))
+      return fail(ATTR_ERR_ALIGNMENT, "Q, G, top_score and top_index must be 16-byte aligned");
+    const Span ss = span_of(top_score, n_q, k, k, 4), si = span_of(top_index, n_q, k, k, 8);
+    const Span sq = span_of(Q, n_q, D, ldq, eb), sg = span_of(G, n_g, D, ldg, eb);
+    if (overlap(ss, si) || overlap(ss, sq) || overlap(ss, sg) || overlap(si, sq) || overlap(si, sg))
+      return fail(ATTR_ERR_INVALID_ARG, "top_score / top_index overlap each other or the inputs");
+    if (n_q == 0) return ATTR_OK;
+    if (n_g == 0 && merge) return ATTR_OK;
+    const ScoreLayout L = score_layout(n_q, n_g, k);
+    if (L.total > 0 && (!ws || ws_bytes < L.total))
+      return fail(ATTR_ERR_WORKSPACE, "attr_score_topk needs %zu workspace bytes", L.total);
+    if (reinterpret_cast<uintptr_t>(ws) & 255u)
+      return fail(ATTR_ERR_ALIGNMENT, "workspace must be 256-byte aligned");
+    char* base = static_cast<char*>(ws);
+    hipError_t e = attr::launch_score_topk(
+        dtype == ATTR_F16, Q, n_q, ldq, G, n_g, ldg, D, k, index_base, merge, top_score, top_index,
+        base ? reinterpret_cast<float*>(base + L.off_s) : nullptr,
+        base ? reinterpret_cast<int64_t*>(base + L.off_i) : nullptr, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return device_fail(e, "attr_score_topk launch");
+    return ATTR_OK;
+  } catch (...) {
+    return fail(ATTR_ERR_INVALID_ARG, "attr_score_topk: host exception");
+  }
 }
 
 }  // extern "C"

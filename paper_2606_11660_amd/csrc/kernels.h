@@ -70,4 +70,14 @@ int colsumsq_panels(int64_t n_rows, int64_t D);
 hipError_t launch_colsumsq(int x_dtype, const void* X, int64_t ldx, int64_t n_rows,
                            int64_t D, float* H, double* part, hipStream_t s);
 
+// ---------------------------------------------------------------------------
+// scoring
+// ---------------------------------------------------------------------------
+int score_parts(int64_t n_q, int64_t n_g);
+int64_t score_rows_per_part(int64_t n_g, int parts);
+hipError_t launch_score_topk(bool f16, const void* Q, int64_t n_q, int64_t ldq, const void* G,
+                             int64_t n_g, int64_t ldg, int64_t D, int k, int64_t index_base,
+                             int merge, float* top_s, int64_t* top_i, float* part_s,
+                             int64_t* part_i, hipStream_t s);
+
 }  // namespace attr

@@ -31,3 +31,41 @@ def row_rel_l2(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
     den = np.linalg.norm(ref, axis=1)
     out = np.where(den > 0, num / np.where(den > 0, den, 1.0), num)
     return out
+
+
+def check_topk(got_s, got_i, ref_scores, k, index_base=0, tol=1e-3):
+    """Top-k parity against the oracle's full fp64 score matrix.
+
+    (a) every returned score is within tol of the oracle's score of the
+        returned index and of the oracle's score at that rank;
+    (b) every oracle item scoring above s_{k+1} + tol is returned;
+    (c) the index at rank r equals the oracle's wherever the oracle scores
+        are separated from both neighbours by more than tol;
+    (d) returned indices are unique and scores non-increasing.
+    """
+    got_s = np.asarray(got_s, dtype=np.float64)
+    got_i = np.asarray(got_i, dtype=np.int64)
+    nq, ng = ref_scores.shape
+    for q in range(nq):
+        ref = ref_scores[q]
+        order = np.lexsort((np.arange(ng), -ref))
+        rs = ref[order]
+        kk = min(k, ng)
+        valid = got_i[q] >= 0
+        assert valid.sum() == kk, (q, valid.sum(), kk)
+        assert (got_i[q, kk:] == -1).all() and np.isneginf(got_s[q, kk:]).all()
+        gi = got_i[q, :kk] - index_base
+        gs = got_s[q, :kk]
+        assert len(set(gi.tolist())) == kk, "duplicate indices"
+        assert (np.diff(gs) <= 0).all(), "scores not sorted"
+        assert (gi >= 0).all() and (gi < ng).all()
+        assert np.abs(gs - ref[gi]).max() <= tol, (q, np.abs(gs - ref[gi]).max())
+        assert np.abs(gs - rs[:kk]).max() <= tol
+        s_next = rs[kk] if ng > kk else -np.inf
+        must = order[:kk][rs[:kk] > s_next + tol]
+        assert set(must.tolist()) <= set(gi.tolist()), (q, "missing a clear winner")
+        for r in range(kk):
+            left = rs[r - 1] - rs[r] if r > 0 else np.inf
+            right = rs[r] - rs[r + 1] if r + 1 < ng else np.inf
+            if left > tol and right > tol:
+                assert gi[r] == order[r], (q, r, gi[r], order[r])

@@ -115,3 +115,33 @@ def test_error_message_is_thread_local_and_cleared(L):
     assert L.attr_last_error() != b""
     assert _project(L, [_mod()], n=0) == OK
     assert L.attr_last_error() == b""
+
+
+def test_score_validation(L):
+    sc = L.attr_score_topk
+    G = FAKE + (1 << 32)
+    TS, TI = FAKE + (2 << 32), FAKE + (3 << 32)
+    args = dict(Q=FAKE, nq=4, ldq=128, G=G, ng=100, ldg=128, dt=P.ATTR_F16, D=128, k=10,
+                base=0, merge=0, ts=TS, ti=TI, ws=None, wsb=0)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return sc(a["Q"], a["nq"], a["ldq"], a["G"], a["ng"], a["ldg"], a["dt"], a["D"], a["k"],
+                  a["base"], a["merge"], a["ts"], a["ti"], a["ws"], a["wsb"], None)
+    assert call(dt=P.ATTR_BF16) == UNSUPPORTED
+    assert call(k=0) == UNSUPPORTED and call(k=129) == UNSUPPORTED
+    assert call(D=96) == ALIGN                       # fp16 needs multiples of 64
+    assert call(D=96, dt=P.ATTR_F32, ldq=96, ldg=96) == WORKSPACE   # fp32: multiples of 32 are fine
+    assert call(ldq=64) == INVALID
+    assert call(nq=-1) == INVALID
+    assert call(merge=2) == INVALID
+    assert call(base=-5) == INVALID
+    assert call(ts=FAKE + 256) == INVALID            # output inside Q
+    assert call(ti=TS + 16) == INVALID               # outputs overlap
+    assert call(G=0) == INVALID
+    assert call() == WORKSPACE
+    need = L.attr_score_topk_workspace_size(4, 100, 128, 10)
+    assert need > 0
+    assert call(ws=FAKE + (4 << 32) + 16, wsb=need) == ALIGN
+    assert call(nq=0) == OK
+    assert call(ng=0, merge=1) == OK

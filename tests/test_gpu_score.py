@@ -1,0 +1,137 @@
+"""GPU parity of attr_score_topk (and the tiny end-to-end pipeline) against
+the fp64 oracle: scores within 1e-3, indices exact wherever the score gaps
+exceed 1e-3, ties ordered by index, padding (-inf, -1)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2606_11660_amd as P
+import synth
+from tests._util import check_topk, dev, host, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _topk(Q, G, k, index_base=0, merge=False, prev=None):
+    nq = Q.shape[0]
+    if prev is None:
+        ts = torch.full((nq, k), 5.0, dtype=torch.float32, device="cuda")
+        ti = torch.full((nq, k), 7, dtype=torch.int64, device="cuda")
+    else:
+        ts, ti = prev
+    P.attr_score_topk(Q, G, k, ts, ti, index_base=index_base, merge=merge)
+    torch.cuda.synchronize()
+    return ts, ti
+
+
+def test_tiny_pipeline_end_to_end():
+    """Tiny workload: project (fp32) -> unit-normalise -> score 8 queries -> top-5."""
+    say("case: tiny end-to-end")
+    x = synth.tiny_inputs()
+    k = 16
+
+    def rows(a, g, n):
+        out = torch.empty((n, k * k), dtype=torch.float32, device="cuda")
+        m = [P.Module(dev(a.reshape(-1, 64)), dev(g.reshape(-1, 64)), dev(x["R"]), dev(x["S"]), 0)]
+        P.attr_project(m, k, n, 32, out)
+        y = torch.empty_like(out)
+        P.attr_precond_apply(out, P.PRECOND_NONE, None, True, y)
+        return y
+
+    G = rows(x["a"], x["g"], 256)
+    Q = rows(x["aq"], x["gq"], 8)
+    ts, ti = _topk(Q, G, 5)
+    Gr = O.unit_normalize(O.project(x["a"], x["g"], x["R"], x["S"]))
+    Qr = O.unit_normalize(O.project(x["aq"], x["gq"], x["R"], x["S"]))
+    check_topk(host(ts), host(ti), O.scores(Qr, Gr), 5)
+    rs, ri = O.score_topk(Qr, Gr, 5)
+    assert np.abs(host(ts) - rs).max() <= 1e-5
+
+
+@pytest.mark.parametrize("k", [1, 10, 100])
+def test_random_unit_rows_f16(k):
+    nq, ng, D = 70, 1000, 128            # two query blocks, ragged store tile
+    say(f"case: random fp16 nq={nq} ng={ng} D={D} k={k}")
+    Q = synth.unit_rows(nq, D, seed=11)
+    G = synth.unit_rows(ng, D, seed=12)
+    ts, ti = _topk(dev(Q), dev(G), k, index_base=1000)
+    check_topk(host(ts), host(ti), O.scores(Q, G), k, index_base=1000)
+
+
+def test_exact_ties_index_order_and_self_cosine():
+    say("case: duplicates / ties")
+    D = 64
+    base = synth.unit_rows(40, D, seed=13)
+    G = np.concatenate([base, base[:10], base[5:15]])     # rows 40..59 duplicate rows 0..14
+    Q = base[:12]
+    ts, ti = _topk(dev(Q), dev(G), 3)
+    ref_s, ref_i = O.score_topk(Q, G, 3)
+    gi = host(ti)
+    # the top entries are exact duplicates of the query: equal scores, index ascending
+    np.testing.assert_array_equal(gi, ref_i)
+    assert np.abs(host(ts) - ref_s).max() <= 1e-3
+    assert np.abs(host(ts)[:, 0] - 1.0).max() <= 2e-3      # self-cosine
+
+
+def test_symmetric_scores_f32():
+    say("case: Q == G symmetric, fp32")
+    X = synth.unit_rows(96, 256, seed=14, dtype=np.float32)
+    ts, ti = _topk(dev(X), dev(X), 96)
+    S = np.full((96, 96), np.nan)
+    for q in range(96):
+        S[q, host(ti)[q]] = host(ts)[q]
+    np.testing.assert_allclose(S, S.T, atol=1e-6)
+    np.testing.assert_allclose(np.diag(S), 1.0, atol=1e-5)
+
+
+def test_merge_chunks_equals_single_call():
+    say("case: merge chunks")
+    nq, ng, D, k = 33, 3000, 192, 20
+    Q = synth.unit_rows(nq, D, seed=15)
+    G = synth.unit_rows(ng, D, seed=16)
+    G[2500] = G[100]                   # tie across chunks
+    Qd, Gd = dev(Q), dev(G)
+    s1, i1 = _topk(Qd, Gd, k)
+    ts = torch.empty((nq, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((nq, k), dtype=torch.int64, device="cuda")
+    P.attr_score_topk(Qd, Gd[:0], k, ts, ti, merge=False)     # empty store -> padding
+    torch.cuda.synchronize()
+    assert (host(ti) == -1).all() and np.isneginf(host(ts)).all()
+    for lo in range(0, ng, 700):
+        hi = min(ng, lo + 700)
+        P.attr_score_topk(Qd, Gd[lo:hi], k, ts, ti, index_base=lo, merge=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(ti), host(i1))
+    np.testing.assert_array_equal(host(ts), host(s1))
+    check_topk(host(ts), host(ti), O.scores(Q, G), k)
+
+
+def test_fewer_rows_than_k():
+    say("case: n_g < k")
+    Q = synth.unit_rows(5, 64, seed=17)
+    G = synth.unit_rows(7, 64, seed=18)
+    ts, ti = _topk(dev(Q), dev(G), 12)
+    check_topk(host(ts), host(ti), O.scores(Q, G), 12)
+
+
+def test_planted_near_duplicates():
+    say("case: planted near-duplicates D=8192")
+    ng, D, nq = 20000, 8192, 64
+    G = synth.unit_rows(ng, D, seed=19)
+    targets = np.random.default_rng(4).choice(ng, 16, replace=False)
+    Q = synth.planted_queries(G[targets], targets, nq)
+    ts, ti = _topk(dev(Q), dev(G), 100)
+    gi, gs = host(ti), host(ts)
+    assert (gi[:16, 0] == targets).all()
+    assert np.abs(gs[:16, 0] - 0.9).max() <= 2e-3
+    check_topk(gs, gi, O.scores(Q, G), 100)
+
+
+def test_gpt2_store_scan():
+    """GPT-2-shaped scoring: 64 queries x 4096 store rows x 12288 dims, top-10."""
+    say("case: gpt2 store scan")
+    Q = synth.unit_rows(64, 12288, seed=21)
+    G = synth.unit_rows(4096, 12288, seed=22)
+    ts, ti = _topk(dev(Q), dev(G), 10)
+    check_topk(host(ts), host(ti), O.scores(Q, G), 10)
