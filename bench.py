@@ -1,0 +1,209 @@
+"""Throughput of the attribution hot path on one MI355X.
+
+Workload (GPT-2-shaped gradient store build + on-the-fly scoring): 12 layers
+x 4 linear modules (qkv 768->2304, out 768->768, up 768->3072, down
+3072->768), 512 tokens per example, k = 16 per module (12288 dims per row),
+fp16 store, 64 query rows with top-10.  One step is one batch of 64
+examples through the whole path:
+
+  attr_project        (bf16 token rows resident in HBM -> fp32 rows)
+  attr_precond_apply  (unit-normalise, cast to the fp16 store slot)
+  attr_score_topk     (64 queries x the 64 new rows, merged into the
+                       running top-10 of the store built so far)
+
+`value` is examples/s over the timed steps.  The dominant kernel is the
+projection; its roofline entry uses the algorithmic bytes of one call
+(every a/g element once, R/S once, the fp32 output row) over the average
+call duration measured with HIP events on the bench stream.  After the timed
+steps the finished store is scanned once more (64 queries x 4096 rows) and
+reported under `store_scan`.  `cpu_baseline` times the fp64 oracle on a
+sample of examples on the host cores.
+
+Usage: python bench.py [--gpus 1] [--steps 64] [--warmup 3]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+BATCH = 64
+
+
+def _cpu_baseline(n_sample: int = 6, min_seconds: float = 12.0):
+    """Time the fp64 oracle on GPT-2-shaped examples on the host: project all
+    48 modules, unit-normalise, score against the 64 queries.  n_sample
+    examples are generated once (not timed) and passed through the oracle
+    repeatedly until min_seconds of CPU work have been timed."""
+    import numpy as np
+    import oracle as O
+    import synth
+    wl = synth.GPT2
+    pairs = [synth.projection_pair(wl, m) for m in range(len(wl.modules))]
+    ex = [[synth.module_example(wl, m, i) for m in range(len(wl.modules))] for i in range(n_sample)]
+    qrows = synth.unit_rows(wl.n_queries, wl.D, seed=21)
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([int(d.get("num_threads", 1)) for d in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    done, passes = 0, 0
+    t0 = time.perf_counter()
+    while True:
+        rows = []
+        for i in range(n_sample):
+            blocks = [O.project(ex[i][m][0][None], ex[i][m][1][None], pairs[m][0], pairs[m][1])
+                      for m in range(len(wl.modules))]
+            rows.append(O.project_concat(blocks)[0])
+        U = O.to_f16(O.unit_normalize(np.stack(rows)))
+        O.score_topk(qrows, U, wl.topk)
+        done += n_sample
+        passes += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    return {"value": done / dt, "unit": "examples/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n_sample} seeded GPT-2-shaped examples (48 modules x 512 tokens, bf16) "
+                      f"through the fp64 oracle {passes} times: project, unit-normalise, score "
+                      f"against 64 queries; {dt:.1f} s timed"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the store shards by rows; see the design notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2606_11660_amd as P
+    import synth
+
+    wl = synth.GPT2
+    k, T, B, D = wl.k, wl.T, BATCH, wl.D
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream(device=dev)
+
+    # ---------------- setup (not timed) ----------------
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    mods = []
+    for m, md in enumerate(wl.modules):
+        a = torch.empty((B * T, md.d_in), dtype=torch.bfloat16, device=dev)
+        g = torch.empty((B * T, md.d_out), dtype=torch.bfloat16, device=dev)
+        a.copy_(torch.randn(a.shape, generator=gen, device=dev))
+        g.copy_(torch.randn(g.shape, generator=gen, device=dev) * wl.g_scale)
+        R, S = synth.projection_pair(wl, m)
+        Rt = torch.from_numpy(R.view(np.int16)).view(torch.bfloat16).to(dev)
+        St = torch.from_numpy(S.view(np.int16)).view(torch.bfloat16).to(dev)
+        mods.append(P.Module(a, g, Rt, St, m * k * k))
+    n_store = max(args.steps, 1) * B
+    store = torch.empty((n_store, D), dtype=torch.float16, device=dev)
+    rows32 = torch.empty((B, D), dtype=torch.float32, device=dev)
+    Qrows = torch.empty((wl.n_queries, D), dtype=torch.float16, device=dev)
+    top_s = torch.empty((wl.n_queries, wl.topk), dtype=torch.float32, device=dev)
+    top_i = torch.empty((wl.n_queries, wl.topk), dtype=torch.int64, device=dev)
+    ws_p, ws_a, ws_s = P.Workspace(dev), P.Workspace(dev), P.Workspace(dev)
+    with torch.cuda.stream(stream):
+        # query rows: the processed rows of the first batch
+        P.attr_project(mods, k, B, T, rows32, ws=ws_p, stream=stream)
+        P.attr_precond_apply(rows32, P.PRECOND_NONE, None, True, Qrows[:B], ws=ws_a, stream=stream)
+    stream.synchronize()
+
+    def step(i):
+        slot = store[(i % (n_store // B)) * B:((i % (n_store // B)) + 1) * B]
+        P.attr_project(mods, k, B, T, rows32, ws=ws_p, stream=stream)
+        P.attr_precond_apply(rows32, P.PRECOND_NONE, None, True, slot, ws=ws_a, stream=stream)
+        P.attr_score_topk(Qrows, slot, wl.topk, top_s, top_i, index_base=(i % (n_store // B)) * B,
+                          merge=i > 0, ws=ws_s, stream=stream)
+
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            step(i)
+    stream.synchronize()
+    torch.cuda.synchronize()
+
+    # ---------------- timed region ----------------
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        for i in range(args.steps):
+            slot = store[i * B:(i + 1) * B]
+            ev[i][0].record(stream)
+            P.attr_project(mods, k, B, T, rows32, ws=ws_p, stream=stream)
+            ev[i][1].record(stream)
+            P.attr_precond_apply(rows32, P.PRECOND_NONE, None, True, slot, ws=ws_a, stream=stream)
+            P.attr_score_topk(Qrows, slot, wl.topk, top_s, top_i, index_base=i * B, merge=i > 0,
+                              ws=ws_s, stream=stream)
+    stream.synchronize()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    proj_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+    # ---------------- full store scan (reported separately) ----------------
+    scan_ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    with torch.cuda.stream(stream):
+        P.attr_score_topk(Qrows, store, wl.topk, top_s, top_i, ws=ws_s, stream=stream)
+        scan_ev[0].record(stream)
+        reps = 10
+        for _ in range(reps):
+            P.attr_score_topk(Qrows, store, wl.topk, top_s, top_i, ws=ws_s, stream=stream)
+        scan_ev[1].record(stream)
+    stream.synchronize()
+    scan_ms = scan_ev[0].elapsed_time(scan_ev[1]) / reps
+    scan_bytes = n_store * D * 2 + wl.n_queries * D * 2
+
+    # algorithmic bytes of one projection call: a/g rows once, R/S once, fp32 rows out
+    per_example = T * wl.elems_per_token() * 2 + D * 4
+    rs_bytes = sum((md.d_in + md.d_out) * k * 2 for md in wl.modules)
+    proj_bytes = B * per_example + rs_bytes
+    achieved = proj_bytes / (proj_ms * 1e-3) / 1e9
+
+    result = {
+        "metric": "projected per-example grads/sec; score pairs/sec + HBM GB/s on store scan",
+        "value": args.steps * B / elapsed,
+        "unit": "examples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded device fill; R, S from the seeded host generator)",
+        "config": {"workload": "gpt2-shaped store build: 12 layers x (qkv 768->2304, out 768->768, "
+                               "up 768->3072, down 3072->768), T=512, k=16, D=12288, "
+                               "batch 64 per step, fp16 store, 64 queries top-10 merged per step",
+                   "global_batch": B, "seq_len": T, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "attr_project (project_main_kernel<bf16,k=16>)",
+                     "bytes_per_launch": proj_bytes, "ms_per_launch": proj_ms},
+        "store_scan": {"queries": wl.n_queries, "rows": n_store, "D": D, "k": wl.topk,
+                       "ms": scan_ms, "pairs_per_s": wl.n_queries * n_store / (scan_ms * 1e-3),
+                       "GBps": scan_bytes / (scan_ms * 1e-3) / 1e9},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = _cpu_baseline()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -240,10 +240,12 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
 size_t attr_precond_accumulate_workspace_size(int64_t n_rows, int64_t D, attr_dtype x_dtype,
                                               attr_precond mode) {
   (void)x_dtype;
-  if (n_rows < 0 || D < 1) return 0;
-  if (mode == ATTR_PRECOND_DIAG) {
-    if (n_rows == 0) return 0;
+  if (n_rows <= 0 || D < 1) return 0;
+  if (mode == ATTR_PRECOND_DIAG)
     return align_up((size_t)attr::colsumsq_panels(n_rows, D) * (size_t)D * sizeof(double));
+  if (mode == ATTR_PRECOND_FULL) {
+    const attr::SyrkPlan P = attr::plan_syrk(n_rows, D);
+    return align_up(P.xt_bytes) + align_up(P.part_bytes) + align_up(P.h64_bytes);
   }
   return 0;
 }
@@ -256,8 +258,9 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
     if (mode != ATTR_PRECOND_DIAG && mode != ATTR_PRECOND_FULL)
       return fail(ATTR_ERR_UNSUPPORTED, "attr_precond_accumulate: mode must be DIAG or FULL");
     if (!valid_dtype(x_dtype)) return fail(ATTR_ERR_UNSUPPORTED, "unknown x_dtype");
-    if (mode == ATTR_PRECOND_FULL)
-      return fail(ATTR_ERR_UNSUPPORTED, "attr_precond_accumulate: FULL mode is not built in this library");
+    const bool full = mode == ATTR_PRECOND_FULL;
+    if (full && x_dtype == ATTR_F32)
+      return fail(ATTR_ERR_UNSUPPORTED, "attr_precond_accumulate: FULL takes ATTR_F16 or ATTR_BF16 rows");
     if (n_rows < 0) return fail(ATTR_ERR_INVALID_ARG, "n_rows is negative");
     if (D < 1) return fail(ATTR_ERR_INVALID_ARG, "D must be >= 1");
     if (D % 8) return fail(ATTR_ERR_ALIGNMENT, "D=%lld must be a multiple of 8", (long long)D);
@@ -267,7 +270,9 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
     if (!H) return fail(ATTR_ERR_INVALID_ARG, "H is NULL");
     if (n_rows > 0 && !X) return fail(ATTR_ERR_INVALID_ARG, "X is NULL");
     if (!aligned16(X) || !aligned16(H)) return fail(ATTR_ERR_ALIGNMENT, "X and H must be 16-byte aligned");
-    if (overlap(span_of(X, n_rows, D, ldx, eb), span_of(H, 1, D, D, 4)))
+    if (full && D % 64) return fail(ATTR_ERR_ALIGNMENT, "FULL needs D a multiple of 64");
+    if (full && D > 32768) return fail(ATTR_ERR_UNSUPPORTED, "FULL needs D <= 32768");
+    if (overlap(span_of(X, n_rows, D, ldx, eb), span_of(H, full ? D : 1, D, D, 4)))
       return fail(ATTR_ERR_INVALID_ARG, "X and H overlap");
     if (n_rows == 0) return ATTR_OK;
     const size_t need = attr_precond_accumulate_workspace_size(n_rows, D, x_dtype, mode);
@@ -276,8 +281,19 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
     if (reinterpret_cast<uintptr_t>(ws) & 255u)
       return fail(ATTR_ERR_ALIGNMENT, "workspace must be 256-byte aligned");
     if (n_rows > (1ll << 40)) return fail(ATTR_ERR_UNSUPPORTED, "n_rows too large");
-    hipError_t e = attr::launch_colsumsq((int)x_dtype, X, ldx, n_rows, D, H,
-                                         static_cast<double*>(ws), static_cast<hipStream_t>(stream));
+    hipError_t e;
+    if (full) {
+      const attr::SyrkPlan P = attr::plan_syrk(n_rows, D);
+      char* b = static_cast<char*>(ws);
+      char* xt = b;
+      char* part = xt + align_up(P.xt_bytes);
+      char* h64 = part + align_up(P.part_bytes);
+      e = attr::launch_syrk(x_dtype == ATTR_BF16, X, ldx, n_rows, D, H, P, xt, part, h64,
+                            static_cast<hipStream_t>(stream));
+    } else {
+      e = attr::launch_colsumsq((int)x_dtype, X, ldx, n_rows, D, H, static_cast<double*>(ws),
+                                static_cast<hipStream_t>(stream));
+    }
     if (e != hipSuccess) return device_fail(e, "attr_precond_accumulate launch");
     return ATTR_OK;
   } catch (...) {
@@ -287,26 +303,23 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
 
 // ---------------------------------------------------------------------------
 size_t attr_precond_apply_workspace_size(int64_t n_rows, int64_t D, attr_precond mode) {
-  (void)n_rows;
-  (void)D;
-  (void)mode;
-  return 0;
+  if (mode != ATTR_PRECOND_FULL || n_rows <= 0 || D < 1) return 0;
+  return attr::apply_full_workspace(n_rows, D, 1);
 }
 
 attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows, int64_t D,
                                int64_t ldx, attr_precond mode, const float* M,
                                int32_t unit_normalize, void* Y, attr_dtype y_dtype, int64_t ldy,
                                void* ws, size_t ws_bytes, void* stream) {
-  (void)ws;
-  (void)ws_bytes;
   try {
     g_err.clear();
     if (mode != ATTR_PRECOND_NONE && mode != ATTR_PRECOND_DIAG && mode != ATTR_PRECOND_FULL)
       return fail(ATTR_ERR_UNSUPPORTED, "unknown preconditioner mode");
     if ((x_dtype != ATTR_F32 && x_dtype != ATTR_F16) || (y_dtype != ATTR_F32 && y_dtype != ATTR_F16))
       return fail(ATTR_ERR_UNSUPPORTED, "attr_precond_apply: dtypes must be ATTR_F32 or ATTR_F16");
-    if (mode == ATTR_PRECOND_FULL)
-      return fail(ATTR_ERR_UNSUPPORTED, "attr_precond_apply: FULL mode is not built in this library");
+    const bool full = mode == ATTR_PRECOND_FULL;
+    if (full && x_dtype != ATTR_F16)
+      return fail(ATTR_ERR_UNSUPPORTED, "attr_precond_apply: FULL takes ATTR_F16 rows");
     if (n_rows < 0) return fail(ATTR_ERR_INVALID_ARG, "n_rows is negative");
     if (D < 1) return fail(ATTR_ERR_INVALID_ARG, "D must be >= 1");
     if (D % 8) return fail(ATTR_ERR_ALIGNMENT, "D=%lld must be a multiple of 8", (long long)D);
@@ -316,15 +329,31 @@ attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows
       return fail(ATTR_ERR_ALIGNMENT, "ldx/ldy must keep rows 16-byte aligned");
     if (n_rows > 0 && (!X || !Y)) return fail(ATTR_ERR_INVALID_ARG, "X or Y is NULL");
     if (mode == ATTR_PRECOND_DIAG && !M) return fail(ATTR_ERR_INVALID_ARG, "DIAG needs M");
+    if (full && !M) return fail(ATTR_ERR_INVALID_ARG, "FULL needs M");
+    if (full && D % 64) return fail(ATTR_ERR_ALIGNMENT, "FULL needs D a multiple of 64");
     if (mode == ATTR_PRECOND_NONE && M) return fail(ATTR_ERR_INVALID_ARG, "NONE takes M = NULL");
     if (!aligned16(X) || !aligned16(Y) || !aligned16(M))
       return fail(ATTR_ERR_ALIGNMENT, "X, Y and M must be 16-byte aligned");
     const Span sx = span_of(X, n_rows, D, ldx, xb), sy = span_of(Y, n_rows, D, ldy, yb);
     const bool inplace = X == Y && x_dtype == y_dtype && ldx == ldy;
     if (!inplace && overlap(sx, sy)) return fail(ATTR_ERR_INVALID_ARG, "X and Y overlap");
-    if (M && overlap(span_of(M, 1, D, D, 4), sy)) return fail(ATTR_ERR_INVALID_ARG, "M and Y overlap");
+    if (full && overlap(sx, sy)) return fail(ATTR_ERR_INVALID_ARG, "FULL cannot run in place");
+    if (M && overlap(span_of(M, full ? D : 1, D, D, 4), sy))
+      return fail(ATTR_ERR_INVALID_ARG, "M and Y overlap");
     if (n_rows == 0) return ATTR_OK;
     if (n_rows > (1ll << 31) - 1) return fail(ATTR_ERR_UNSUPPORTED, "n_rows exceeds one launch");
+    if (full) {
+      if (ldx * 256 * 2 >= (1ll << 31)) return fail(ATTR_ERR_UNSUPPORTED, "row stride too large");
+      const size_t need = attr::apply_full_workspace(n_rows, D, unit_normalize ? 1 : 0);
+      if (!ws || ws_bytes < need)
+        return fail(ATTR_ERR_WORKSPACE, "attr_precond_apply (FULL) needs %zu workspace bytes", need);
+      if (reinterpret_cast<uintptr_t>(ws) & 255u)
+        return fail(ATTR_ERR_ALIGNMENT, "workspace must be 256-byte aligned");
+      hipError_t e = attr::launch_apply_full(X, n_rows, ldx, D, M, (int)y_dtype, Y, ldy,
+                                             unit_normalize ? 1 : 0, ws, static_cast<hipStream_t>(stream));
+      if (e != hipSuccess) return device_fail(e, "attr_precond_apply (FULL) launch");
+      return ATTR_OK;
+    }
     hipError_t e = attr::launch_rowscale((int)x_dtype, (int)y_dtype, X, ldx, n_rows, D,
                                          mode == ATTR_PRECOND_DIAG ? M : nullptr, unit_normalize ? 1 : 0,
                                          nullptr, 0, Y, ldy, static_cast<hipStream_t>(stream));
@@ -337,26 +366,27 @@ attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows
 
 // ---------------------------------------------------------------------------
 struct ScoreLayout {
-  size_t off_s, off_i, total;
+  attr::ScorePlan plan;
+  size_t off_s, off_i, off_p, total;
 };
 
-static ScoreLayout score_layout(int64_t n_q, int64_t n_g, int32_t k) {
-  ScoreLayout L{0, 0, 0};
+static ScoreLayout score_layout(int64_t n_q, int64_t n_g, int64_t D, int32_t k, int eb) {
+  ScoreLayout L{};
+  L.plan = attr::plan_score(n_q, n_g, D, k, eb);
   if (n_q <= 0 || n_g <= 0) return L;
-  int parts = attr::score_parts(n_q, n_g);
-  const int64_t rpp = attr::score_rows_per_part(n_g, parts);
-  parts = (int)((n_g + rpp - 1) / rpp);
-  const size_t n = (size_t)n_q * (size_t)parts * (size_t)k;
+  const size_t n = L.plan.list_entries;
   L.off_s = 0;
   L.off_i = align_up(n * sizeof(float));
-  L.total = L.off_i + align_up(n * sizeof(int64_t));
+  L.off_p = L.off_i + align_up(n * sizeof(int64_t));
+  L.total = L.off_p + align_up(L.plan.spart_bytes);
   return L;
 }
 
 size_t attr_score_topk_workspace_size(int64_t n_q, int64_t n_g, int64_t D, int32_t k) {
-  (void)D;
-  if (n_q < 0 || n_g < 0 || k < 1 || k > 128) return 0;
-  return score_layout(n_q, n_g, k).total;
+  if (n_q < 0 || n_g < 0 || k < 1 || k > 128 || D < 1) return 0;
+  // the fp16 plan needs at least as much workspace as the fp32 plan
+  const ScoreLayout a = score_layout(n_q, n_g, D, k, 2), b = score_layout(n_q, n_g, D, k, 4);
+  return a.total > b.total ? a.total : b.total;
 }
 
 attr_status attr_score_topk(const void* Q, int64_t n_q, int64_t ldq, const void* G, int64_t n_g,
@@ -394,16 +424,17 @@ attr_status attr_score_topk(const void* Q, int64_t n_q, int64_t ldq, const void*
       return fail(ATTR_ERR_INVALID_ARG, "top_score / top_index overlap each other or the inputs");
     if (n_q == 0) return ATTR_OK;
     if (n_g == 0 && merge) return ATTR_OK;
-    const ScoreLayout L = score_layout(n_q, n_g, k);
+    const ScoreLayout L = score_layout(n_q, n_g, D, k, eb);
     if (L.total > 0 && (!ws || ws_bytes < L.total))
       return fail(ATTR_ERR_WORKSPACE, "attr_score_topk needs %zu workspace bytes", L.total);
     if (reinterpret_cast<uintptr_t>(ws) & 255u)
       return fail(ATTR_ERR_ALIGNMENT, "workspace must be 256-byte aligned");
     char* base = static_cast<char*>(ws);
     hipError_t e = attr::launch_score_topk(
-        dtype == ATTR_F16, Q, n_q, ldq, G, n_g, ldg, D, k, index_base, merge, top_score, top_index,
-        base ? reinterpret_cast<float*>(base + L.off_s) : nullptr,
-        base ? reinterpret_cast<int64_t*>(base + L.off_i) : nullptr, static_cast<hipStream_t>(stream));
+        dtype == ATTR_F16, L.plan, Q, n_q, ldq, G, n_g, ldg, k, index_base, merge, top_score,
+        top_index, base ? reinterpret_cast<float*>(base + L.off_s) : nullptr,
+        base ? reinterpret_cast<int64_t*>(base + L.off_i) : nullptr,
+        base ? reinterpret_cast<float*>(base + L.off_p) : nullptr, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return device_fail(e, "attr_score_topk launch");
     return ATTR_OK;
   } catch (...) {

@@ -1,0 +1,164 @@
+// Full second-moment preconditioner applied to store rows: y = M x for every
+// row x, with M = (G^T G / N)^{-1/2} (the flat autocorrelation / empirical
+// Fisher preconditioner of the method-family table), followed by unit
+// normalisation (section "Attribution Pipelines").
+//
+// M arrives in fp32.  Preparatory kernels find max|M| and split the scaled
+// matrix A = 2^s M (s chosen so that max|A| <= 2^15) into two fp16 matrices
+// on the same scale, A_hi = fp16(A) and A_lo = fp16(A - A_hi), so that
+// A_hi + A_lo equals A to about 22 significant bits: the preconditioner is
+// badly conditioned and an fp16 (or bf16) M alone perturbs the whitened
+// rows by percents.  Y = 2^-s X (A_hi + A_lo)^T is then one MFMA GEMM whose
+// K loop runs over A_hi and then over A_lo into the same fp32 accumulators;
+// the epilogue applies 2^-s, writes Y and per-row partial sums of squares
+// (from the fp32 values), which the row-scale kernel turns into the
+// unit-norm scale in a second pass.
+#include "common.h"
+#include "gemm.h"
+#include "kernels.h"
+
+namespace attr {
+namespace {
+
+// max|M| as the bit pattern of a non-negative float (integer order equals
+// float order there), so the reduction is exact and order independent.
+__global__ __launch_bounds__(256) void absmax_kernel(const float* __restrict__ M, int64_t n,
+                                                     unsigned int* __restrict__ out) {
+  float m = 0.f;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    m = fmaxf(m, fabsf(M[i]));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, kWave));
+  if ((threadIdx.x & 63) == 0) atomicMax(out, __float_as_uint(m));
+}
+
+__global__ void zero_word_kernel(unsigned int* p) { *p = 0u; }
+
+// exponent s with max|M| * 2^s <= 2^15 (0 for an all-zero M)
+__device__ inline int split_exponent(unsigned int maxbits) {
+  const float mx = __uint_as_float(maxbits);
+  if (!(mx > 0.f)) return 0;
+  int e;
+  frexpf(mx, &e);  // mx = f * 2^e, f in [0.5, 1)
+  return 15 - e;
+}
+
+__global__ __launch_bounds__(256) void split_m_kernel(const float* __restrict__ M, int64_t n,
+                                                      const unsigned int* __restrict__ maxbits,
+                                                      _Float16* __restrict__ hi,
+                                                      _Float16* __restrict__ lo) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const float a = ldexpf(M[i], split_exponent(*maxbits));
+  const _Float16 h = (_Float16)a;
+  hi[i] = h;
+  lo[i] = (_Float16)(a - (float)h);
+}
+
+template <typename YT>
+__device__ inline void store_y(YT* p, float v);
+template <>
+__device__ inline void store_y<float>(float* p, float v) {
+  *p = v;
+}
+template <>
+__device__ inline void store_y<_Float16>(_Float16* p, float v) {
+  *p = (_Float16)v;
+}
+
+template <typename YT>
+__global__ __launch_bounds__(256) void apply_full_kernel(
+    const _Float16* __restrict__ X, int64_t n_rows, int64_t ldx, int64_t D,
+    const _Float16* __restrict__ Mhi, const _Float16* __restrict__ Mlo,
+    const unsigned int* __restrict__ maxbits, YT* __restrict__ Y, int64_t ldy,
+    float* __restrict__ rowss, int n_ss, int n_tn) {
+  __shared__ GemmSmem sm;
+  const int tn = (int)(blockIdx.x % (uint32_t)n_tn);
+  const int64_t tm = blockIdx.x / (uint32_t)n_tn;
+  const int64_t r0 = tm * GT, c0 = (int64_t)tn * GT;
+  int64_t nr = n_rows - r0;
+  nr = nr > GT ? GT : nr;
+  int64_t nc = D - c0;
+  nc = nc > GT ? GT : nc;
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + r0 * ldx, (uint32_t)(nr * ldx * 2));
+  const __amdgpu_buffer_rsrc_t rlo = make_rsrc(Mlo + c0 * D, (uint32_t)(nc * D * 2));
+  const __amdgpu_buffer_rsrc_t rhi = make_rsrc(Mhi + c0 * D, (uint32_t)(nc * D * 2));
+  GemmCore<F16Tag> core;
+  core.zero();
+  const int n_stage = (int)(D / GK);
+  core.run(sm, rx, ldx, rhi, D, n_stage);
+  core.run(sm, rx, ldx, rlo, D, n_stage);
+  const float unscale = ldexpf(1.f, -split_exponent(*maxbits));
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = GemmCore<F16Tag>::row_of(i, r);
+      float ss = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int col = GemmCore<F16Tag>::col_of(j);
+        const float v = core.acc[i][j][r] * unscale;
+        if (row < nr && col < nc) {
+          store_y<YT>(Y + (r0 + row) * ldy + c0 + col, v);
+          ss += v * v;
+        }
+      }
+      // reduce over the 16 lanes that share this row
+      ss += __shfl_xor(ss, 1, kWave);
+      ss += __shfl_xor(ss, 2, kWave);
+      ss += __shfl_xor(ss, 4, kWave);
+      ss += __shfl_xor(ss, 8, kWave);
+      if (rowss && (lane & 15) == 0 && row < nr)
+        rowss[(r0 + row) * n_ss + 2 * tn + (wave & 1)] = ss;
+    }
+}
+
+}  // namespace
+
+int apply_full_nss(int64_t D) { return (int)(2 * ((D + GT - 1) / GT)); }
+
+hipError_t launch_apply_full(const void* X, int64_t n_rows, int64_t ldx, int64_t D, const float* M,
+                             int y_dtype, void* Y, int64_t ldy, int unit, void* ws,
+                             hipStream_t s) {
+  char* base = static_cast<char*>(ws);
+  const size_t mbytes = (size_t)D * (size_t)D * 2;
+  const size_t mb_al = (mbytes + 255) / 256 * 256;
+  _Float16* hi = reinterpret_cast<_Float16*>(base);
+  _Float16* lo = reinterpret_cast<_Float16*>(base + mb_al);
+  unsigned int* maxbits = reinterpret_cast<unsigned int*>(base + 2 * mb_al);
+  float* rowss = unit ? reinterpret_cast<float*>(base + 2 * mb_al + 256) : nullptr;
+  const int64_t nm = D * D;
+  hipLaunchKernelGGL(zero_word_kernel, dim3(1), dim3(1), 0, s, maxbits);
+  hipLaunchKernelGGL(absmax_kernel, dim3(1024), dim3(256), 0, s, M, nm, maxbits);
+  hipLaunchKernelGGL(split_m_kernel, dim3((unsigned)((nm + 255) / 256)), dim3(256), 0, s, M, nm,
+                     (const unsigned int*)maxbits, hi, lo);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int n_tn = (int)((D + GT - 1) / GT);
+  const int64_t n_tm = (n_rows + GT - 1) / GT;
+  const int n_ss = apply_full_nss(D);
+  dim3 grid((unsigned)(n_tm * n_tn)), block(256);
+  if (y_dtype == 2)
+    hipLaunchKernelGGL(apply_full_kernel<_Float16>, grid, block, 0, s, (const _Float16*)X, n_rows,
+                       ldx, D, hi, lo, (const unsigned int*)maxbits, (_Float16*)Y, ldy, rowss, n_ss,
+                       n_tn);
+  else
+    hipLaunchKernelGGL(apply_full_kernel<float>, grid, block, 0, s, (const _Float16*)X, n_rows, ldx,
+                       D, hi, lo, (const unsigned int*)maxbits, (float*)Y, ldy, rowss, n_ss, n_tn);
+  e = hipGetLastError();
+  if (e != hipSuccess || !unit) return e;
+  return launch_rowscale(y_dtype, y_dtype, Y, ldy, n_rows, D, nullptr, 1, rowss, n_ss, Y, ldy, s);
+}
+
+size_t apply_full_workspace(int64_t n_rows, int64_t D, int unit) {
+  const size_t mbytes = (size_t)D * (size_t)D * 2;
+  const size_t mb_al = (mbytes + 255) / 256 * 256;
+  size_t total = 2 * mb_al + 256;
+  if (unit) total += ((size_t)n_rows * (size_t)apply_full_nss(D) * 4 + 255) / 256 * 256;
+  return total;
+}
+
+}  // namespace attr

@@ -73,11 +73,41 @@ hipError_t launch_colsumsq(int x_dtype, const void* X, int64_t ldx, int64_t n_ro
 // ---------------------------------------------------------------------------
 // scoring
 // ---------------------------------------------------------------------------
-int score_parts(int64_t n_q, int64_t n_g);
-int64_t score_rows_per_part(int64_t n_g, int parts);
-hipError_t launch_score_topk(bool f16, const void* Q, int64_t n_q, int64_t ldq, const void* G,
-                             int64_t n_g, int64_t ldg, int64_t D, int k, int64_t index_base,
-                             int merge, float* top_s, int64_t* top_i, float* part_s,
-                             int64_t* part_i, hipStream_t s);
+struct ScorePlan {
+  int n_qb;              // 64-query blocks
+  int n_grp;             // 128-byte K-groups per row
+  int split;             // D-slices (1: fused plan)
+  int n_tiles;           // 128-row tiles (split-K plan)
+  int n_parts;           // row partitions, one sorted list each per query
+  int64_t rows_per_part;
+  size_t spart_bytes;    // split-K partial scores
+  size_t list_entries;   // n_q * n_parts * k
+};
+ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes);
+hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int64_t n_q,
+                             int64_t ldq, const void* G, int64_t n_g, int64_t ldg, int k,
+                             int64_t index_base, int merge, float* top_s, int64_t* top_i,
+                             float* part_s, int64_t* part_i, float* spart, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// full second moment: accumulate (SYRK) and apply
+// ---------------------------------------------------------------------------
+struct SyrkPlan {
+  int nt;          // 256-wide tiles per side
+  int n_up;        // upper-triangle tiles
+  int J;           // K-slices per chunk
+  int64_t Cs;      // rows per slice
+  int64_t C;       // rows per chunk (J * Cs)
+  size_t xt_bytes, part_bytes, h64_bytes;
+};
+SyrkPlan plan_syrk(int64_t n_rows, int64_t D);
+hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, int64_t D, float* H,
+                       const SyrkPlan& P, void* xt, void* part, void* h64, hipStream_t s);
+
+int apply_full_nss(int64_t D);
+size_t apply_full_workspace(int64_t n_rows, int64_t D, int unit);
+hipError_t launch_apply_full(const void* X, int64_t n_rows, int64_t ldx, int64_t D, const float* M,
+                             int y_dtype, void* Y, int64_t ldy, int unit, void* ws,
+                             hipStream_t s);
 
 }  // namespace attr

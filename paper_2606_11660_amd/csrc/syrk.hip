@@ -1,0 +1,189 @@
+// Full second-moment accumulation H += X^T X over store rows (the flat
+// autocorrelation / empirical Fisher preconditioner of the method-family
+// table; TrackStar's Fisher fitting step in section "Attribution Pipelines").
+//
+// The contraction runs over rows of X, so the MFMA operands need K = row
+// index contiguous.  Rows are processed in chunks of up to 65536: a
+// transpose kernel writes the chunk as XT [D, C] (64 x 64 tiles through LDS;
+// rows past the end become zeros), then the 256 x 256 block-tile GEMM core
+// computes only the upper-triangle tiles (tp <= tq) of XT XT^T.  Each chunk
+// is split into J <= 4 K-slices computed by separate workgroups, so that
+// 528 tiles x J slices fill the 256 CUs; slice results go to fp32 partial
+// tiles and a reduce kernel adds them, in slice order, into an fp64
+// accumulator.  Precision: fp32 MFMA accumulation over at most 16384 rows,
+// fp64 across slices and chunks, one rounding into H at the end of the call
+// (the spectrum of H spans ~6 decades on low-rank-plus-noise stores, and long
+// fp32 accumulation visibly perturbs its small eigenvalues).
+// Deterministic: fixed tile, slice and chunk orders, no atomics.
+#include "common.h"
+#include "gemm.h"
+#include "kernels.h"
+
+namespace attr {
+namespace {
+
+constexpr int SYRK_CHUNK = 65536;
+constexpr int TILE_E = GT * GT;  // elements per tile
+
+// XT[c][r] = X[r0 + r][c] for r < C (zero past n_rows), c < D.  64 x 64 tiles.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ X, int64_t ldx,
+                                                        int64_t n_rows, int64_t r0, int64_t D,
+                                                        int64_t C, T* __restrict__ XT) {
+  __shared__ T tile[64][66];
+  const int64_t tr = (int64_t)blockIdx.x * 64;  // chunk-row block
+  const int64_t tc = (int64_t)blockIdx.y * 64;  // column block
+  const int t = threadIdx.x;
+  // load: 64 rows x 64 columns, 16 consecutive elements... 256 threads x 16 elements
+  {
+    const int lr = t >> 2, lc = (t & 3) * 16;
+    const int64_t row = r0 + tr + lr;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t col = tc + lc + e;
+      T v = (T)0.f;
+      if (row < n_rows && col < D) v = X[row * ldx + col];
+      tile[lr][lc + e] = v;
+    }
+  }
+  __syncthreads();
+  {
+    const int lc = t >> 2, lr = (t & 3) * 16;  // output row = column lc, 16 chunk rows
+    const int64_t oc = tc + lc;
+    if (oc < D) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) XT[oc * C + tr + lr + e] = tile[lr + e][lc];
+    }
+  }
+}
+
+// Upper-triangle tile u -> (tp, tq), tp <= tq, row-major over tp.
+__device__ inline void upper_tile(int u, int nt, int& tp, int& tq) {
+  int p = 0;
+  while (u >= nt - p) {
+    u -= nt - p;
+    ++p;
+  }
+  tp = p;
+  tq = p + u;
+}
+
+template <typename Tag, typename T>
+__global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ XT, int64_t C,
+                                                   int64_t D, int nt, int n_up, int64_t Cs,
+                                                   float* __restrict__ part) {
+  __shared__ GemmSmem sm;
+  const int u = (int)(blockIdx.x % (uint32_t)n_up);
+  const int j = (int)(blockIdx.x / (uint32_t)n_up);
+  int tp, tq;
+  upper_tile(u, nt, tp, tq);
+  int64_t np = D - (int64_t)tp * GT, nq = D - (int64_t)tq * GT;
+  np = np > GT ? GT : np;
+  nq = nq > GT ? GT : nq;
+  const T* a = XT + (int64_t)tp * GT * C + (int64_t)j * Cs;
+  const T* b = XT + (int64_t)tq * GT * C + (int64_t)j * Cs;
+  // range: the tile's rows, each C long (the K window is [0, Cs) of that)
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(a, (uint32_t)((np - 1) * C * 2 + Cs * 2));
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(b, (uint32_t)((nq - 1) * C * 2 + Cs * 2));
+  GemmCore<Tag> core;
+  core.zero();
+  core.run(sm, ra, C, rb, C, (int)(Cs / GK));
+  float* dst = part + ((int64_t)j * n_up + u) * TILE_E;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dst[((i * 8 + jj) * 4 + r) * 256 + threadIdx.x] = core.acc[i][jj][r];
+}
+
+// h64[u][e] += sum_j part[j][u][e], slices in order (fragment-order layout).
+__global__ __launch_bounds__(256) void syrk_reduce_kernel(const float* __restrict__ part, int J,
+                                                          int64_t n_e, double* __restrict__ h64) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= n_e) return;
+  double s = 0.0;
+  for (int j = 0; j < J; ++j) s += (double)part[(int64_t)j * n_e + e];
+  h64[e] += s;
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(double* __restrict__ p, int64_t n) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < n) p[e] = 0.0;
+}
+
+// H[p][q] += h64 for p <= q; fragment-order element f of tile u maps to
+// (i, jj, r, thread) with row 128 (w/2) + 16 i + 4 (lane/16) + r and column
+// 128 (w%2) + 16 jj + lane%16.
+__global__ __launch_bounds__(256) void syrk_store_kernel(const double* __restrict__ h64, int nt,
+                                                         int64_t D, float* __restrict__ H) {
+  const int u = blockIdx.y;
+  int tp, tq;
+  upper_tile(u, nt, tp, tq);
+  const int64_t f = (int64_t)blockIdx.x * 256 + threadIdx.x;  // 0 .. TILE_E
+  const int th = (int)(f & 255), w = th >> 6, lane = th & 63;
+  const int irj = (int)(f >> 8);
+  const int r = irj & 3, jj = (irj >> 2) & 7, i = irj >> 5;
+  const int64_t p = (int64_t)tp * GT + 128 * (w >> 1) + 16 * i + 4 * (lane >> 4) + r;
+  const int64_t q = (int64_t)tq * GT + 128 * (w & 1) + 16 * jj + (lane & 15);
+  if (p < D && q < D && p <= q) {
+    float* hp = H + p * D + q;
+    *hp = (float)((double)*hp + h64[(int64_t)u * TILE_E + f]);
+  }
+}
+
+}  // namespace
+
+SyrkPlan plan_syrk(int64_t n_rows, int64_t D) {
+  SyrkPlan P{};
+  P.nt = (int)((D + GT - 1) / GT);
+  P.n_up = P.nt * (P.nt + 1) / 2;
+  int64_t c = n_rows < SYRK_CHUNK ? n_rows : SYRK_CHUNK;
+  c = (c + 63) / 64 * 64;
+  if (c < 64) c = 64;
+  int J = (int)(c / 16384);
+  J = J < 1 ? 1 : (J > 4 ? 4 : J);
+  int64_t cs = (c + J - 1) / J;
+  cs = (cs + 63) / 64 * 64;
+  P.J = J;
+  P.Cs = cs;
+  P.C = cs * J;
+  P.xt_bytes = (size_t)D * (size_t)P.C * 2;
+  P.part_bytes = (size_t)J * (size_t)P.n_up * TILE_E * 4;
+  P.h64_bytes = (size_t)P.n_up * TILE_E * 8;
+  return P;
+}
+
+hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, int64_t D, float* H,
+                       const SyrkPlan& P, void* xt, void* part, void* h64, hipStream_t s) {
+  const int64_t n_e = (int64_t)P.n_up * TILE_E;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n_e + 255) / 256)), dim3(256), 0, s,
+                     (double*)h64, n_e);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  for (int64_t r0 = 0; r0 < n_rows; r0 += P.C) {
+    dim3 gt((unsigned)(P.C / 64), (unsigned)((D + 63) / 64));
+    if (bf16)
+      hipLaunchKernelGGL(transpose_kernel<__bf16>, gt, dim3(256), 0, s, (const __bf16*)X, ldx, n_rows,
+                         r0, D, P.C, (__bf16*)xt);
+    else
+      hipLaunchKernelGGL(transpose_kernel<_Float16>, gt, dim3(256), 0, s, (const _Float16*)X, ldx,
+                         n_rows, r0, D, P.C, (_Float16*)xt);
+    dim3 gs((unsigned)(P.n_up * P.J));
+    if (bf16)
+      hipLaunchKernelGGL((syrk_kernel<Bf16Tag, __bf16>), gs, dim3(256), 0, s, (const __bf16*)xt, P.C,
+                         D, P.nt, P.n_up, P.Cs, (float*)part);
+    else
+      hipLaunchKernelGGL((syrk_kernel<F16Tag, _Float16>), gs, dim3(256), 0, s, (const _Float16*)xt,
+                         P.C, D, P.nt, P.n_up, P.Cs, (float*)part);
+    hipLaunchKernelGGL(syrk_reduce_kernel, dim3((unsigned)((n_e + 255) / 256)), dim3(256), 0, s,
+                       (const float*)part, P.J, n_e, (double*)h64);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(syrk_store_kernel, dim3(TILE_E / 256, (unsigned)P.n_up), dim3(256), 0, s,
+                     (const double*)h64, P.nt, D, H);
+  return hipGetLastError();
+}
+
+}  // namespace attr

@@ -145,3 +145,21 @@ def test_score_validation(L):
     assert call(ws=FAKE + (4 << 32) + 16, wsb=need) == ALIGN
     assert call(nq=0) == OK
     assert call(ng=0, merge=1) == OK
+
+
+def test_full_mode_validation(L):
+    acc, app = L.attr_precond_accumulate, L.attr_precond_apply
+    H = FAKE + (1 << 34)
+    Y = FAKE + (1 << 35)
+    assert acc(FAKE, P.ATTR_F32, 100, 256, 256, P.PRECOND_FULL, H, None, 0, None) == UNSUPPORTED
+    assert acc(FAKE, P.ATTR_F16, 100, 200, 200, P.PRECOND_FULL, H, None, 0, None) == ALIGN
+    assert acc(FAKE, P.ATTR_F16, 100, 256, 256, P.PRECOND_FULL, FAKE + 4096, None, 0, None) == INVALID
+    assert acc(FAKE, P.ATTR_F16, 100, 256, 256, P.PRECOND_FULL, H, None, 0, None) == WORKSPACE
+    need = L.attr_precond_accumulate_workspace_size(100, 256, P.ATTR_F16, P.PRECOND_FULL)
+    assert need > 256 * 256 * 8
+    assert app(FAKE, P.ATTR_F32, 4, 256, 256, P.PRECOND_FULL, H, 1, Y, P.ATTR_F16, 256, None, 0, None) == UNSUPPORTED
+    assert app(FAKE, P.ATTR_F16, 4, 256, 256, P.PRECOND_FULL, None, 1, Y, P.ATTR_F16, 256, None, 0, None) == INVALID
+    assert app(FAKE, P.ATTR_F16, 4, 256, 256, P.PRECOND_FULL, H, 1, FAKE, P.ATTR_F16, 256, None, 0, None) == INVALID
+    assert app(FAKE, P.ATTR_F16, 4, 256, 256, P.PRECOND_FULL, H, 1, Y, P.ATTR_F16, 256, None, 0, None) == WORKSPACE
+    assert L.attr_precond_apply_workspace_size(4, 256, P.PRECOND_FULL) >= 2 * 256 * 256 * 2
+    assert L.attr_precond_apply_workspace_size(4, 256, P.PRECOND_DIAG) == 0
