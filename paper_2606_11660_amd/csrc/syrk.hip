@@ -25,35 +25,38 @@ namespace {
 constexpr int SYRK_CHUNK = 65536;
 constexpr int TILE_E = GT * GT;  // elements per tile
 
-// XT[c][r] = X[r0 + r][c] for r < C (zero past n_rows), c < D.  64 x 64 tiles.
+// XT[c][r] = X[r0 + r][c] for r < C (zero past n_rows), c < D.  64 x 64
+// tiles through LDS; global reads and writes are 16-byte vectors along rows.
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ X, int64_t ldx,
                                                         int64_t n_rows, int64_t r0, int64_t D,
                                                         int64_t C, T* __restrict__ XT) {
-  __shared__ T tile[64][66];
+  __shared__ uint16_t tile[64][64 + 2];
   const int64_t tr = (int64_t)blockIdx.x * 64;  // chunk-row block
-  const int64_t tc = (int64_t)blockIdx.y * 64;  // column block
+  const int64_t tc = (int64_t)blockIdx.y * 64;  // column block (D is a multiple of 64)
   const int t = threadIdx.x;
-  // load: 64 rows x 64 columns, 16 consecutive elements... 256 threads x 16 elements
-  {
-    const int lr = t >> 2, lc = (t & 3) * 16;
-    const int64_t row = r0 + tr + lr;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int64_t col = tc + lc + e;
-      T v = (T)0.f;
-      if (row < n_rows && col < D) v = X[row * ldx + col];
-      tile[lr][lc + e] = v;
+  for (int h = 0; h < 2; ++h) {
+    const int lr = (t >> 3) + 32 * h, lc = (t & 7) * 8;
+    const int64_t row = r0 + tr + lr;
+    i32x4 v = {0, 0, 0, 0};
+    if (row < n_rows) v = *(const i32x4*)(X + row * ldx + tc + lc);
+    const uint32_t w[4] = {(uint32_t)v.x, (uint32_t)v.y, (uint32_t)v.z, (uint32_t)v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      tile[lr][lc + 2 * e] = (uint16_t)(w[e] & 0xffffu);
+      tile[lr][lc + 2 * e + 1] = (uint16_t)(w[e] >> 16);
     }
   }
   __syncthreads();
-  {
-    const int lc = t >> 2, lr = (t & 3) * 16;  // output row = column lc, 16 chunk rows
-    const int64_t oc = tc + lc;
-    if (oc < D) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) XT[oc * C + tr + lr + e] = tile[lr + e][lc];
-    }
+  for (int h = 0; h < 2; ++h) {
+    const int oc = (t >> 3) + 32 * h, orr = (t & 7) * 8;  // output row (column of X), 8 chunk rows
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = (uint32_t)tile[orr + 2 * e][oc] | ((uint32_t)tile[orr + 2 * e + 1][oc] << 16);
+    *(i32x4*)(XT + (tc + oc) * C + tr + orr) = i32x4{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
   }
 }
 
