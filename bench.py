@@ -33,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16
 BATCH = 64
 
 
@@ -74,12 +75,129 @@ def _cpu_baseline(n_sample: int = 6, min_seconds: float = 12.0):
                       f"against 64 queries; {dt:.1f} s timed"}
 
 
+
+def _timeit(fn, stream, reps):
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        fn()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+    stream.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def _other_rows(stream, dev):
+    """Timings of the preconditioner rows on the 10^6 x 8192 low-rank-plus-noise
+    store and of the 4M-row store scan (Q sweep), each against its roofline."""
+    import torch
+    import paper_2606_11660_amd as P
+    out = {}
+    N, D = 1_000_000, 8192
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(3)
+    with torch.cuda.stream(stream):
+        F = torch.randn((D, 64), generator=gen, device=dev)
+        X = torch.empty((N, D), dtype=torch.float16, device=dev)
+        for i in range(0, N, 65536):
+            n = min(65536, N - i)
+            Z = torch.randn((n, 64), generator=gen, device=dev)
+            X[i:i + n] = (Z @ F.T + 0.1 * torch.randn((n, D), generator=gen, device=dev)).half()
+        del F, Z
+    stream.synchronize()
+    xb = N * D * 2
+    h = torch.zeros(D, dtype=torch.float32, device=dev)
+    ms = _timeit(lambda: P.attr_precond_accumulate(X, P.PRECOND_DIAG, h, stream=stream), stream, 3)
+    out["diag_accumulate"] = {"shape": [N, D], "ms": ms, "GBps": xb / ms / 1e6,
+                              "frac_hbm": xb / ms / 1e6 / HBM_PEAK_GBPS}
+    H = torch.zeros((D, D), dtype=torch.float32, device=dev)
+    ms = _timeit(lambda: P.attr_precond_accumulate(X, P.PRECOND_FULL, H, stream=stream), stream, 2)
+    fl = N * D * (D + 1)
+    out["syrk"] = {"shape": [N, D], "ms": ms, "TFLOPs": fl / ms / 1e9,
+                   "frac_mfma": fl / ms / 1e9 / MFMA_PEAK_TFLOPS,
+                   "flops": "N*D*(D+1), upper triangle incl. diagonal"}
+    m = torch.rand(D, generator=gen, device=dev) + 0.5
+    Y = torch.empty_like(X)
+    ms = _timeit(lambda: P.attr_precond_apply(X, P.PRECOND_DIAG, m, True, Y, stream=stream), stream, 3)
+    out["diag_apply_unit"] = {"shape": [N, D], "ms": ms, "GBps": 2 * xb / ms / 1e6,
+                              "frac_hbm": 2 * xb / ms / 1e6 / HBM_PEAK_GBPS}
+    B = torch.randn((D, D), generator=gen, device=dev) / D ** 0.5
+    M = (B @ B.T + torch.eye(D, device=dev)).contiguous()
+    del B
+    ms = _timeit(lambda: P.attr_precond_apply(X, P.PRECOND_FULL, M, True, Y, stream=stream), stream, 2)
+    fl = 2.0 * N * D * D
+    out["full_apply_unit"] = {"shape": [N, D], "ms": ms, "TFLOPs": fl / ms / 1e9,
+                              "frac_mfma": fl / ms / 1e9 / MFMA_PEAK_TFLOPS,
+                              "flops": "2*N*D^2 algorithmic (the hi/lo split executes it twice)"}
+    del X, Y, H, M
+    torch.cuda.empty_cache()
+
+    # store scan: 4M unit rows x 8192 fp16 (65.5 GB), planted near-duplicates
+    NS = 4_000_000
+    G = torch.empty((NS, D), dtype=torch.float16, device=dev)
+    with torch.cuda.stream(stream):
+        for i in range(0, NS, 65536):
+            n = min(65536, NS - i)
+            c = torch.randn((n, D), generator=gen, device=dev)
+            G[i:i + n] = (c / c.norm(dim=1, keepdim=True)).half()
+        del c
+    stream.synchronize()
+    tg = torch.Generator()
+    tg.manual_seed(4)
+    targets = torch.randperm(NS, generator=tg)[:16].to(dev)
+    scan = {}
+    for nq in (16, 64, 256, 1024):
+        with torch.cuda.stream(stream):
+            q = torch.randn((nq, D), generator=gen, device=dev)
+            q = q / q.norm(dim=1, keepdim=True)
+            g = G[targets].float()
+            g = g / g.norm(dim=1, keepdim=True)
+            u = q[:16] - (q[:16] * g).sum(1, keepdim=True) * g
+            u = u / u.norm(dim=1, keepdim=True)
+            q[:16] = 0.9 * g + (1 - 0.81) ** 0.5 * u
+            Q = q.half().contiguous()
+        stream.synchronize()
+        ts = torch.empty((nq, 100), dtype=torch.float32, device=dev)
+        ti = torch.empty((nq, 100), dtype=torch.int64, device=dev)
+        ms = _timeit(lambda: P.attr_score_topk(Q, G, 100, ts, ti, stream=stream), stream, 1)
+        ok = bool((ti[:16, 0] == targets).all().item())
+        scan[str(nq)] = {"ms": ms, "pairs_per_s": nq * NS / (ms * 1e-3),
+                         "GBps": NS * D * 2 / ms / 1e6,
+                         "frac_hbm": NS * D * 2 / ms / 1e6 / HBM_PEAK_GBPS,
+                         "TFLOPs": 2.0 * nq * NS * D / ms / 1e9,
+                         "frac_mfma": 2.0 * nq * NS * D / ms / 1e9 / MFMA_PEAK_TFLOPS,
+                         "planted_rank1": ok}
+    out["store_scan_4M_x_8192_top100"] = scan
+    del G
+    torch.cuda.empty_cache()
+    return out
+
+
+def _copy_reference(dev):
+    """A plain device copy of 1 GiB, five times: the reference kernel whose
+    FETCH_SIZE / WRITE_SIZE counters calibrate the traffic figures."""
+    import torch
+    x = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+    x.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_reference_bytes": 1 << 30, "copies": 5}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=64)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--quick", action="store_true", help="skip the preconditioner / store-scan rows")
+    ap.add_argument("--copy-reference", action="store_true",
+                    help="only run the 1 GiB copy used to calibrate traffic counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -96,6 +214,9 @@ def main():
     k, T, B, D = wl.k, wl.T, BATCH, wl.D
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_reference:
+        _copy_reference(dev)
+        return
     stream = torch.cuda.Stream(device=dev)
 
     # ---------------- setup (not timed) ----------------
@@ -200,6 +321,13 @@ def main():
                        "ms": scan_ms, "pairs_per_s": wl.n_queries * n_store / (scan_ms * 1e-3),
                        "GBps": scan_bytes / (scan_ms * 1e-3) / 1e9},
     }
+    del mods, store, rows32
+    torch.cuda.empty_cache()
+    if not args.quick:
+        try:
+            result["other_rows"] = _other_rows(stream, dev)
+        except Exception as exc:  # report, keep the headline line
+            result["other_rows"] = {"error": repr(exc)}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = _cpu_baseline()
     print(json.dumps(result), flush=True)

@@ -37,6 +37,36 @@ __device__ inline i32x4 load16_cached(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
+// Raw buffer descriptor words (same layout make_rsrc builds), for inline asm.
+__device__ inline i32x4 make_desc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  return i32x4{(int)(uint32_t)a, (int)(uint32_t)((a >> 32) & 0xffffu), (int)bytes, kRsrcWord3};
+}
+
+// Direct-to-LDS 16-byte buffer load: lane l's 16 bytes at voff land at LDS
+// byte address lds_base + 16 l (lanes out of the descriptor's range write
+// zeros).  Issued through inline asm so that the compiler does not add its
+// own conservative wait before every later LDS read; the caller owns the
+// vmcnt accounting (one instruction per call) and the barrier.
+__device__ inline void lds_dma16(const i32x4& desc, uint32_t voff, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %0, %1, 0 offen lds"
+      :
+      : "v"(voff), "s"(desc), "s"(lds_base)
+      : "memory", "m0");
+}
+__device__ inline void lds_dma16_nt(const i32x4& desc, uint32_t voff, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %0, %1, 0 offen nt lds"
+      :
+      : "v"(voff), "s"(desc), "s"(lds_base)
+      : "memory", "m0");
+}
+
 // One 16-byte A fragment times one 16-byte B fragment on the matrix cores,
 // accumulated into a 16x16 fp32 tile.  For bf16/fp16 a fragment is 8 values
 // of K (one 16x16x32 MFMA); for fp32 it is 4 values of K (four 16x16x4

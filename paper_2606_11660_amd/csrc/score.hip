@@ -8,10 +8,7 @@
 // fragments (as in the projection); query fragments come from L2.
 //
 // Two plans, chosen on the host from the problem shape:
-//  * fused (large stores): a workgroup owns 64 queries and a contiguous row
-//    partition; each finished tile goes to LDS and one lane per query walks
-//    it in row order against the query's running threshold, inserting
-//    winners into a sorted per-query list in LDS.  Rows are visited in
+//  * streaming (large stores): see score_stream_kernel.  Rows are visited in
 //    increasing index order, so a strict ">" keeps the lower index on ties.
 //    The Q x N score matrix never reaches memory.
 //  * split-K (small stores, too few tiles to fill 256 CUs): workgroups own
@@ -154,67 +151,319 @@ __device__ inline void write_list(float (*ls)[KMAX], int (*li)[KMAX], int q_loca
 }
 
 // ---------------------------------------------------------------------------
-// fused plan
+// streaming plan (large stores)
 // ---------------------------------------------------------------------------
-template <bool F16, int KMAX>
-__global__ __launch_bounds__(256) void score_fused_kernel(
+// A workgroup owns 64 queries (16 per wave) and a contiguous partition of
+// store rows, walked in tiles of 64 rows.  The tile sequence is cut into
+// 128-byte K-groups ("stages"): for every stage the 64 store rows and the 64
+// query rows go straight from memory into a shared LDS ring by
+// direct-to-LDS buffer loads (1 KB, line-coalesced instructions that land in
+// the XOR-swizzled fragment layout), RING - 1 stages ahead.  No vector load
+// feeds a register inside the loop, so the only waits are explicit: every
+// stage costs each wave exactly 4 load instructions, the wait for stage st
+// is vmcnt <= 4 * (stages issued after st), then one barrier (all waves'
+// loads landed; all waves finished the previous stage, whose slot is then
+// refilled).
+//
+// Each wave computes its 16 queries (every fourth of the block) x 64 rows,
+// so after a tile it holds every score of its own queries and needs no
+// exchange.  Top-k selection is software-pipelined behind the stream: when
+// a tile ends its scores move to a pending copy and are compared with the
+// 16 running thresholds (k-th best so far, kept in registers); during the
+// next tile's stages the wave walks its queries, one per stage, and inserts
+// the passing rows of that query, in row order.  Each query's sorted list
+// lives in a private LDS region of its wave, padded with (-inf, -1); a
+// query with candidates loads it into registers (entry p in lane p % 64,
+// slot p / 64), inserts with all 64 lanes at once (the position is the
+// number of entries >= s: existing entries have lower row indices, so ties
+// keep them first; the tail moves one lane up through a wave-wide DPP
+// shift) and stores it back.  The selection code is a short loop rather than
+// a per-query unrolled copy, so that it stays in the instruction cache.
+// Partitions are mapped so that the query blocks sharing a partition run on
+// the same XCD at the same time and share its L2.
+constexpr int SR = 64;  // store rows per tile
+constexpr int SQ = 64;  // queries per workgroup
+
+template <int N>
+__device__ inline void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// n = 4 m, m in [0, 6]
+__device__ inline void wait_vmcnt_4m(int n) {
+  switch (n) {
+    case 24: wait_vmcnt<24>(); break;
+    case 20: wait_vmcnt<20>(); break;
+    case 16: wait_vmcnt<16>(); break;
+    case 12: wait_vmcnt<12>(); break;
+    case 8: wait_vmcnt<8>(); break;
+    case 4: wait_vmcnt<4>(); break;
+    default: wait_vmcnt<0>(); break;
+  }
+}
+
+__device__ inline float sel4(const f32x4& a, int r) {
+  float v = a[0];
+  v = r == 1 ? a[1] : v;
+  v = r == 2 ? a[2] : v;
+  v = r == 3 ? a[3] : v;
+  return v;
+}
+
+// lane l takes lane l - 1's value, lane 0 takes `fill` (DPP wave_shr:1)
+__device__ inline int wave_shr1(int v, int fill) {
+  return __builtin_amdgcn_update_dpp(fill, v, 0x138, 0xf, 0xf, false);
+}
+
+// Register-resident sorted list of one query: entry p in lane p % 64 of
+// slot p / 64; positions >= k are don't-care.
+template <int NS>
+struct RegList {
+  float s[NS];
+  int i[NS];
+  // kth entry's score
+  __device__ inline float kth(int k) const {
+    float t = s[0];
+#pragma unroll
+    for (int j = 1; j < NS; ++j) t = (k - 1) / 64 == j ? s[j] : t;
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, t), (k - 1) & 63));
+  }
+  // insert (v, idx): idx exceeds every row present, v > kth(k)
+  __device__ inline void insert(float v, int idx, int k, int lane) {
+    int pos = 0;
+#pragma unroll
+    for (int j = 0; j < NS; ++j)
+      pos += __builtin_popcountll(__builtin_amdgcn_ballot_w64(64 * j + lane < k && s[j] >= v));
+    float us[NS];
+    int ui[NS];
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+      const int cs = j ? __builtin_amdgcn_readlane(__builtin_bit_cast(int, s[j - 1]), 63) : 0;
+      const int ci = j ? __builtin_amdgcn_readlane(i[j - 1], 63) : 0;
+      us[j] = __builtin_bit_cast(float, wave_shr1(__builtin_bit_cast(int, s[j]), cs));
+      ui[j] = wave_shr1(i[j], ci);
+    }
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+      const int p = 64 * j + lane;
+      s[j] = p < pos ? s[j] : (p == pos ? v : us[j]);
+      i[j] = p < pos ? i[j] : (p == pos ? idx : ui[j]);
+    }
+  }
+};
+
+template <bool F16, int KMAX, int RING>
+__global__ __launch_bounds__(256) void score_stream_kernel(
     const char* __restrict__ Q, int64_t n_q, int64_t ldq, const char* __restrict__ G,
     int64_t n_g, int64_t ldg, int n_grp, int k, int64_t rows_per_part, int n_parts, int n_qb,
     float* __restrict__ part_s, int64_t* __restrict__ part_i, int64_t index_base) {
+  static_assert(RING >= 3 && 4 * (RING - 2) <= 24, "wait_vmcnt_4m range");
+  using Tag = typename STag<F16>::tag;
   constexpr int EB = STag<F16>::bytes;
-  __shared__ float ls[SQB][KMAX];
-  __shared__ int li[SQB][KMAX];
-  __shared__ float sc[SQB][SCP];
-  __shared__ i32x4 xpose[4][2 * 128];
+  constexpr int NS = (KMAX + 63) / 64;
+  __shared__ i32x4 ring[RING][(SR + SQ) * 8];  // store rows, then query rows
+  __shared__ float2 lists[4][16][KMAX];        // per wave, per query: (score, row bits)
 
-  const int qb = (int)(blockIdx.x % (uint32_t)n_qb);
-  const int p = (int)(blockIdx.x / (uint32_t)n_qb);
-  const int64_t q0 = (int64_t)qb * SQB;
-  const int64_t r_begin = (int64_t)p * rows_per_part;
-  int64_t r_end = r_begin + rows_per_part;
-  r_end = r_end > n_g ? n_g : r_end;
+  const uint32_t b = blockIdx.x;
+  const int xcd = (int)(b & 7u);
+  const uint32_t jb = b >> 3;
+  const int qb = (int)(jb % (uint32_t)n_qb);
+  const int p = (int)(jb / (uint32_t)n_qb) * 8 + xcd;
+  if (p >= n_parts) return;  // uniform
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
 
-  for (int e = threadIdx.x; e < SQB * KMAX; e += 256) {
-    ls[e / KMAX][e % KMAX] = -__builtin_inff();
-    li[e / KMAX][e % KMAX] = -1;
-  }
-  TopList<KMAX> tl{ls, li, 0, -__builtin_inff()};
-  __syncthreads();
-
+  const int64_t q0 = (int64_t)qb * SQ;
   int64_t nq_blk = n_q - q0;
-  nq_blk = nq_blk > SQB ? SQB : nq_blk;
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(Q + q0 * ldq * EB, (uint32_t)(nq_blk * ldq * EB));
+  nq_blk = nq_blk > SQ ? SQ : nq_blk;
+  // wave w holds block queries w, w + 4, ..., w + 60 (slot j = query 4 j + w), so
+  // that a partial block spreads its selection work over all four waves
+  int nq_w = (int)((nq_blk - wave + 3) / 4);
+  nq_w = nq_w < 0 ? 0 : (nq_w > 16 ? 16 : nq_w);
+  // a store read by a single query block is not kept in L2
+  const bool g_nt = n_qb == 1;
 
-  for (int64_t r0 = r_begin; r0 < r_end; r0 += STN) {
-    int64_t nrow = r_end - (r0 + 32 * wave);
-    nrow = nrow < 0 ? 0 : (nrow > 32 ? 32 : nrow);
-    const __amdgpu_buffer_rsrc_t rg =
-        make_rsrc(G + (r0 + 32 * wave) * ldg * EB, (uint32_t)(nrow * ldg * EB));
-    f32x4 acc[4][2];
+  const int64_t r_begin = (int64_t)p * rows_per_part;
+  int64_t r_end = r_begin + rows_per_part;
+  r_end = r_end > n_g ? n_g : r_end;
+  const int64_t nrows = r_end > r_begin ? r_end - r_begin : 0;
+  const int n_tiles = (int)((nrows + SR - 1) / SR);
+  const int total = n_tiles * n_grp;
+
+  float2(*wl)[KMAX] = lists[wave];
+  for (int ql = 0; ql < 16; ++ql)
 #pragma unroll
-    for (int qt = 0; qt < 4; ++qt)
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) acc[qt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    score_tile<F16>(rq, ldq, rg, ldg, 0, n_grp, lane, &xpose[wave][0], acc);
-#pragma unroll
-    for (int qt = 0; qt < 4; ++qt)
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          sc[16 * qt + 4 * (lane >> 4) + r][32 * wave + 16 * rt + (lane & 15)] = acc[qt][rt][r];
-    __syncthreads();
-    if (wave == 0 && lane < nq_blk) {
-      int64_t nvalid = r_end - r0;
-      nvalid = nvalid > STN ? STN : nvalid;
-      for (int j = 0; j < (int)nvalid; ++j) tl.push(lane, k, sc[lane][j], (int)(r0 + j));
+    for (int j = 0; j < NS; ++j)
+      if (64 * j + lane < KMAX) wl[ql][64 * j + lane] = float2{-__builtin_inff(), __builtin_bit_cast(float, -1)};
+
+  const i32x4 dq = make_desc(Q + q0 * ldq * EB, (uint32_t)(nq_blk * ldq * EB));
+  const int lr = lane >> 3, lc = (lane & 7) ^ lr;
+  const int ri = lane & 15, rgrp = lane >> 4;
+  const uint32_t ring_base = (uint32_t)(uintptr_t)&ring[0][0];
+  constexpr uint32_t SLOT_BYTES = (SR + SQ) * 8 * 16;
+  // per-lane byte offsets of this wave's two 8-row blocks (K-group 0)
+  const uint32_t goff0 = (uint32_t)((int64_t)(16 * wave + lr) * ldg * EB + lc * 16);
+  const uint32_t goff1 = goff0 + (uint32_t)(8 * ldg * EB);
+  const uint32_t qoff0 = (uint32_t)((int64_t)(4 * lr + wave) * ldq * EB + lc * 16);
+  const uint32_t qoff1 = qoff0 + (uint32_t)(32 * ldq * EB);
+  const uint32_t lds_g = ring_base + (uint32_t)(16 * wave) * 128u;
+  const uint32_t lds_q = ring_base + (uint32_t)(SR + 16 * wave) * 128u;
+
+  // issue cursor: next stage to load is (it_tile, it_g) into slot islot
+  int it_tile = 0, it_g = 0, issued = 0, islot = 0;
+  i32x4 dt{0, 0, 0, 0};
+  auto tile_desc = [&](int tile) {
+    const int64_t row0 = r_begin + (int64_t)tile * SR;
+    int64_t nr = r_end - row0;
+    nr = nr > SR ? SR : nr;
+    dt = make_desc(G + row0 * ldg * EB, (uint32_t)(nr * ldg * EB));
+  };
+  auto issue_next = [&]() {
+    const uint32_t sb = (uint32_t)islot * SLOT_BYTES;
+    const uint32_t go = (uint32_t)it_g * 128u;
+    if (g_nt) {
+      lds_dma16_nt(dt, goff0 + go, lds_g + sb);
+      lds_dma16(dq, qoff0 + go, lds_q + sb);
+      lds_dma16_nt(dt, goff1 + go, lds_g + sb + 1024u);
+      lds_dma16(dq, qoff1 + go, lds_q + sb + 1024u);
+    } else {
+      lds_dma16(dt, goff0 + go, lds_g + sb);
+      lds_dma16(dq, qoff0 + go, lds_q + sb);
+      lds_dma16(dt, goff1 + go, lds_g + sb + 1024u);
+      lds_dma16(dq, qoff1 + go, lds_q + sb + 1024u);
     }
-    __syncthreads();
+    ++issued;
+    islot = islot == RING - 1 ? 0 : islot + 1;
+    if (++it_g == n_grp) {
+      it_g = 0;
+      ++it_tile;
+      if (it_tile < n_tiles) tile_desc(it_tile);
+    }
+  };
+
+  if (total > 0) tile_desc(0);
+#pragma unroll
+  for (int u = 0; u < RING - 1; ++u)
+    if (issued < total) issue_next();
+
+  // running thresholds: lane l of thr4[r] holds query 4 (l / 16) + r
+  f32x4 thr4 = f32x4{-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
+  // pending tile: scores (pend[rt][r] in lane l: query 4 (l / 16) + r, row
+  // 16 rt + l % 16), candidate bits cm (bit 4 rt + r) and its first row
+  f32x4 pend[4];
+  uint32_t cm = 0;
+  bool pend_any = false;
+  int pend_rbase = 0;
+
+  auto process_query = [&](int ql) {
+    const int r = ql & 3, grp = ql >> 2;
+    uint64_t m[4];
+    bool has = false;
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      m[rt] = __builtin_amdgcn_ballot_w64(rgrp == grp && ((cm >> (4 * rt + r)) & 1u));
+      has |= m[rt] != 0;
+    }
+    if (!has) return;
+    float thr = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sel4(thr4, r)), 16 * grp));
+    float2* lp = wl[ql];
+    RegList<NS> L;
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+      const float2 e = lp[(64 * j + lane) & (KMAX - 1)];
+      L.s[j] = e.x;
+      L.i[j] = __builtin_bit_cast(int, e.y);
+    }
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      const float v = sel4(pend[rt], r);
+      uint64_t mm = m[rt];
+      while (mm) {
+        const int src = __builtin_ctzll(mm);
+        mm &= mm - 1;
+        const float cv = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), src));
+        if (cv > thr) {
+          L.insert(cv, pend_rbase + 16 * rt + (src & 15), k, lane);
+          thr = L.kth(k);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NS; ++j)
+      if (64 * j + lane < k) lp[64 * j + lane] = float2{L.s[j], __builtin_bit_cast(float, L.i[j])};
+    const bool mine = rgrp == grp;
+    thr4[0] = mine && r == 0 ? thr : thr4[0];
+    thr4[1] = mine && r == 1 ? thr : thr4[1];
+    thr4[2] = mine && r == 2 ? thr : thr4[2];
+    thr4[3] = mine && r == 3 ? thr : thr4[3];
+  };
+
+  int st = 0, cslot = 0;
+  for (int tile = 0; tile < n_tiles; ++tile) {
+    f32x4 acc[4];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int g = 0; g < n_grp; ++g, ++st) {
+      // stage st landed: at most (loads issued after it) of this wave's
+      // loads are still outstanding
+      const int after = total - 1 - st;
+      if (after >= RING - 2) {
+        wait_vmcnt<4 * (RING - 2)>();
+      } else {
+        wait_vmcnt_4m(4 * after);
+      }
+      // this wave's LDS reads of the previous stage are complete before
+      // anyone refills that slot
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      if (issued < total) issue_next();
+      const i32x4* sl = ring[cslot];
+      cslot = cslot == RING - 1 ? 0 : cslot + 1;
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int qrow = SR + 16 * wave + ri;
+        const i32x4 qf = sl[qrow * 8 + ((4 * s2 + rgrp) ^ (qrow & 7))];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+          const int grow = 16 * rt + ri;
+          const i32x4 gf = sl[grow * 8 + ((4 * s2 + rgrp) ^ (grow & 7))];
+          acc[rt] = mma16(Tag{}, qf, gf, acc[rt]);
+        }
+      }
+      // previous tile's selection, spread over this tile's stages
+      if (pend_any)
+        for (int ql = g; ql < nq_w; ql += n_grp) process_query(ql);
+    }
+    // hand this tile over to the selection
+    const int rbase = tile * SR;
+    const int nvalid = (int)(nrows - rbase > SR ? SR : nrows - rbase);
+    cm = 0;
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      pend[rt] = acc[rt];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        cm |= (4 * rgrp + r < nq_w && 16 * rt + ri < nvalid && acc[rt][r] > thr4[r]) ? 1u << (4 * rt + r) : 0u;
+    }
+    pend_any = __builtin_amdgcn_ballot_w64(cm != 0) != 0;
+    pend_rbase = rbase;
   }
-  if (wave == 0 && lane < nq_blk)
-    write_list<KMAX>(ls, li, lane, q0 + lane, p, n_parts, k, index_base, part_s, part_i);
+  if (pend_any)
+    for (int ql = 0; ql < nq_w; ++ql) process_query(ql);
+  for (int ql = 0; ql < nq_w; ++ql) {
+    const int64_t q = q0 + 4 * ql + wave;
+    float* ds = part_s + (q * n_parts + p) * (int64_t)k;
+    int64_t* di = part_i + (q * n_parts + p) * (int64_t)k;
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+      const int pos = 64 * j + lane;
+      if (pos < k) {
+        const float2 e = wl[ql][pos];
+        const int idx = __builtin_bit_cast(int, e.y);
+        ds[pos] = e.x;
+        di[pos] = idx >= 0 ? index_base + r_begin + idx : -1;
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -296,35 +545,24 @@ __global__ __launch_bounds__(256) void score_select_kernel(const float* __restri
   int64_t r1 = r0 + rows_per_part;
   r1 = r1 > n_g ? n_g : r1;
   const int64_t plane = n_g * nqp;
-  const int jr = t >> 1;        // row within the chunk
-  const int qh = (t & 1) * 32;  // first of this thread's 32 queries
+  const int qv = 4 * (t & 15);  // this thread's 4 queries
   for (int64_t c0 = r0; c0 < r1; c0 += STN) {
     int64_t nrow = r1 - c0;
     nrow = nrow > STN ? STN : nrow;
-    if (jr < nrow) {
-      const f32x4* src = (const f32x4*)(spart + (c0 + jr) * nqp + q0 + qh);
-      f32x4 acc[8];
-#pragma unroll
-      for (int v = 0; v < 8; ++v) acc[v] = src[v];
+    for (int jr = t >> 4; jr < nrow; jr += 16) {
+      const f32x4* src = (const f32x4*)(spart + (c0 + jr) * nqp + q0 + qv);
+      f32x4 acc = src[0];
       int sp = 1;
-      for (; sp + 4 <= n_split; sp += 4) {
-        f32x4 x[4][8];
+      for (; sp + 8 <= n_split; sp += 8) {
+        f32x4 x[8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 8; ++u) x[u] = src[(sp + u) * plane / 4];
 #pragma unroll
-          for (int v = 0; v < 8; ++v) x[u][v] = src[(sp + u) * plane / 4 + v];
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int v = 0; v < 8; ++v) acc[v] += x[u][v];
+        for (int u = 0; u < 8; ++u) acc += x[u];
       }
-      for (; sp < n_split; ++sp)
+      for (; sp < n_split; ++sp) acc += src[sp * plane / 4];
 #pragma unroll
-        for (int v = 0; v < 8; ++v) acc[v] += src[sp * plane / 4 + v];
-#pragma unroll
-      for (int v = 0; v < 8; ++v)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sc[qh + 4 * v + e][jr] = acc[v][e];
+      for (int e = 0; e < 4; ++e) sc[qv + e][jr] = acc[e];
     }
     __syncthreads();
     if (t < nq_blk)
@@ -436,19 +674,25 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
   if (split >= 2) {
     P.split = (int)split;
     P.n_tiles = (int)n_tiles;
-    int64_t parts = n_tiles < 255 ? n_tiles : 255;
+    // select workgroups own 16-row multiples, enough of them to spread the
+    // slice sums over the chip
+    int64_t parts = (n_g + 15) / 16;
+    parts = parts > 255 ? 255 : parts;
     int64_t rpp = (n_g + parts - 1) / parts;
-    rpp = (rpp + STN - 1) / STN * STN;
+    rpp = (rpp + 15) / 16 * 16;
     P.rows_per_part = rpp;
     P.n_parts = (int)((n_g + rpp - 1) / rpp);
     P.spart_bytes = (size_t)split * (size_t)n_g * (size_t)P.n_qb * SQB * 4;
   } else {
     P.split = 1;
+    // streaming plan: 64 queries per workgroup
+    P.n_qb = (int)((n_q + 63) / 64);
     int64_t parts = (512 + P.n_qb - 1) / P.n_qb;
-    parts = parts > n_tiles ? n_tiles : parts;
-    parts = parts > 255 ? 255 : (parts < 1 ? 1 : parts);
+    const int64_t t64 = (n_g + SR - 1) / SR;
+    parts = parts > t64 ? t64 : parts;
+    parts = parts > 248 ? 248 : (parts < 1 ? 1 : parts);
     int64_t rpp = (n_g + parts - 1) / parts;
-    rpp = (rpp + STN - 1) / STN * STN;
+    rpp = (rpp + SR - 1) / SR * SR;
     P.rows_per_part = rpp;
     P.n_parts = (int)((n_g + rpp - 1) / rpp);
     P.spart_bytes = 0;
@@ -463,19 +707,21 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
                              float* part_s, int64_t* part_i, float* spart, hipStream_t s) {
   const int n_parts = n_g > 0 ? plan.n_parts : 0;
   if (n_g > 0 && plan.split <= 1) {
-    dim3 grid((unsigned)(plan.n_qb * plan.n_parts)), block(256);
-#define ATTR_SF(F, KM)                                                                         \
-  hipLaunchKernelGGL((score_fused_kernel<F, KM>), grid, block, 0, s, (const char*)Q, n_q, ldq,   \
-                     (const char*)G, n_g, ldg, plan.n_grp, k, plan.rows_per_part, plan.n_parts, \
+    const int parts_pad = (plan.n_parts + 7) / 8 * 8;
+    dim3 grid((unsigned)(plan.n_qb * parts_pad)), block(256);
+#define ATTR_SS(F, KM, RG)                                                                    \
+  hipLaunchKernelGGL((score_stream_kernel<F, KM, RG>), grid, block, 0, s, (const char*)Q, n_q, ldq, \
+                     (const char*)G, n_g, ldg, plan.n_grp, k, plan.rows_per_part, plan.n_parts,   \
                      plan.n_qb, part_s, part_i, index_base)
+    // LDS: ring RING x 16 KB + lists 4 x 16 x KMAX x 8 B <= 160 KB
     if (f16) {
-      if (k <= 16) ATTR_SF(true, 16);
-      else ATTR_SF(true, 128);
+      if (k <= 64) ATTR_SS(true, 64, 8);
+      else ATTR_SS(true, 128, 6);
     } else {
-      if (k <= 16) ATTR_SF(false, 16);
-      else ATTR_SF(false, 128);
+      if (k <= 64) ATTR_SS(false, 64, 8);
+      else ATTR_SS(false, 128, 6);
     }
-#undef ATTR_SF
+#undef ATTR_SS
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   } else if (n_g > 0) {

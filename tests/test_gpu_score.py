@@ -135,3 +135,20 @@ def test_gpt2_store_scan():
     G = synth.unit_rows(4096, 12288, seed=22)
     ts, ti = _topk(dev(Q), dev(G), 10)
     check_topk(host(ts), host(ti), O.scores(Q, G), 10)
+
+
+@pytest.mark.parametrize("nq,ng,D,k,dt", [(300, 9000, 256, 100, np.float16),
+                                          (40, 40001, 128, 10, np.float16),
+                                          (70, 33000, 96, 5, np.float32),
+                                          (17, 70000, 64, 128, np.float16)])
+def test_streaming_plan(nq, ng, D, k, dt):
+    """Shapes large enough for the streaming (LDS-ring) plan: ragged query
+    blocks, ragged partitions and tiles, duplicate rows, fp32 and fp16."""
+    say(f"case: streaming nq={nq} ng={ng} D={D} k={k} {dt.__name__}")
+    Q = synth.unit_rows(nq, D, seed=31, dtype=dt)
+    G = synth.unit_rows(ng, D, seed=32, dtype=dt)
+    G[ng - 5] = G[3]                       # exact tie far apart
+    Q[0] = G[3]
+    ts, ti = _topk(dev(Q), dev(G), k, index_base=7)
+    check_topk(host(ts), host(ti), O.scores(Q, G), k, index_base=7)
+    assert host(ti)[0, 0] == 3 + 7 and host(ti)[0, 1] == ng - 5 + 7
