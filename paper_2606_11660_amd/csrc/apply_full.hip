@@ -80,14 +80,13 @@ __global__ __launch_bounds__(256) void apply_full_kernel(
   nr = nr > GT ? GT : nr;
   int64_t nc = D - c0;
   nc = nc > GT ? GT : nc;
-  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + r0 * ldx, (uint32_t)(nr * ldx * 2));
-  const __amdgpu_buffer_rsrc_t rlo = make_rsrc(Mlo + c0 * D, (uint32_t)(nc * D * 2));
-  const __amdgpu_buffer_rsrc_t rhi = make_rsrc(Mhi + c0 * D, (uint32_t)(nc * D * 2));
+  const i32x4 dx = make_desc(X + r0 * ldx, (uint32_t)(nr * ldx * 2));
+  const i32x4 dlo = make_desc(Mlo + c0 * D, (uint32_t)(nc * D * 2));
+  const i32x4 dhi = make_desc(Mhi + c0 * D, (uint32_t)(nc * D * 2));
   GemmCore<F16Tag> core;
   core.zero();
-  const int n_stage = (int)(D / GK);
-  core.run(sm, rx, ldx, rhi, D, n_stage);
-  core.run(sm, rx, ldx, rlo, D, n_stage);
+  const int n_st = (int)(D / GKS);
+  core.run(sm, dx, ldx, dhi, dlo, D, n_st, 2 * n_st);
   const float unscale = ldexpf(1.f, -split_exponent(*maxbits));
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

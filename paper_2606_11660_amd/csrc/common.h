@@ -67,6 +67,16 @@ __device__ inline void lds_dma16_nt(const i32x4& desc, uint32_t voff, uint32_t l
       : "memory", "m0");
 }
 
+// s_waitcnt lgkmcnt(0) through the builtin, so that the compiler's own wait
+// insertion knows every LDS read before it has completed (an inline-asm wait
+// is opaque to it and would be followed by redundant waits); the empty asm
+// keeps memory operations from moving across it.
+__device__ inline void wait_lgkm0() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // vmcnt 63, expcnt 7, lgkmcnt 0
+  asm volatile("" ::: "memory");
+}
+
 // One 16-byte A fragment times one 16-byte B fragment on the matrix cores,
 // accumulated into a 16x16 fp32 tile.  For bf16/fp16 a fragment is 8 values
 // of K (one 16x16x32 MFMA); for fp32 it is 4 values of K (four 16x16x4

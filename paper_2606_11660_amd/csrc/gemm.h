@@ -4,27 +4,47 @@
 //
 // One workgroup (4 waves, 2 x 2) owns a 256 x 256 tile of C; each wave holds
 // a 128 x 128 sub-tile as 8 x 8 MFMA accumulators (256 accumulator
-// registers).  K advances in stages of 64 (128 bytes per row): every stage of
-// A and B (32 KB each) is loaded with line-coalesced 16-byte loads (8 lanes
-// per 128-byte row segment), parked in registers while the previous stage
-// computes, and written to an XOR-swizzled LDS buffer (chunk ^ row % 8) from
-// which MFMA fragments are read without bank conflicts.  Two LDS buffers,
-// one barrier per stage.  Rows outside [0, M) / [0, N) read as zeros through
-// the buffer resources' range check.
+// registers).  K advances in stages of 64 (128 bytes per row).  Every stage of
+// A and B (32 KB each) goes from memory straight into one of two LDS slots by
+// direct-to-LDS buffer loads (8 rows x 128 bytes per instruction, 16
+// instructions per wave and stage), so no operand passes through registers
+// on its way to LDS and no wave spends instructions on LDS stores.  In LDS a
+// row is 128 bytes; its 16-byte chunk c sits in slot c ^ (row % 8), which the
+// loads produce by fetching the permuted chunk, so that the MFMA fragment
+// reads hit distinct bank groups.
+//
+// A stage is consumed as two K-halves, h0 and h1, each 64 MFMAs from 16
+// fragments held in registers (two fragment sets).  The step of stage s
+// runs: wait for stage s, barrier (stage s visible to every
+// wave; every wave has finished reading stage s - 1, whose slot is then
+// refilled with stage s + 1), then the MFMAs of h1 of stage s - 1 while the
+// fragments of h0 of stage s are read, then the MFMAs of h0 of stage s while
+// the fragments of h1 of stage s are read.  The 16 loads of stage s + 1 are
+// spread over the first 64 MFMAs of the step (two per 8: late enough not to
+// fill the address queue in one burst, early enough to land before the next
+// step), the 32 fragment reads over all 128 (two per 8): issued in bursts
+// they fill the address and LDS command queues and stall the wave, and with
+// it the matrix core.  Rows outside the operand's
+// range read as zeros through the buffer descriptors' range check.
 #pragma once
 
 #include "common.h"
 
 namespace attr {
 
-constexpr int GT = 256;         // block tile (rows of A and of B)
-constexpr int GK = 64;          // K per stage (elements; 128 bytes)
-constexpr int G_STAGE_BYTES = GT * 128;  // one operand, one stage
+constexpr int GT = 256;                  // block tile (rows of A and of B)
+constexpr int GKS = 64;                  // K per stage (elements; 128 bytes)
+constexpr uint32_t G_SLOT = GT * 128;    // bytes per operand per slot
 
 struct GemmSmem {
   i32x4 a[2][GT * 8];
   i32x4 b[2][GT * 8];
 };
+
+template <int N>
+__device__ inline void gemm_wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 template <typename Tag>
 struct GemmCore {
@@ -37,77 +57,122 @@ struct GemmCore {
       for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  __device__ inline void scale(float s) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) acc[i][j] *= s;
-  }
-
-  // Accumulate K in [0, n_stage * 64) of rows (a rows rsrc ra, stride lda
-  // elements; b rows rsrc rb, stride ldb).  Both resources start at the
-  // tile's first row.
-  __device__ inline void run(GemmSmem& sm, __amdgpu_buffer_rsrc_t ra, int64_t lda,
-                             __amdgpu_buffer_rsrc_t rb, int64_t ldb, int n_stage) {
-    const int t = threadIdx.x;
-    const int wave = t >> 6, lane = t & 63;
+  // Accumulate n_st stages (K = 64 n_st) of the tile's rows: A rows through
+  // descriptor da (row stride lda elements), B rows through db (stride ldb);
+  // both descriptors start at the tile's first row.  Stages [0, n_sw) take
+  // K = [0, 64 n_sw) of A and of db; stages [n_sw, n_st) take K restarting
+  // from 0 of A and of db2 (two products summed into one accumulator).  Byte
+  // offsets within a descriptor must fit 31 bits.
+  __device__ inline void run(GemmSmem& sm, const i32x4& da, int64_t lda, const i32x4& db,
+                             const i32x4& db2, int64_t ldb, int n_sw, int n_st) {
+    if (n_st <= 0) return;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
     const int wm = wave >> 1, wn = wave & 1;
-    // load mapping: instruction j (0..7) of a wave covers rows 64 wave + 8 j + lane / 8
-    const int lrow = lane >> 3, lch = lane & 7;
-    const uint32_t a_off0 = (uint32_t)((int64_t)(64 * wave + lrow) * lda * 2 + lch * 16);
-    const uint32_t b_off0 = (uint32_t)((int64_t)(64 * wave + lrow) * ldb * 2 + lch * 16);
-    const uint32_t a_step8 = (uint32_t)(8 * lda * 2), b_step8 = (uint32_t)(8 * ldb * 2);
-    // LDS slots written by this lane (row r = 64 wave + 8 j + lrow, r % 8 == lrow)
-    const int wslot0 = (64 * wave + lrow) * 8 + (lch ^ lrow);
-    // fragment read slots
-    const int ri = lane & 15, rg = lane >> 4;
-
-    i32x4 ga[8], gb[8];
-    auto gload = [&](int st) {
-      const uint32_t ko = (uint32_t)st * 128u;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) ga[j] = load16_cached(ra, a_off0 + j * a_step8 + ko);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) gb[j] = load16_cached(rb, b_off0 + j * b_step8 + ko);
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) sm.a[buf][wslot0 + j * 64] = ga[j];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) sm.b[buf][wslot0 + j * 64] = gb[j];
-    };
-    auto compute = [&](int buf) {
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        i32x4 fa[8], fb[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int row = 128 * wm + 16 * i + ri;
-          fa[i] = sm.a[buf][row * 8 + ((4 * s + rg) ^ (row & 7))];
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int row = 128 * wn + 16 * j + ri;
-          fb[j] = sm.b[buf][row * 8 + ((4 * s + rg) ^ (row & 7))];
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-#pragma unroll
-          for (int j = 0; j < 8; ++j) acc[i][j] = mma16(Tag{}, fa[i], fb[j], acc[i][j]);
+    // loads: instruction h (0..7) of a wave covers rows 64 wave + 8 h + lane / 8;
+    // the lane's LDS slot (lane % 8) receives chunk (lane % 8) ^ (lane / 8)
+    const int lr = lane >> 3;
+    const int lc = (lane & 7) ^ lr;
+    const uint32_t a_off = (uint32_t)((int64_t)(64 * wave + lr) * lda * 2 + lc * 16);
+    const uint32_t b_off = (uint32_t)((int64_t)(64 * wave + lr) * ldb * 2 + lc * 16);
+    const uint32_t a8 = (uint32_t)(8 * lda * 2), b8 = (uint32_t)(8 * ldb * 2);
+    const uint32_t lds_a = (uint32_t)(uintptr_t)&sm.a[0][0] + (uint32_t)(64 * wave) * 128u;
+    const uint32_t lds_b = (uint32_t)(uintptr_t)&sm.b[0][0] + (uint32_t)(64 * wave) * 128u;
+    // load instruction c (0..15) of stage st: A rows for c < 8, B rows after.
+    // A stage past the end is issued with every lane out of range: it
+    // fetches nothing and zero-fills a slot that is no longer read.
+    auto issue_one = [&](int st, int c) {
+      const bool sw = st >= n_sw;
+      const uint32_t ko = (uint32_t)(sw ? st - n_sw : st) * 128u + (st < n_st ? 0u : 0x80000000u);
+      const uint32_t sb = (uint32_t)(st & 1) * G_SLOT;
+      const int h = c & 7;
+      if (c < 8) {
+        lds_dma16(da, a_off + h * a8 + ko, lds_a + sb + h * 1024u);
+      } else {
+        lds_dma16(sw ? db2 : db, b_off + h * b8 + ko, lds_b + sb + h * 1024u);
       }
     };
+    // fragment reads: lane (ri, rg) takes row 16 t + ri, chunk 4 half + rg in
+    // slot (4 half + rg) ^ (ri % 8)
+    const int ri = lane & 15, rg = lane >> 4;
+    const int fa0 = (128 * wm + ri) * 8, fb0 = (128 * wn + ri) * 8;
+    const int fs0 = rg ^ (ri & 7), fs1 = (4 + rg) ^ (ri & 7);
+    // the 16 fragments of a half, two per call, B first: every MFMA row needs
+    // all of B but only its own row of A
+    auto read_pair = [&](int i, const i32x4* pa, const i32x4* pb, int fs, i32x4 (&fa)[8],
+                         i32x4 (&fb)[8]) {
+      if (i < 4) {
+        fb[2 * i] = pb[fb0 + 128 * (2 * i) + fs];
+        fb[2 * i + 1] = pb[fb0 + 128 * (2 * i + 1) + fs];
+      } else {
+        fa[2 * i - 8] = pa[fa0 + 128 * (2 * i - 8) + fs];
+        fa[2 * i - 7] = pa[fa0 + 128 * (2 * i - 7) + fs];
+      }
+    };
+    auto mma_row = [&](int i, const i32x4 (&fa)[8], const i32x4 (&fb)[8]) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = mma16(Tag{}, fa[i], fb[j], acc[i][j]);
+    };
+    i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
 
-    if (n_stage <= 0) return;
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int st = 0; st < n_stage; ++st) {
-      const bool more = st + 1 < n_stage;
-      if (more) gload(st + 1);
-      compute(st & 1);
-      if (more) lstore((st + 1) & 1);
-      __syncthreads();
+    // prologue: stage 0 in, stage 1 on its way, h0 of stage 0 in registers
+#pragma unroll
+    for (int c = 0; c < 16; ++c) issue_one(0, c);
+    gemm_wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+#pragma unroll
+    for (int c = 0; c < 16; ++c) issue_one(1, c);
+    {
+      const i32x4* pa = sm.a[0];
+      const i32x4* pb = sm.b[0];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        h0a[i] = pa[fa0 + 128 * i + fs0];
+        h0b[i] = pb[fb0 + 128 * i + fs0];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, pa, pb, fs1, h1a, h1b);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_row(i, h0a, h0b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
+    for (int st = 1; st < n_st; ++st) {
+      // stage st landed (nothing later is in flight); this wave's reads of
+      // stage st - 1 are complete
+      gemm_wait_vm<0>();
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+      const i32x4* pa = sm.a[st & 1];
+      const i32x4* pb = sm.b[st & 1];
+      // h1 of stage st - 1, reading h0 of stage st, loading stage st + 1
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, pa, pb, fs0, h0a, h0b);
+        issue_one(st + 1, 2 * i);
+        issue_one(st + 1, 2 * i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_row(i, h1a, h1b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // h0 of stage st, reading h1 of stage st
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, pa, pb, fs1, h1a, h1b);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_row(i, h0a, h0b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // h1 of the last stage
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);
+    // the zero-filling loads past the end have landed and every wave's LDS
+    // reads are complete before the caller reuses the slots
+    gemm_wait_vm<0>();
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
   }
 
   // Row / column of accumulator element (i, j, r) for this lane.

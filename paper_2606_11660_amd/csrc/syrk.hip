@@ -71,26 +71,58 @@ __device__ inline void upper_tile(int u, int nt, int& tp, int& tq) {
   tq = p + u;
 }
 
+// Upper-triangle tile v in band order: bands of 4 tile rows, each walked
+// column by column (the rows of a band first), so that consecutive tiles
+// share their row blocks.
+__device__ inline void band_tile(int v, int nt, int& tp, int& tq) {
+  tp = 0;
+  tq = 0;
+  for (int b0 = 0; b0 < nt; b0 += 4) {
+    const int bh = nt - b0 < 4 ? nt - b0 : 4;
+    const int cnt = bh * (bh + 1) / 2 + (nt - b0 - bh) * bh;
+    if (v < cnt) {
+      for (int q = b0; q < nt; ++q) {
+        const int c = q - b0 + 1 < bh ? q - b0 + 1 : bh;
+        if (v < c) {
+          tp = b0 + v;
+          tq = q;
+          return;
+        }
+        v -= c;
+      }
+    }
+    v -= cnt;
+  }
+}
+
+// Work item of workgroup b: workgroups go to the 8 XCDs round robin
+// (b % 8), so XCD x is given the contiguous item range [x per_xcd,
+// (x + 1) per_xcd) in dispatch order; items are slice-major and band-ordered
+// within a slice, so the workgroups resident on one XCD at a time share row
+// blocks through its L2.
 template <typename Tag, typename T>
 __global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ XT, int64_t C,
-                                                   int64_t D, int nt, int n_up, int64_t Cs,
+                                                   int64_t D, int nt, int n_up, int J,
+                                                   int per_xcd, int64_t Cs,
                                                    float* __restrict__ part) {
   __shared__ GemmSmem sm;
-  const int u = (int)(blockIdx.x % (uint32_t)n_up);
-  const int j = (int)(blockIdx.x / (uint32_t)n_up);
+  const int item = (int)(blockIdx.x & 7u) * per_xcd + (int)(blockIdx.x >> 3);
+  if (item >= n_up * J) return;  // uniform
+  const int j = item / n_up;
   int tp, tq;
-  upper_tile(u, nt, tp, tq);
+  band_tile(item - j * n_up, nt, tp, tq);
+  const int u = tp * nt - tp * (tp - 1) / 2 + (tq - tp);  // row-major upper index
   int64_t np = D - (int64_t)tp * GT, nq = D - (int64_t)tq * GT;
   np = np > GT ? GT : np;
   nq = nq > GT ? GT : nq;
   const T* a = XT + (int64_t)tp * GT * C + (int64_t)j * Cs;
   const T* b = XT + (int64_t)tq * GT * C + (int64_t)j * Cs;
   // range: the tile's rows, each C long (the K window is [0, Cs) of that)
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(a, (uint32_t)((np - 1) * C * 2 + Cs * 2));
-  const __amdgpu_buffer_rsrc_t rb = make_rsrc(b, (uint32_t)((nq - 1) * C * 2 + Cs * 2));
+  const i32x4 da = make_desc(a, (uint32_t)((np - 1) * C * 2 + Cs * 2));
+  const i32x4 db = make_desc(b, (uint32_t)((nq - 1) * C * 2 + Cs * 2));
   GemmCore<Tag> core;
   core.zero();
-  core.run(sm, ra, C, rb, C, (int)(Cs / GK));
+  core.run(sm, da, C, db, db, C, (int)(Cs / GKS), (int)(Cs / GKS));
   float* dst = part + ((int64_t)j * n_up + u) * TILE_E;
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -172,13 +204,14 @@ hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, in
     else
       hipLaunchKernelGGL(transpose_kernel<_Float16>, gt, dim3(256), 0, s, (const _Float16*)X, ldx,
                          n_rows, r0, D, P.C, (_Float16*)xt);
-    dim3 gs((unsigned)(P.n_up * P.J));
+    const int per_xcd = (P.n_up * P.J + 7) / 8;
+    dim3 gs((unsigned)(8 * per_xcd));
     if (bf16)
       hipLaunchKernelGGL((syrk_kernel<Bf16Tag, __bf16>), gs, dim3(256), 0, s, (const __bf16*)xt, P.C,
-                         D, P.nt, P.n_up, P.Cs, (float*)part);
+                         D, P.nt, P.n_up, P.J, per_xcd, P.Cs, (float*)part);
     else
       hipLaunchKernelGGL((syrk_kernel<F16Tag, _Float16>), gs, dim3(256), 0, s, (const _Float16*)xt,
-                         P.C, D, P.nt, P.n_up, P.Cs, (float*)part);
+                         P.C, D, P.nt, P.n_up, P.J, per_xcd, P.Cs, (float*)part);
     hipLaunchKernelGGL(syrk_reduce_kernel, dim3((unsigned)((n_e + 255) / 256)), dim3(256), 0, s,
                        (const float*)part, P.J, n_e, (double*)h64);
     e = hipGetLastError();
