@@ -76,6 +76,24 @@ def _cpu_baseline(n_sample: int = 6, min_seconds: float = 12.0):
 
 
 
+def _measured_traffic():
+    """HBM bytes per attr_project call from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE runs, scaled by the copy-kernel
+    calibration), or None when the projection source has changed since the
+    counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "project_gpt2_traffic.txt")
+    src = os.path.join(ROOT, "paper_2606_11660_amd", "csrc", "project.hip")
+    try:
+        fields = dict(line.split(": ", 1) for line in open(path).read().splitlines() if ": " in line)
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        if fields.get("source_sha256_16", "").strip() != digest:
+            return None
+        return int(fields["traffic_bytes_per_call"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def _timeit(fn, stream, reps):
     import torch
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -314,8 +332,9 @@ def main():
                                "batch 64 per step, fp16 store, 64 queries top-10 merged per step",
                    "global_batch": B, "seq_len": T, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
-                     "kernel": "attr_project (project_main_kernel<bf16,k=16>)",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": _measured_traffic(),
+                     "kernel": "attr_project call: 2 x project_pack_kernel + project_main_kernel"
+                               "<bf16,k=16> + project_reduce_kernel",
                      "bytes_per_launch": proj_bytes, "ms_per_launch": proj_ms},
         "store_scan": {"queries": wl.n_queries, "rows": n_store, "D": D, "k": wl.topk,
                        "ms": scan_ms, "pairs_per_s": wl.n_queries * n_store / (scan_ms * 1e-3),

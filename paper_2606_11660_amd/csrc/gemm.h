@@ -20,7 +20,7 @@
 // refilled with stage s + 1), then the MFMAs of h1 of stage s - 1 while the
 // fragments of h0 of stage s are read, then the MFMAs of h0 of stage s while
 // the fragments of h1 of stage s are read.  The 16 loads of stage s + 1 are
-// spread over the first 64 MFMAs of the step (two per 8: late enough not to
+// spread over the first 64 MFMAs of the step (one per 4: late enough not to
 // fill the address queue in one burst, early enough to land before the next
 // step), the 32 fragment reads over all 128 (two per 8): issued in bursts
 // they fill the address and LDS command queues and stall the wave, and with
@@ -151,9 +151,14 @@ struct GemmCore {
       for (int i = 0; i < 8; ++i) {
         read_pair(i, pa, pb, fs0, h0a, h0b);
         issue_one(st + 1, 2 * i);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
         issue_one(st + 1, 2 * i + 1);
         __builtin_amdgcn_sched_barrier(0);
-        mma_row(i, h1a, h1b);
+#pragma unroll
+        for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
       // h0 of stage st, reading h1 of stage st
