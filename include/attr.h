@@ -177,13 +177,17 @@ attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows
 
 /* For every query q: s_qj = <Q_q, G_j> (fp32 accumulation; the cosine when
  * both sides are unit rows) over the n_g store rows, and the k best
- * (index_base + j) ordered by (score desc, index asc); NaN scores are never
- * selected; missing slots are (-inf, -1).  The Q x n_g score matrix is never
- * written to memory (exact top-k lookup, section "Attribution Pipelines").
+ * (index_base + j) ordered by (score desc, index asc); NaN and -inf scores
+ * are never selected; missing slots are (-inf, -1).  Exact top-k lookup,
+ * section "Attribution Pipelines".  With few queries the scan streams the
+ * store once and the score matrix never reaches memory; with many fp16
+ * queries (n_q >= 128) it is computed chunk by chunk into the workspace
+ * (~256 MB per chunk) and selected exactly from there.
  *
  *   Q, ldq       device [n_q, D];  G, ldg: device [n_g, D]; both `dtype`
  *                (ATTR_F16 or ATTR_F32); D a multiple of 64 (fp16) or 32
- *                (fp32); n_q, n_g below 2^31
+ *                (fp32); n_q, n_g below 2^31; 256 rows of either operand
+ *                must span less than 2 GiB (ld * 256 * element size)
  *   k            1..128
  *   index_base   added to the local row index j (store offset of G), >= 0
  *   merge        0: overwrite top_*;  1: top_* hold a previous sorted

@@ -408,8 +408,8 @@ attr_status attr_score_topk(const void* Q, int64_t n_q, int64_t ldq, const void*
     if (ldq < D || ldg < D) return fail(ATTR_ERR_INVALID_ARG, "ldq/ldg < D");
     if (ldq % (16 / eb) || ldg % (16 / eb))
       return fail(ATTR_ERR_ALIGNMENT, "ldq/ldg must keep rows 16-byte aligned");
-    if (ldq * 64 * eb >= (1ll << 31) || ldg * 32 * eb >= (1ll << 31))
-      return fail(ATTR_ERR_UNSUPPORTED, "row stride too large");
+    if (ldq * 256 * eb >= (1ll << 31) || ldg * 256 * eb >= (1ll << 31))
+      return fail(ATTR_ERR_UNSUPPORTED, "row stride too large (256 rows must span < 2 GiB)");
     if (merge != 0 && merge != 1) return fail(ATTR_ERR_INVALID_ARG, "merge must be 0 or 1");
     if (index_base < 0 || index_base > (1ll << 62))
       return fail(ATTR_ERR_INVALID_ARG, "index_base must be in [0, 2^62]");

@@ -80,8 +80,10 @@ struct ScorePlan {
   int n_tiles;           // 128-row tiles (split-K plan)
   int n_parts;           // row partitions, one sorted list each per query
   int64_t rows_per_part;
-  size_t spart_bytes;    // split-K partial scores
+  size_t spart_bytes;    // split-K partial scores / GEMM-plan score chunk
   size_t list_entries;   // n_q * n_parts * k
+  int gemm;              // GEMM plan: row chunks of `chunk` rows, one list per chunk
+  int64_t chunk;
 };
 ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes);
 hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int64_t n_q,

@@ -18,6 +18,7 @@
 // arg-max in (score desc, index asc) order, which also merges a previous
 // result when a store is scored chunk by chunk.
 #include "common.h"
+#include "gemm.h"
 #include "kernels.h"
 
 namespace attr {
@@ -467,6 +468,221 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// GEMM plan (many queries: the scan is bound by the matrix cores)
+// ---------------------------------------------------------------------------
+// The store is taken in chunks of rows.  For each chunk the 256 x 256 block
+// GEMM core computes the fp32 score matrix S[q][r] into the workspace (sized
+// to stay in the MALL), then one workgroup per query selects that chunk's
+// top k exactly:
+//  * a strided sample of 2048 scores is sorted; the sample at a rank chosen
+//    so that ~2k + 256 scores are expected above it is a threshold tau;
+//  * one pass collects the scores >= tau into LDS (counting them all); if
+//    there are at least k of them the top k are all among them (the k-th
+//    best is >= tau), and if at most 4096 a bitonic sort orders them by
+//    (score desc, index asc) and the first k are the chunk's list;
+//  * otherwise tau moves by bisection over the sample ranks (more passes);
+//    if no rank works (a chunk of massive ties or one ordered against the
+//    sample), k arg-max passes over the chunk give the same list exactly.
+// Chunks of at most 4096 rows are sorted whole.  NaN and -inf scores are
+// never selected; lists are padded with (-inf, -1).  Chunk lists are merged
+// by the common merge kernel.
+constexpr int RS_CAP = 4096;  // candidates sorted per (query, chunk)
+constexpr int RS_SMP = 2048;  // threshold samples
+
+template <typename Tag>
+__global__ __launch_bounds__(256) void score_gemm_kernel(
+    const _Float16* __restrict__ Q, int64_t n_q, int64_t ldq, const _Float16* __restrict__ G,
+    int64_t nc, int64_t ldg, int n_qt, int n_items, int per_xcd, int n_st,
+    float* __restrict__ S, int64_t lds) {
+  __shared__ GemmSmem sm;
+  // XCD x (workgroup b goes to XCD b % 8) takes a contiguous range of
+  // (query tile fastest, row tile) items: the query tiles of one row tile
+  // read the same store rows through the same L2
+  const int item = (int)(blockIdx.x & 7u) * per_xcd + (int)(blockIdx.x >> 3);
+  if (item >= n_items) return;  // uniform
+  const int qt = item % n_qt, rt = item / n_qt;
+  const int64_t q0 = (int64_t)qt * GT, c0 = (int64_t)rt * GT;
+  int64_t nq = n_q - q0, nr = nc - c0;
+  nq = nq > GT ? GT : nq;
+  nr = nr > GT ? GT : nr;
+  const i32x4 dq = make_desc(Q + q0 * ldq, (uint32_t)(nq * ldq * 2));
+  const i32x4 dg = make_desc(G + c0 * ldg, (uint32_t)(nr * ldg * 2));
+  GemmCore<Tag> core;
+  core.zero();
+  core.run(sm, dq, ldq, dg, dg, ldg, n_st, n_st);
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = GemmCore<Tag>::row_of(i, r);
+      if (row < nq) {
+        float* dst = S + (q0 + row) * lds + c0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int col = GemmCore<Tag>::col_of(j);
+          if (col < nr) dst[col] = core.acc[i][j][r];
+        }
+      }
+    }
+}
+
+// Order-preserving key of a float (larger float, larger key).  Selectable
+// scores are those above -inf and not NaN: keys in (fkey(-inf), fkey(+inf)].
+__device__ inline uint32_t fkey(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ inline float fkey_inv(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
+}
+__device__ inline bool selectable(uint32_t key) { return key > 0x007fffffu && key <= 0xff800000u; }
+// (score desc, index asc) as one descending 64-bit key; 0 is padding
+__device__ inline uint64_t rs_key(uint32_t key, int64_t j) {
+  return ((uint64_t)key << 32) | (uint64_t)(0xffffffffu - (uint32_t)j);
+}
+
+// Descending bitonic sort of n (a power of two) keys in LDS, 256 threads.
+template <typename T>
+__device__ inline void bitonic_desc(T* a, int n) {
+  for (int size = 2; size <= n; size <<= 1)
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      __syncthreads();
+      for (int t = threadIdx.x; t < n / 2; t += 256) {
+        const int i = 2 * t - (t & (stride - 1));
+        const int j = i + stride;
+        const T x = a[i], y = a[j];
+        const bool down = (i & size) == 0;
+        if (down ? (x < y) : (x > y)) {
+          a[i] = y;
+          a[j] = x;
+        }
+      }
+    }
+  __syncthreads();
+}
+
+__device__ inline uint64_t block_max_u64(uint64_t v, uint64_t* red) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, off, kWave);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), off, kWave);
+    const uint64_t o = ((uint64_t)hi << 32) | lo;
+    v = o > v ? o : v;
+  }
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint64_t m = red[0];
+#pragma unroll
+  for (int w = 1; w < 4; ++w) m = red[w] > m ? red[w] : m;
+  return m;
+}
+
+__global__ __launch_bounds__(256) void score_rselect_kernel(
+    const float* __restrict__ S, int64_t lds, int64_t nc, int k, int part, int n_parts,
+    int64_t index_base, float* __restrict__ part_s, int64_t* __restrict__ part_i) {
+  __shared__ uint64_t cand[RS_CAP];
+  __shared__ uint32_t smp[RS_SMP];
+  __shared__ uint64_t red_u[4];
+  __shared__ int n_cand;
+  const int64_t q = blockIdx.x;
+  const int t = threadIdx.x;
+  const float* s = S + q * lds;
+  float* ds = part_s + (q * n_parts + part) * (int64_t)k;
+  int64_t* di = part_i + (q * n_parts + part) * (int64_t)k;
+
+  // collect every selectable score >= tau (up to RS_CAP of them); returns
+  // how many there are
+  auto take = [&](float v, int64_t j, uint32_t tau) {
+    const uint32_t key = fkey(v);
+    if (selectable(key) && key >= tau) {
+      const int p = atomicAdd(&n_cand, 1);
+      if (p < RS_CAP) cand[p] = rs_key(key, j);
+    }
+  };
+  auto collect = [&](uint32_t tau) -> int {
+    __syncthreads();
+    if (t == 0) n_cand = 0;
+    __syncthreads();
+    // rows of S start 1 KB aligned (lds is a multiple of 256)
+    const f32x4* s4 = reinterpret_cast<const f32x4*>(s);
+    const int64_t n4 = nc >> 2;
+    for (int64_t j4 = t; j4 < n4; j4 += 256) {
+      const f32x4 v = s4[j4];
+      take(v[0], 4 * j4, tau);
+      take(v[1], 4 * j4 + 1, tau);
+      take(v[2], 4 * j4 + 2, tau);
+      take(v[3], 4 * j4 + 3, tau);
+    }
+    for (int64_t j = 4 * n4 + t; j < nc; j += 256) take(s[j], j, tau);
+    __syncthreads();
+    return n_cand;
+  };
+
+  bool ok = false;
+  int c = 0;
+  if (nc <= RS_CAP) {
+    c = collect(0x00800000u);  // every selectable score
+    ok = true;
+  } else {
+    for (int j = t; j < RS_SMP; j += 256) {
+      const uint32_t key = fkey(s[(int64_t)j * nc / RS_SMP]);
+      smp[j] = selectable(key) ? key : 0u;
+    }
+    bitonic_desc(smp, RS_SMP);
+    int lo = 0, hi = RS_SMP - 1;
+    int rho = (int)(((int64_t)(2 * k + 256) * RS_SMP + nc - 1) / nc) - 1;
+    rho = rho < 0 ? 0 : (rho > hi ? hi : rho);
+    while (lo <= hi) {
+      const uint32_t tau = smp[rho];
+      if (tau == 0u) {  // fewer selectable samples than rho + 1
+        hi = rho - 1;
+      } else {
+        c = collect(tau);
+        if (c >= k && c <= RS_CAP) {
+          ok = true;
+          break;
+        }
+        if (c < k) lo = rho + 1;
+        else hi = rho - 1;
+      }
+      rho = (lo + hi) / 2;
+    }
+  }
+  if (ok) {
+    int n_sort = 64;  // power of two >= max(c, k)
+    while (n_sort < c || n_sort < k) n_sort <<= 1;
+    for (int j = c + t; j < n_sort; j += 256) cand[j] = 0ull;
+    bitonic_desc(cand, n_sort);
+    for (int j = t; j < k; j += 256) {
+      const uint64_t e = cand[j];
+      ds[j] = e ? fkey_inv((uint32_t)(e >> 32)) : -__builtin_inff();
+      di[j] = e ? index_base + (int64_t)(0xffffffffu - (uint32_t)e) : -1;
+    }
+  } else {
+    // exact: the r-th entry is the largest key below the (r-1)-th
+    uint64_t prev = ~0ull;
+    for (int r = 0; r < k; ++r) {
+      uint64_t best = 0ull;
+      if (prev != 0ull)
+        for (int64_t j = t; j < nc; j += 256) {
+          const uint32_t key = fkey(s[j]);
+          if (selectable(key)) {
+            const uint64_t e = rs_key(key, j);
+            if (e < prev && e > best) best = e;
+          }
+        }
+      best = block_max_u64(best, red_u);
+      if (t == 0) {
+        ds[r] = best ? fkey_inv((uint32_t)(best >> 32)) : -__builtin_inff();
+        di[r] = best ? index_base + (int64_t)(0xffffffffu - (uint32_t)best) : -1;
+      }
+      prev = best;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // split-K plan
 // ---------------------------------------------------------------------------
 // Partial scores of (query block, row tile, D-slice) -> spart[slice][row][q].
@@ -661,6 +877,27 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
   P.n_qb = (int)((n_q + SQB - 1) / SQB);
   P.n_grp = (int)(D * elem_bytes / 128);
   if (n_q <= 0 || n_g <= 0) return P;
+  if (elem_bytes == 2 && D % GKS == 0 && n_q >= 128 && n_g >= 4096) {
+    // GEMM plan: score chunks of at most ~256 MB (MALL-resident between the
+    // GEMM and the selection) and 128K rows, at most 255 chunks (the merge
+    // takes 256 sources)
+    int64_t chunk = ((int64_t)256 << 20) / (n_q * 4);
+    chunk = chunk > 131072 ? 131072 : chunk;  // <= 32 rows per threshold sample
+    const int64_t min_chunk = (n_g + 254) / 255;
+    chunk = chunk < min_chunk ? min_chunk : chunk;
+    chunk = chunk < 4096 ? 4096 : chunk;
+    chunk = (chunk + GT - 1) / GT * GT;
+    const int64_t all = (n_g + GT - 1) / GT * GT;
+    chunk = chunk > all ? all : chunk;
+    P.gemm = 1;
+    P.chunk = chunk;
+    P.n_parts = (int)((n_g + chunk - 1) / chunk);
+    P.rows_per_part = chunk;
+    P.split = 1;
+    P.spart_bytes = (size_t)n_q * (size_t)chunk * 4;
+    P.list_entries = (size_t)n_q * (size_t)P.n_parts * (size_t)k;
+    return P;
+  }
   const int64_t n_tiles = (n_g + STN - 1) / STN;
   // Too few (query block, row tile) pairs to occupy 256 CUs: split D.
   int64_t split = 1;
@@ -706,7 +943,24 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
                              int64_t index_base, int merge, float* top_s, int64_t* top_i,
                              float* part_s, int64_t* part_i, float* spart, hipStream_t s) {
   const int n_parts = n_g > 0 ? plan.n_parts : 0;
-  if (n_g > 0 && plan.split <= 1) {
+  if (n_g > 0 && plan.gemm) {
+    const int n_qt = (int)((n_q + GT - 1) / GT);
+    const int n_st = plan.n_grp;  // 64-element fp16 stages (128 bytes)
+    for (int c = 0; c < plan.n_parts; ++c) {
+      const int64_t r0 = (int64_t)c * plan.chunk;
+      const int64_t nc = n_g - r0 < plan.chunk ? n_g - r0 : plan.chunk;
+      const int n_items = n_qt * (int)((nc + GT - 1) / GT);
+      const int per_xcd = (n_items + 7) / 8;
+      hipLaunchKernelGGL(score_gemm_kernel<F16Tag>, dim3((unsigned)(8 * per_xcd)), dim3(256), 0, s,
+                         (const _Float16*)Q, n_q, ldq, (const _Float16*)G + r0 * ldg, nc, ldg, n_qt,
+                         n_items, per_xcd, n_st, spart, plan.chunk);
+      hipLaunchKernelGGL(score_rselect_kernel, dim3((unsigned)n_q), dim3(256), 0, s,
+                         (const float*)spart, plan.chunk, nc, k, c, plan.n_parts,
+                         index_base + r0, part_s, part_i);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  } else if (n_g > 0 && plan.split <= 1) {
     const int parts_pad = (plan.n_parts + 7) / 8 * 8;
     dim3 grid((unsigned)(plan.n_qb * parts_pad)), block(256);
 #define ATTR_SS(F, KM, RG)                                                                    \

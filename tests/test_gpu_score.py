@@ -137,7 +137,7 @@ def test_gpt2_store_scan():
     check_topk(host(ts), host(ti), O.scores(Q, G), 10)
 
 
-@pytest.mark.parametrize("nq,ng,D,k,dt", [(300, 9000, 256, 100, np.float16),
+@pytest.mark.parametrize("nq,ng,D,k,dt", [(100, 9000, 256, 100, np.float16),
                                           (40, 40001, 128, 10, np.float16),
                                           (70, 33000, 96, 5, np.float32),
                                           (17, 70000, 64, 128, np.float16)])
@@ -152,3 +152,82 @@ def test_streaming_plan(nq, ng, D, k, dt):
     ts, ti = _topk(dev(Q), dev(G), k, index_base=7)
     check_topk(host(ts), host(ti), O.scores(Q, G), k, index_base=7)
     assert host(ti)[0, 0] == 3 + 7 and host(ti)[0, 1] == ng - 5 + 7
+
+
+# ---------------------------------------------------------------------------
+# GEMM plan (fp16, n_q >= 128, n_g >= 4096): chunked score matrix + exact
+# per-chunk selection
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("nq,ng,D,k", [(130, 5000, 256, 10), (300, 9000, 256, 100),
+                                       (257, 4100, 64, 128)])
+def test_gemm_plan(nq, ng, D, k):
+    """Ragged query tiles (130, 257 = 256 + 1) and row tiles, a tie far apart,
+    a NaN row that must never be selected."""
+    say(f"case: gemm plan nq={nq} ng={ng} D={D} k={k}")
+    Q = synth.unit_rows(nq, D, seed=41)
+    G = synth.unit_rows(ng, D, seed=42)
+    G[ng - 5] = G[3]
+    Q[0] = G[3]
+    G[17] = np.nan
+    ts, ti = _topk(dev(Q), dev(G), k, index_base=11)
+    ref = O.scores(Q, G)
+    ref[:, 17] = -np.inf                  # NaN is never selected
+    gi = host(ti)
+    assert not (gi == 17 + 11).any()
+    check_topk(host(ts), gi, ref, k, index_base=11)
+    assert gi[0, 0] == 3 + 11 and gi[0, 1] == ng - 5 + 11
+
+
+def test_gemm_plan_several_chunks():
+    """8192 queries make 8192-row chunks: a 20000-row store is three chunks
+    (the last ragged); sampled queries are checked against the oracle, and
+    the result equals two merged calls."""
+    say("case: gemm plan, three chunks")
+    nq, ng, D, k = 8192, 20000, 64, 16
+    Q = synth.unit_rows(nq, D, seed=43)
+    G = synth.unit_rows(ng, D, seed=44)
+    G[19990] = G[5]                       # tie across chunks
+    Q[7] = G[5]
+    Qd, Gd = dev(Q), dev(G)
+    ts, ti = _topk(Qd, Gd, k)
+    sample = np.r_[0:8, 4000:4008, nq - 8:nq]
+    check_topk(host(ts)[sample], host(ti)[sample], O.scores(Q[sample], G), k)
+    assert host(ti)[7, 0] == 5 and host(ti)[7, 1] == 19990
+    ts2 = torch.empty_like(ts)
+    ti2 = torch.empty_like(ti)
+    P.attr_score_topk(Qd, Gd[:9000], k, ts2, ti2)
+    P.attr_score_topk(Qd, Gd[9000:], k, ts2, ti2, index_base=9000, merge=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(ti2), host(ti))
+    np.testing.assert_array_equal(host(ts2), host(ts))
+
+
+def test_gemm_plan_all_ties():
+    """Every score equal: more than 2048 rows pass any threshold, so the
+    exact arg-max selection runs; ties resolve to the lowest indices."""
+    say("case: gemm plan, all scores tied")
+    nq, ng, D, k = 128, 5000, 64, 20
+    row = synth.unit_rows(1, D, seed=45)
+    G = np.repeat(row, ng, axis=0)
+    Q = synth.unit_rows(nq, D, seed=46)
+    ts, ti = _topk(dev(Q), dev(G), k)
+    np.testing.assert_array_equal(host(ti), np.tile(np.arange(k), (nq, 1)))
+    ref = O.scores(Q, G[:1])
+    assert np.abs(host(ts) - ref).max() <= 1e-3
+
+
+def test_gemm_plan_misleading_sample():
+    """Rows at the sampled positions (every 4th of 8192) score 0, the others
+    1: the sampled threshold passes 8192 rows, so the exact fallback must
+    return the first k rows scoring 1."""
+    say("case: gemm plan, sample-adversarial store")
+    nq, ng, D, k = 128, 8192, 64, 100
+    e0 = np.zeros(D, dtype=np.float16); e0[0] = 1
+    e1 = np.zeros(D, dtype=np.float16); e1[1] = 1
+    G = np.where((np.arange(ng) % 4 == 0)[:, None], e1, e0).astype(np.float16)
+    Q = np.tile(e0, (nq, 1))
+    ts, ti = _topk(dev(Q), dev(G), k)
+    want = np.flatnonzero(np.arange(ng) % 4 != 0)[:k]
+    np.testing.assert_array_equal(host(ti), np.tile(want, (nq, 1)))
+    assert (host(ts) == 1.0).all()
