@@ -109,7 +109,9 @@ def _timeit(fn, stream, reps):
 
 def _other_rows(stream, dev):
     """Timings of the preconditioner rows on the 10^6 x 8192 low-rank-plus-noise
-    store and of the 4M-row store scan (Q sweep), each against its roofline."""
+    store and of the 4M-row store scan (Q sweep: Q <= 64 runs the streaming
+    plan, HBM-bound; Q >= 128 the GEMM plan, MFMA-bound), each against its
+    roofline."""
     import torch
     import paper_2606_11660_amd as P
     out = {}
@@ -181,7 +183,8 @@ def _other_rows(stream, dev):
         ti = torch.empty((nq, 100), dtype=torch.int64, device=dev)
         ms = _timeit(lambda: P.attr_score_topk(Q, G, 100, ts, ti, stream=stream), stream, 1)
         ok = bool((ti[:16, 0] == targets).all().item())
-        scan[str(nq)] = {"ms": ms, "pairs_per_s": nq * NS / (ms * 1e-3),
+        scan[str(nq)] = {"plan": "streaming" if nq < 128 else "gemm",
+                         "ms": ms, "pairs_per_s": nq * NS / (ms * 1e-3),
                          "GBps": NS * D * 2 / ms / 1e6,
                          "frac_hbm": NS * D * 2 / ms / 1e6 / HBM_PEAK_GBPS,
                          "TFLOPs": 2.0 * nq * NS * D / ms / 1e9,
@@ -191,6 +194,44 @@ def _other_rows(stream, dev):
     del G
     torch.cuda.empty_cache()
     return out
+
+
+def _profile_row(row, dev):
+    """One row of the path on its own, sized for counter runs (rocprofv3
+    --pmc): `syrk` / `full_apply` on a 131072 x 8192 low-rank-plus-noise
+    store, `scan16` / `scan1024` on a 1M x 8192 unit fp16 store with top-100."""
+    import torch
+    import paper_2606_11660_amd as P
+    D = 8192
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(3)
+    if row in ("syrk", "full_apply"):
+        N = 131072
+        F = torch.randn((D, 64), generator=gen, device=dev)
+        Z = torch.randn((N, 64), generator=gen, device=dev)
+        X = (Z @ F.T + 0.1 * torch.randn((N, D), generator=gen, device=dev)).half()
+        del F, Z
+        if row == "syrk":
+            H = torch.zeros((D, D), dtype=torch.float32, device=dev)
+            P.attr_precond_accumulate(X, P.PRECOND_FULL, H)
+        else:
+            B = torch.randn((D, D), generator=gen, device=dev) / D ** 0.5
+            M = (B @ B.T + torch.eye(D, device=dev)).contiguous()
+            Y = torch.empty_like(X)
+            P.attr_precond_apply(X, P.PRECOND_FULL, M, True, Y)
+    else:
+        N, nq = 1_000_000, int(row[4:])
+        G = torch.empty((N, D), dtype=torch.float16, device=dev)
+        for i in range(0, N, 65536):
+            c = torch.randn((min(65536, N - i), D), generator=gen, device=dev)
+            G[i:i + c.shape[0]] = (c / c.norm(dim=1, keepdim=True)).half()
+        q = torch.randn((nq, D), generator=gen, device=dev)
+        Q = (q / q.norm(dim=1, keepdim=True)).half()
+        ts = torch.empty((nq, 100), dtype=torch.float32, device=dev)
+        ti = torch.empty((nq, 100), dtype=torch.int64, device=dev)
+        P.attr_score_topk(Q, G, 100, ts, ti)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_row": row}))
 
 
 def _copy_reference(dev):
@@ -216,6 +257,8 @@ def main():
     ap.add_argument("--quick", action="store_true", help="skip the preconditioner / store-scan rows")
     ap.add_argument("--copy-reference", action="store_true",
                     help="only run the 1 GiB copy used to calibrate traffic counters")
+    ap.add_argument("--profile-row", choices=["syrk", "full_apply", "scan16", "scan1024"],
+                    help="only run one row of the path once, for counter runs")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -234,6 +277,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.copy_reference:
         _copy_reference(dev)
+        return
+    if args.profile_row:
+        _profile_row(args.profile_row, dev)
         return
     stream = torch.cuda.Stream(device=dev)
 

@@ -72,7 +72,10 @@ __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTa
   if (j >= args.n) return;
   const PackEntry pe = args.e[j];
   char* pk = pk_base + pe.pk_off;
-  if (threadIdx.x == 0) {
+  // blockIdx.y splits a module's fragments over gridDim.y workgroups
+  const int f0 = (int)(blockIdx.y * blockDim.x + threadIdx.x);
+  const int fstep = (int)(gridDim.y * blockDim.x);
+  if (blockIdx.y == 0 && threadIdx.x == 0) {
     ProjTab t;
     t.a = pe.a;
     t.g = pe.g;
@@ -89,7 +92,7 @@ __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTa
     const char* src = (const char*)(side == 0 ? pe.S : pe.R);
     char* dst = pk + (side == 0 ? 0 : (size_t)pe.d_in * K * E_t::bytes);
     const int n_frag16 = (d / KS) * NK * kWave;  // 16-byte fragments
-    for (int f = threadIdx.x; f < n_frag16; f += blockDim.x) {
+    for (int f = f0; f < n_frag16; f += fstep) {
       const int lane = f % kWave;
       const int ct = (f / kWave) % NK;
       const int ks = f / (kWave * NK);
@@ -356,7 +359,7 @@ size_t project_packed_bytes(int64_t d_in, int64_t d_out, int k, int elem_bytes) 
 
 hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab* tab,
                                char* pk_base, hipStream_t s) {
-  dim3 grid(args.n), block(256);
+  dim3 grid(args.n, 8), block(256);
 #define ATTR_PACK(B, N) \
   hipLaunchKernelGGL((project_pack_kernel<B, N>), grid, block, 0, s, args, tab, pk_base)
   if (bf16) {
