@@ -48,13 +48,20 @@ __device__ inline i32x4 make_desc(const void* base, uint32_t bytes) {
 // zeros).  Issued through inline asm so that the compiler does not add its
 // own conservative wait before every later LDS read; the caller owns the
 // vmcnt accounting (one instruction per call) and the barrier.
+// The descriptor and the LDS base must be wave-uniform; they are passed
+// through readfirstlane so that the compiler, when it cannot prove that,
+// does not wrap the instruction in a waterfall loop.
+__device__ inline i32x4 uniform_desc(const i32x4& d) {
+  return i32x4{__builtin_amdgcn_readfirstlane(d.x), __builtin_amdgcn_readfirstlane(d.y),
+               __builtin_amdgcn_readfirstlane(d.z), __builtin_amdgcn_readfirstlane(d.w)};
+}
 __device__ inline void lds_dma16(const i32x4& desc, uint32_t voff, uint32_t lds_base) {
   asm volatile(
       "s_mov_b32 m0, %2\n\t"
       "s_nop 0\n\t"
       "buffer_load_dwordx4 %0, %1, 0 offen lds"
       :
-      : "v"(voff), "s"(desc), "s"(lds_base)
+      : "v"(voff), "s"(uniform_desc(desc)), "s"(__builtin_amdgcn_readfirstlane(lds_base))
       : "memory", "m0");
 }
 __device__ inline void lds_dma16_nt(const i32x4& desc, uint32_t voff, uint32_t lds_base) {
@@ -63,7 +70,7 @@ __device__ inline void lds_dma16_nt(const i32x4& desc, uint32_t voff, uint32_t l
       "s_nop 0\n\t"
       "buffer_load_dwordx4 %0, %1, 0 offen nt lds"
       :
-      : "v"(voff), "s"(desc), "s"(lds_base)
+      : "v"(voff), "s"(uniform_desc(desc)), "s"(__builtin_amdgcn_readfirstlane(lds_base))
       : "memory", "m0");
 }
 

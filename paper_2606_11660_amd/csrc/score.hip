@@ -252,16 +252,19 @@ struct RegList {
   }
 };
 
-template <bool F16, int KMAX, int RING>
+template <bool F16, int KMAX, int RING, int GPS>
 __global__ __launch_bounds__(256) void score_stream_kernel(
     const char* __restrict__ Q, int64_t n_q, int64_t ldq, const char* __restrict__ G,
     int64_t n_g, int64_t ldg, int n_grp, int k, int64_t rows_per_part, int n_parts, int n_qb,
     float* __restrict__ part_s, int64_t* __restrict__ part_i, int64_t index_base) {
-  static_assert(RING >= 3 && 4 * (RING - 2) <= 24, "wait_vmcnt_4m range");
+  // GPS 128-byte K-groups per stage: a stage row is RB bytes (CPR chunks),
+  // RPI rows per 1 KB load, LPW loads per wave and stage
+  constexpr int RB = 128 * GPS, CPR = 8 * GPS, RPI = 8 / GPS, LPW = 4 * GPS;
+  static_assert(RING >= 3 && LPW * (RING - 2) <= 24, "wait_vmcnt_4m range");
   using Tag = typename STag<F16>::tag;
   constexpr int EB = STag<F16>::bytes;
   constexpr int NS = (KMAX + 63) / 64;
-  __shared__ i32x4 ring[RING][(SR + SQ) * 8];  // store rows, then query rows
+  __shared__ i32x4 ring[RING][(SR + SQ) * CPR];  // store rows, then query rows
   __shared__ float2 lists[4][16][KMAX];        // per wave, per query: (score, row bits)
 
   const uint32_t b = blockIdx.x;
@@ -288,7 +291,8 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   r_end = r_end > n_g ? n_g : r_end;
   const int64_t nrows = r_end > r_begin ? r_end - r_begin : 0;
   const int n_tiles = (int)((nrows + SR - 1) / SR);
-  const int total = n_tiles * n_grp;
+  const int n_stg = n_grp / GPS;  // stages per tile (n_grp is a multiple of GPS)
+  const int total = n_tiles * n_stg;
 
   float2(*wl)[KMAX] = lists[wave];
   for (int ql = 0; ql < 16; ++ql)
@@ -297,17 +301,23 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
       if (64 * j + lane < KMAX) wl[ql][64 * j + lane] = float2{-__builtin_inff(), __builtin_bit_cast(float, -1)};
 
   const i32x4 dq = make_desc(Q + q0 * ldq * EB, (uint32_t)(nq_blk * ldq * EB));
-  const int lr = lane >> 3, lc = (lane & 7) ^ lr;
+  // load lane -> row lr of the instruction's RPI rows, LDS slot lane % CPR of
+  // that row, which holds chunk (lane % CPR) ^ (row % 8)
+  const int lr = lane / CPR;
   const int ri = lane & 15, rgrp = lane >> 4;
   const uint32_t ring_base = (uint32_t)(uintptr_t)&ring[0][0];
-  constexpr uint32_t SLOT_BYTES = (SR + SQ) * 8 * 16;
-  // per-lane byte offsets of this wave's two 8-row blocks (K-group 0)
-  const uint32_t goff0 = (uint32_t)((int64_t)(16 * wave + lr) * ldg * EB + lc * 16);
-  const uint32_t goff1 = goff0 + (uint32_t)(8 * ldg * EB);
-  const uint32_t qoff0 = (uint32_t)((int64_t)(4 * lr + wave) * ldq * EB + lc * 16);
-  const uint32_t qoff1 = qoff0 + (uint32_t)(32 * ldq * EB);
-  const uint32_t lds_g = ring_base + (uint32_t)(16 * wave) * 128u;
-  const uint32_t lds_q = ring_base + (uint32_t)(SR + 16 * wave) * 128u;
+  constexpr uint32_t SLOT_BYTES = (SR + SQ) * RB;
+  // per-lane byte offsets of this wave's 16 store rows / 16 query rows in
+  // groups of RPI rows (stage 0); query slot j is block query 4 j + wave
+  uint32_t goff[2 * GPS], qoff[2 * GPS];
+#pragma unroll
+  for (int h = 0; h < 2 * GPS; ++h) {
+    const int lc = (lane % CPR) ^ ((RPI * h + lr) & 7);  // LDS rows 16 wave + RPI h + lr
+    goff[h] = (uint32_t)((int64_t)(16 * wave + RPI * h + lr) * ldg * EB + lc * 16);
+    qoff[h] = (uint32_t)((int64_t)(4 * (RPI * h + lr) + wave) * ldq * EB + lc * 16);
+  }
+  const uint32_t lds_g = ring_base + (uint32_t)(16 * wave) * RB;
+  const uint32_t lds_q = ring_base + (uint32_t)(SR + 16 * wave) * RB;
 
   // issue cursor: next stage to load is (it_tile, it_g) into slot islot
   int it_tile = 0, it_g = 0, issued = 0, islot = 0;
@@ -320,21 +330,23 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   };
   auto issue_next = [&]() {
     const uint32_t sb = (uint32_t)islot * SLOT_BYTES;
-    const uint32_t go = (uint32_t)it_g * 128u;
+    const uint32_t go = (uint32_t)it_g * RB;
     if (g_nt) {
-      lds_dma16_nt(dt, goff0 + go, lds_g + sb);
-      lds_dma16(dq, qoff0 + go, lds_q + sb);
-      lds_dma16_nt(dt, goff1 + go, lds_g + sb + 1024u);
-      lds_dma16(dq, qoff1 + go, lds_q + sb + 1024u);
+#pragma unroll
+      for (int h = 0; h < 2 * GPS; ++h) {
+        lds_dma16_nt(dt, goff[h] + go, lds_g + sb + 1024u * h);
+        lds_dma16(dq, qoff[h] + go, lds_q + sb + 1024u * h);
+      }
     } else {
-      lds_dma16(dt, goff0 + go, lds_g + sb);
-      lds_dma16(dq, qoff0 + go, lds_q + sb);
-      lds_dma16(dt, goff1 + go, lds_g + sb + 1024u);
-      lds_dma16(dq, qoff1 + go, lds_q + sb + 1024u);
+#pragma unroll
+      for (int h = 0; h < 2 * GPS; ++h) {
+        lds_dma16(dt, goff[h] + go, lds_g + sb + 1024u * h);
+        lds_dma16(dq, qoff[h] + go, lds_q + sb + 1024u * h);
+      }
     }
     ++issued;
     islot = islot == RING - 1 ? 0 : islot + 1;
-    if (++it_g == n_grp) {
+    if (++it_g == n_stg) {
       it_g = 0;
       ++it_tile;
       if (it_tile < n_tiles) tile_desc(it_tile);
@@ -403,14 +415,14 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
     f32x4 acc[4];
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int g = 0; g < n_grp; ++g, ++st) {
+    for (int g = 0; g < n_stg; ++g, ++st) {
       // stage st landed: at most (loads issued after it) of this wave's
       // loads are still outstanding
       const int after = total - 1 - st;
       if (after >= RING - 2) {
-        wait_vmcnt<4 * (RING - 2)>();
+        wait_vmcnt<LPW * (RING - 2)>();
       } else {
-        wait_vmcnt_4m(4 * after);
+        wait_vmcnt_4m(LPW * after);
       }
       // this wave's LDS reads of the previous stage are complete before
       // anyone refills that slot
@@ -420,19 +432,19 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
       const i32x4* sl = ring[cslot];
       cslot = cslot == RING - 1 ? 0 : cslot + 1;
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
+      for (int s2 = 0; s2 < 2 * GPS; ++s2) {
         const int qrow = SR + 16 * wave + ri;
-        const i32x4 qf = sl[qrow * 8 + ((4 * s2 + rgrp) ^ (qrow & 7))];
+        const i32x4 qf = sl[qrow * CPR + ((4 * s2 + rgrp) ^ (qrow & 7))];
 #pragma unroll
         for (int rt = 0; rt < 4; ++rt) {
           const int grow = 16 * rt + ri;
-          const i32x4 gf = sl[grow * 8 + ((4 * s2 + rgrp) ^ (grow & 7))];
+          const i32x4 gf = sl[grow * CPR + ((4 * s2 + rgrp) ^ (grow & 7))];
           acc[rt] = mma16(Tag{}, qf, gf, acc[rt]);
         }
       }
       // previous tile's selection, spread over this tile's stages
       if (pend_any)
-        for (int ql = g; ql < nq_w; ql += n_grp) process_query(ql);
+        for (int ql = g; ql < nq_w; ql += n_stg) process_query(ql);
     }
     // hand this tile over to the selection
     const int rbase = tile * SR;
@@ -814,6 +826,9 @@ __device__ inline Cand wave_best(Cand c) {
 }
 
 // One workgroup per query: k rounds of block arg-max over the source heads.
+// Up to 4 sources per thread: n_parts + merge <= 1024.
+constexpr int MERGE_SPT = 4;
+
 __global__ __launch_bounds__(256) void score_merge_kernel(const float* __restrict__ part_s,
                                                           const int64_t* __restrict__ part_i,
                                                           int n_parts, int k, int merge,
@@ -824,23 +839,36 @@ __global__ __launch_bounds__(256) void score_merge_kernel(const float* __restric
   const int64_t q = blockIdx.x;
   const int t = threadIdx.x;
   const int n_src = n_parts + (merge ? 1 : 0);
-  const float* src_s = nullptr;
-  const int64_t* src_i = nullptr;
-  if (t < n_parts) {
-    src_s = part_s + (q * n_parts + t) * (int64_t)k;
-    src_i = part_i + (q * n_parts + t) * (int64_t)k;
-  } else if (t < n_src) {
-    src_s = top_s + q * (int64_t)k;
-    src_i = top_i + q * (int64_t)k;
-  }
-  int head = 0;
-  Cand cur{-__builtin_inff(), -1};
-  if (src_s) {
-    cur.s = src_s[0];
-    cur.i = src_i[0];
+  const float* src_s[MERGE_SPT];
+  const int64_t* src_i[MERGE_SPT];
+  int head[MERGE_SPT];
+  Cand cur[MERGE_SPT];
+#pragma unroll
+  for (int m = 0; m < MERGE_SPT; ++m) {
+    const int src = t + 256 * m;
+    src_s[m] = nullptr;
+    src_i[m] = nullptr;
+    if (src < n_parts) {
+      src_s[m] = part_s + (q * n_parts + src) * (int64_t)k;
+      src_i[m] = part_i + (q * n_parts + src) * (int64_t)k;
+    } else if (src < n_src) {
+      src_s[m] = top_s + q * (int64_t)k;
+      src_i[m] = top_i + q * (int64_t)k;
+    }
+    head[m] = 0;
+    cur[m] = src_s[m] ? Cand{src_s[m][0], src_i[m][0]} : Cand{-__builtin_inff(), -1};
   }
   for (int j = 0; j < k; ++j) {
-    Cand b = wave_best(cur);
+    // this thread's best head
+    Cand tb = cur[0];
+    int tm = 0;
+#pragma unroll
+    for (int m = 1; m < MERGE_SPT; ++m)
+      if (better(cur[m], tb)) {
+        tb = cur[m];
+        tm = m;
+      }
+    Cand b = wave_best(tb);
     if ((t & 63) == 0) wb[t >> 6] = b;
     __syncthreads();
     Cand best = wb[0];
@@ -852,15 +880,13 @@ __global__ __launch_bounds__(256) void score_merge_kernel(const float* __restric
       oi[j] = best.i;
     }
     // the source whose head won advances (indices are unique across sources)
-    if (best.i >= 0 && cur.i == best.i && cur.s == best.s && src_s) {
-      ++head;
-      if (head < k) {
-        cur.s = src_s[head];
-        cur.i = src_i[head];
-      } else {
-        cur.s = -__builtin_inff();
-        cur.i = -1;
-      }
+    if (best.i >= 0 && tb.i == best.i && tb.s == best.s) {
+#pragma unroll
+      for (int m = 0; m < MERGE_SPT; ++m)
+        if (m == tm) {
+          ++head[m];
+          cur[m] = head[m] < k ? Cand{src_s[m][head[m]], src_i[m][head[m]]} : Cand{-__builtin_inff(), -1};
+        }
     }
     __syncthreads();
   }
@@ -922,12 +948,17 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     P.spart_bytes = (size_t)split * (size_t)n_g * (size_t)P.n_qb * SQB * 4;
   } else {
     P.split = 1;
-    // streaming plan: 64 queries per workgroup
+    // streaming plan: 64 queries per workgroup; one workgroup per CU (two for
+    // k <= 32, whose lists are small enough to share the LDS), as many
+    // partitions as workgroups fit at once (an exact multiple of the CU
+    // count: 248 workgroups ran ~13% slower than 256 on k <= 32)
     P.n_qb = (int)((n_q + 63) / 64);
-    int64_t parts = (512 + P.n_qb - 1) / P.n_qb;
+    int64_t per_wave = (k <= 32 ? 2 : 1) * (int64_t)256;
+    per_wave = per_wave > 1016 ? 1016 : per_wave;  // the merge takes <= 1024 sources
+    int64_t parts = (per_wave + P.n_qb - 1) / P.n_qb;
     const int64_t t64 = (n_g + SR - 1) / SR;
     parts = parts > t64 ? t64 : parts;
-    parts = parts > 248 ? 248 : (parts < 1 ? 1 : parts);
+    parts = parts > per_wave ? per_wave : (parts < 1 ? 1 : parts);
     int64_t rpp = (n_g + parts - 1) / parts;
     rpp = (rpp + SR - 1) / SR * SR;
     P.rows_per_part = rpp;
@@ -963,17 +994,32 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
   } else if (n_g > 0 && plan.split <= 1) {
     const int parts_pad = (plan.n_parts + 7) / 8 * 8;
     dim3 grid((unsigned)(plan.n_qb * parts_pad)), block(256);
-#define ATTR_SS(F, KM, RG)                                                                    \
-  hipLaunchKernelGGL((score_stream_kernel<F, KM, RG>), grid, block, 0, s, (const char*)Q, n_q, ldq, \
-                     (const char*)G, n_g, ldg, plan.n_grp, k, plan.rows_per_part, plan.n_parts,   \
+#define ATTR_SS(F, KM, RG, GP)                                                                   \
+  hipLaunchKernelGGL((score_stream_kernel<F, KM, RG, GP>), grid, block, 0, s, (const char*)Q, n_q,  \
+                     ldq, (const char*)G, n_g, ldg, plan.n_grp, k, plan.rows_per_part, plan.n_parts, \
                      plan.n_qb, part_s, part_i, index_base)
-    // LDS: ring RING x 16 KB + lists 4 x 16 x KMAX x 8 B <= 160 KB
-    if (f16) {
-      if (k <= 64) ATTR_SS(true, 64, 8);
-      else ATTR_SS(true, 128, 6);
+    // LDS: ring RING x (GPS x 16 KB) + lists 4 x 16 x KMAX x 8 B <= 160 KB; two
+    // K-groups per stage (256-byte row segments) when the groups pair up
+    const bool wide = plan.n_grp % 2 == 0;
+    if (k <= 32) {  // 80 KB of LDS: two workgroups per CU
+      if (f16) ATTR_SS(true, 32, 4, 1);
+      else ATTR_SS(false, 32, 4, 1);
+    } else if (f16) {
+      if (k <= 64) {
+        if (wide) ATTR_SS(true, 64, 4, 2);
+        else ATTR_SS(true, 64, 8, 1);
+      } else {
+        if (wide) ATTR_SS(true, 128, 3, 2);
+        else ATTR_SS(true, 128, 6, 1);
+      }
     } else {
-      if (k <= 64) ATTR_SS(false, 64, 8);
-      else ATTR_SS(false, 128, 6);
+      if (k <= 64) {
+        if (wide) ATTR_SS(false, 64, 4, 2);
+        else ATTR_SS(false, 64, 8, 1);
+      } else {
+        if (wide) ATTR_SS(false, 128, 3, 2);
+        else ATTR_SS(false, 128, 6, 1);
+      }
     }
 #undef ATTR_SS
     hipError_t e = hipGetLastError();

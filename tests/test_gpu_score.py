@@ -140,7 +140,10 @@ def test_gpt2_store_scan():
 @pytest.mark.parametrize("nq,ng,D,k,dt", [(100, 9000, 256, 100, np.float16),
                                           (40, 40001, 128, 10, np.float16),
                                           (70, 33000, 96, 5, np.float32),
-                                          (17, 70000, 64, 128, np.float16)])
+                                          (17, 70000, 64, 128, np.float16),
+                                          (50, 30000, 256, 32, np.float16),
+                                          (50, 30000, 256, 33, np.float16),
+                                          (9, 30000, 64, 64, np.float32)])
 def test_streaming_plan(nq, ng, D, k, dt):
     """Shapes large enough for the streaming (LDS-ring) plan: ragged query
     blocks, ragged partitions and tiles, duplicate rows, fp32 and fp16."""
