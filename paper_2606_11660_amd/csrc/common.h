@@ -74,6 +74,22 @@ __device__ inline void lds_dma16_nt(const i32x4& desc, uint32_t voff, uint32_t l
       : "memory", "m0");
 }
 
+// Direct-to-LDS load with the LDS base already in M0 (set_m0): the
+// instruction offset OFF is added to both the memory offset and the LDS
+// address, so up to four consecutive 1 KB destinations share one M0 write
+// (the caller subtracts OFF from voff).
+__device__ inline void set_m0(uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" : : "s"(__builtin_amdgcn_readfirstlane(lds_base)) : "memory", "m0");
+}
+template <int OFF>
+__device__ inline void lds_dma16_m0(const i32x4& desc, uint32_t voff) {
+  static_assert(OFF >= 0 && OFF < 4096, "12-bit instruction offset");
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds"
+               :
+               : "v"(voff), "s"(uniform_desc(desc)), "n"(OFF)
+               : "memory");
+}
+
 // s_waitcnt lgkmcnt(0) through the builtin, so that the compiler's own wait
 // insertion knows every LDS read before it has completed (an inline-asm wait
 // is opaque to it and would be followed by redundant waits); the empty asm

@@ -28,6 +28,8 @@
 // range read as zeros through the buffer descriptors' range check.
 #pragma once
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace attr {
@@ -78,18 +80,34 @@ struct GemmCore {
     const uint32_t a8 = (uint32_t)(8 * lda * 2), b8 = (uint32_t)(8 * ldb * 2);
     const uint32_t lds_a = (uint32_t)(uintptr_t)&sm.a[0][0] + (uint32_t)(64 * wave) * 128u;
     const uint32_t lds_b = (uint32_t)(uintptr_t)&sm.b[0][0] + (uint32_t)(64 * wave) * 128u;
-    // load instruction c (0..15) of stage st: A rows for c < 8, B rows after.
-    // A stage past the end is issued with every lane out of range: it
-    // fetches nothing and zero-fills a slot that is no longer read.
-    auto issue_one = [&](int st, int c) {
+    // loads of stage st come in 4 groups of 4 instructions (A rows 0-31 and
+    // 32-63 of the wave, then B): group g sets M0 once, instruction u of it
+    // lands at M0 + 1024 u through the instruction offset.  A stage past the
+    // end is issued with every lane out of range: it fetches nothing and
+    // zero-fills a slot that is no longer read.
+    auto issue_grp = [&](int st, int g) {
+      const uint32_t sb = (uint32_t)(st & 1) * G_SLOT;
+      set_m0((g < 2 ? lds_a : lds_b) + sb + (uint32_t)(g & 1) * 4096u);
+    };
+    auto issue_u = [&](int st, int g, auto uc) {
+      constexpr int u = decltype(uc)::value;
       const bool sw = st >= n_sw;
       const uint32_t ko = (uint32_t)(sw ? st - n_sw : st) * 128u + (st < n_st ? 0u : 0x80000000u);
-      const uint32_t sb = (uint32_t)(st & 1) * G_SLOT;
-      const int h = c & 7;
-      if (c < 8) {
-        lds_dma16(da, a_off + h * a8 + ko, lds_a + sb + h * 1024u);
+      const int h = 4 * (g & 1) + u;
+      if (g < 2) {
+        lds_dma16_m0<1024 * u>(da, a_off + h * a8 + ko - 1024u * u);
       } else {
-        lds_dma16(sw ? db2 : db, b_off + h * b8 + ko, lds_b + sb + h * 1024u);
+        lds_dma16_m0<1024 * u>(sw ? db2 : db, b_off + h * b8 + ko - 1024u * u);
+      }
+    };
+    auto issue_all = [&](int st) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        issue_grp(st, g);
+        issue_u(st, g, std::integral_constant<int, 0>{});
+        issue_u(st, g, std::integral_constant<int, 1>{});
+        issue_u(st, g, std::integral_constant<int, 2>{});
+        issue_u(st, g, std::integral_constant<int, 3>{});
       }
     };
     // fragment reads: lane (ri, rg) takes row 16 t + ri, chunk 4 half + rg in
@@ -116,12 +134,10 @@ struct GemmCore {
     i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
 
     // prologue: stage 0 in, stage 1 on its way, h0 of stage 0 in registers
-#pragma unroll
-    for (int c = 0; c < 16; ++c) issue_one(0, c);
+    issue_all(0);
     gemm_wait_vm<0>();
     __builtin_amdgcn_s_barrier();
-#pragma unroll
-    for (int c = 0; c < 16; ++c) issue_one(1, c);
+    issue_all(1);
     {
       const i32x4* pa = sm.a[0];
       const i32x4* pb = sm.b[0];
@@ -150,12 +166,23 @@ struct GemmCore {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         read_pair(i, pa, pb, fs0, h0a, h0b);
-        issue_one(st + 1, 2 * i);
+        // loads 2 i and 2 i + 1 of stage st + 1: group i / 2, members
+        // 2 (i % 2) and 2 (i % 2) + 1
+        if ((i & 1) == 0) {
+          issue_grp(st + 1, i >> 1);
+          issue_u(st + 1, i >> 1, std::integral_constant<int, 0>{});
+        } else {
+          issue_u(st + 1, i >> 1, std::integral_constant<int, 2>{});
+        }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
-        issue_one(st + 1, 2 * i + 1);
+        if ((i & 1) == 0) {
+          issue_u(st + 1, i >> 1, std::integral_constant<int, 1>{});
+        } else {
+          issue_u(st + 1, i >> 1, std::integral_constant<int, 3>{});
+        }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);

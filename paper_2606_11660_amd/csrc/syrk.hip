@@ -96,21 +96,23 @@ __device__ inline void band_tile(int v, int nt, int& tp, int& tq) {
 }
 
 // Work item of workgroup b: workgroups go to the 8 XCDs round robin
-// (b % 8), so XCD x is given the contiguous item range [x per_xcd,
-// (x + 1) per_xcd) in dispatch order; items are slice-major and band-ordered
-// within a slice, so the workgroups resident on one XCD at a time share row
-// blocks through its L2.
+// (b % 8).  The K-slices are taken one after the other by the whole chip, so
+// that the rows being read at any time are one slice's (256 MB at 8192
+// columns, about the MALL's size); within a slice XCD x takes the contiguous
+// band-ordered tile range [x per_xcd, (x + 1) per_xcd), so the workgroups
+// resident on one XCD share row blocks through its L2.
 template <typename Tag, typename T>
 __global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ XT, int64_t C,
                                                    int64_t D, int nt, int n_up, int J,
                                                    int per_xcd, int64_t Cs,
                                                    float* __restrict__ part) {
   __shared__ GemmSmem sm;
-  const int item = (int)(blockIdx.x & 7u) * per_xcd + (int)(blockIdx.x >> 3);
-  if (item >= n_up * J) return;  // uniform
-  const int j = item / n_up;
+  const int l = (int)(blockIdx.x >> 3);
+  const int j = l / per_xcd;
+  const int v = (int)(blockIdx.x & 7u) * per_xcd + (l - j * per_xcd);
+  if (j >= J || v >= n_up) return;  // uniform
   int tp, tq;
-  band_tile(item - j * n_up, nt, tp, tq);
+  band_tile(v, nt, tp, tq);
   const int u = tp * nt - tp * (tp - 1) / 2 + (tq - tp);  // row-major upper index
   int64_t np = D - (int64_t)tp * GT, nq = D - (int64_t)tq * GT;
   np = np > GT ? GT : np;
@@ -176,8 +178,11 @@ SyrkPlan plan_syrk(int64_t n_rows, int64_t D) {
   int64_t c = n_rows < SYRK_CHUNK ? n_rows : SYRK_CHUNK;
   c = (c + 63) / 64 * 64;
   if (c < 64) c = 64;
-  int J = (int)(c / 16384);
-  J = J < 1 ? 1 : (J > 4 ? 4 : J);
+#ifndef ATTR_SYRK_SLICE
+#define ATTR_SYRK_SLICE 16384
+#endif
+  int J = (int)(c / ATTR_SYRK_SLICE);
+  J = J < 1 ? 1 : (J > SYRK_CHUNK / ATTR_SYRK_SLICE ? SYRK_CHUNK / ATTR_SYRK_SLICE : J);
   int64_t cs = (c + J - 1) / J;
   cs = (cs + 63) / 64 * 64;
   P.J = J;
@@ -204,8 +209,8 @@ hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, in
     else
       hipLaunchKernelGGL(transpose_kernel<_Float16>, gt, dim3(256), 0, s, (const _Float16*)X, ldx,
                          n_rows, r0, D, P.C, (_Float16*)xt);
-    const int per_xcd = (P.n_up * P.J + 7) / 8;
-    dim3 gs((unsigned)(8 * per_xcd));
+    const int per_xcd = (P.n_up + 7) / 8;  // tiles per XCD and slice
+    dim3 gs((unsigned)(8 * per_xcd * P.J));
     if (bf16)
       hipLaunchKernelGGL((syrk_kernel<Bf16Tag, __bf16>), gs, dim3(256), 0, s, (const __bf16*)xt, P.C,
                          D, P.nt, P.n_up, P.J, per_xcd, P.Cs, (float*)part);
