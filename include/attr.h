@@ -128,12 +128,13 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
  *         the upper triangle including the diagonal is updated, the strict
  *         lower triangle is never read or written)
  * Accumulation is additive across calls, so a store can be processed in
- * chunks; divide by the total row count afterwards.  Each call's sum is
- * formed in fp32 panels combined with error-free (two-float) summation and
- * rounded once into H.
+ * chunks; divide by the total row count afterwards.  Within a call, partial
+ * sums are formed in fp32 (DIAG: 8-row groups; FULL: matrix-core products
+ * over at most 16384 rows), combined in fp64 in a fixed order and rounded
+ * once into H, so results are deterministic.
  *
- *   X, ldx   device [n_rows, D] rows, dtype ATTR_F16 or ATTR_F32 (DIAG also
- *            ATTR_BF16), ldx >= D
+ *   X, ldx   device [n_rows, D] rows: DIAG takes ATTR_F16, ATTR_BF16 or
+ *            ATTR_F32, FULL takes ATTR_F16 or ATTR_BF16; ldx >= D
  *   D        multiple of 8 (DIAG) or of 64 (FULL); FULL needs D <= 32768
  *   mode     ATTR_PRECOND_DIAG or ATTR_PRECOND_FULL
  *   ws       attr_precond_accumulate_workspace_size(n_rows, D, x_dtype, mode)
@@ -154,8 +155,9 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
  *   [D, D] row-major, symmetric in use: y_p = sum_q M[p*D+q] x_q);
  *   if unit_normalize, y /= ||y||_2 over the whole row (a zero row stays 0);
  *   Y = y cast to y_dtype (round to nearest even).
- * FULL evaluates M as an fp16 pair M_hi + 2^-12 * M_lo on fp16 MFMA with
- * fp32 accumulation (about 22 significant bits of M).
+ * FULL evaluates M as a scaled fp16 pair, A = 2^s M (max|A| <= 2^15),
+ * A_hi = fp16(A), A_lo = fp16(A - A_hi), y = 2^-s X (A_hi + A_lo)^T on fp16
+ * MFMA with fp32 accumulation (about 22 significant bits of M).
  *
  *   X, ldx   device [n_rows, D], x_dtype ATTR_F32 or ATTR_F16
  *            (FULL: ATTR_F16 only)
