@@ -826,6 +826,54 @@ __device__ inline Cand wave_best(Cand c) {
 }
 
 // One workgroup per query: k rounds of block arg-max over the source heads.
+// Split-K plan with at most 256 store rows (a batch of new rows scored and
+// merged into a running list): one wave per query sums the slices of its
+// scores in slice order and takes the k best of those rows and of the
+// previous list (merge) by k rounds of wave arg-max, writing the list in
+// place.  Replaces the partition select and the merge launches.
+__global__ __launch_bounds__(64) void score_small_select_kernel(
+    const float* __restrict__ spart, int64_t nqp, int64_t n_g, int n_split, int k, int merge,
+    int64_t index_base, float* top_s, int64_t* top_i) {
+  const int64_t q = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int64_t plane = n_g * nqp;
+  Cand c[6];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const int64_t j = lane + 64 * m;
+    c[m] = Cand{-__builtin_inff(), -1};
+    if (j < n_g) {
+      const float* src = spart + j * nqp + q;
+      float acc = src[0];
+      for (int sp = 1; sp < n_split; ++sp) acc += src[sp * plane];
+      // NaN and -inf are never selected
+      if (acc > -__builtin_inff()) c[m] = Cand{acc, index_base + j};
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    const int e = lane + 64 * m;
+    c[4 + m] = Cand{-__builtin_inff(), -1};
+    if (merge && e < k) c[4 + m] = Cand{top_s[q * k + e], top_i[q * k + e]};
+  }
+  for (int r = 0; r < k; ++r) {
+    Cand lb = c[0];
+#pragma unroll
+    for (int m = 1; m < 6; ++m)
+      if (better(c[m], lb)) lb = c[m];
+    const Cand wb = wave_best(lb);
+    if (lane == 0) {
+      top_s[q * k + r] = wb.i >= 0 ? wb.s : -__builtin_inff();
+      top_i[q * k + r] = wb.i;
+    }
+    if (wb.i >= 0) {
+#pragma unroll
+      for (int m = 0; m < 6; ++m)
+        if (c[m].i == wb.i && c[m].s == wb.s) c[m].i = -1;  // indices are unique
+    }
+  }
+}
+
 // Up to 4 sources per thread: n_parts + merge <= 1024.
 constexpr int MERGE_SPT = 4;
 
@@ -1036,6 +1084,12 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
                          spart);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (n_g <= 256) {
+      hipLaunchKernelGGL(score_small_select_kernel, dim3((unsigned)n_q), dim3(64), 0, s,
+                         (const float*)spart, (int64_t)plan.n_qb * SQB, n_g, plan.split, k,
+                         merge, index_base, top_s, top_i);
+      return hipGetLastError();
+    }
     dim3 g2((unsigned)(plan.n_qb * plan.n_parts)), b2(256);
     if (k <= 16)
       hipLaunchKernelGGL(score_select_kernel<16>, g2, b2, 0, s, (const float*)spart, n_q,

@@ -107,6 +107,32 @@ def test_merge_chunks_equals_single_call():
     check_topk(host(ts), host(ti), O.scores(Q, G), k)
 
 
+@pytest.mark.parametrize("k", [10, 128])
+def test_merge_small_batches_like_the_bench(k):
+    """The bench's pattern: 64-row batches scored and merged into the running
+    list (split-K plan with at most 256 rows: fused select and merge), with
+    NaN and duplicate rows; equals one call over the whole store."""
+    say(f"case: merge 64-row batches k={k}")
+    nq, ng, D = 64, 640, 12288
+    Q = synth.unit_rows(nq, D, seed=51)
+    G = synth.unit_rows(ng, D, seed=52)
+    G[600] = G[5]                          # tie across batches
+    Q[3] = G[5]
+    G[70] = np.nan                         # never selected
+    Qd, Gd = dev(Q), dev(G)
+    ts = torch.empty((nq, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((nq, k), dtype=torch.int64, device="cuda")
+    for b in range(0, ng, 64):
+        P.attr_score_topk(Qd, Gd[b:b + 64], k, ts, ti, index_base=b, merge=b > 0)
+    torch.cuda.synchronize()
+    ref = O.scores(Q, G)
+    ref[:, 70] = -np.inf
+    gi = host(ti)
+    assert not (gi == 70).any()
+    check_topk(host(ts), gi, ref, k)
+    assert gi[3, 0] == 5 and gi[3, 1] == 600
+
+
 def test_fewer_rows_than_k():
     say("case: n_g < k")
     Q = synth.unit_rows(5, 64, seed=17)
