@@ -838,18 +838,36 @@ __global__ __launch_bounds__(64) void score_small_select_kernel(
   const int lane = threadIdx.x;
   const int64_t plane = n_g * nqp;
   Cand c[6];
+  // rows lane + 64 m; slices summed in order, 8 slices of all four rows in
+  // flight at once
+  float acc[4];
+  bool live[4];
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
-    const int64_t j = lane + 64 * m;
-    c[m] = Cand{-__builtin_inff(), -1};
-    if (j < n_g) {
-      const float* src = spart + j * nqp + q;
-      float acc = src[0];
-      for (int sp = 1; sp < n_split; ++sp) acc += src[sp * plane];
-      // NaN and -inf are never selected
-      if (acc > -__builtin_inff()) c[m] = Cand{acc, index_base + j};
-    }
+    live[m] = lane + 64 * m < n_g;
+    acc[m] = live[m] ? spart[(lane + 64 * m) * nqp + q] : 0.f;
   }
+  int sp = 1;
+  for (; sp + 8 <= n_split; sp += 8) {
+    float x[4][8];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        x[m][u] = live[m] ? spart[(sp + u) * plane + (lane + 64 * m) * nqp + q] : 0.f;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc[m] += x[m][u];
+  }
+  for (; sp < n_split; ++sp)
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+      if (live[m]) acc[m] += spart[sp * plane + (lane + 64 * m) * nqp + q];
+#pragma unroll
+  for (int m = 0; m < 4; ++m)  // NaN and -inf are never selected
+    c[m] = live[m] && acc[m] > -__builtin_inff() ? Cand{acc[m], index_base + lane + 64 * m}
+                                                 : Cand{-__builtin_inff(), -1};
 #pragma unroll
   for (int m = 0; m < 2; ++m) {
     const int e = lane + 64 * m;
