@@ -107,14 +107,68 @@ def _timeit(fn, stream, reps):
     return e0.elapsed_time(e1) / reps
 
 
-def _other_rows(stream, dev):
-    """Timings of the preconditioner rows on the 10^6 x 8192 low-rank-plus-noise
-    store and of the 4M-row store scan (Q sweep: Q <= 64 runs the streaming
-    plan, HBM-bound; Q >= 128 the GEMM plan, MFMA-bound), each against its
-    roofline."""
+def _llama1b_projection(stream, dev):
+    """Projection of the 1B-shaped model (16 layers x q,k,v,o 2048->2048,
+    gate/up 2048->8192, down 8192->2048; k = 16, row of 28672): a resident
+    batch of 16 examples with ragged lengths (uniform in [256, 2048], seed 4),
+    tokens packed back to back (row_offset / length).  Algorithmic bytes are
+    the valid tokens' a/g rows, R/S once and the fp32 rows.  The second
+    variant points q/k/v at one input tensor and gate/up at another (the
+    model's real sharing): its unique bytes are 0.870 of the first, and the
+    rate is reported over those unique bytes."""
+    import numpy as np
     import torch
     import paper_2606_11660_amd as P
-    out = {}
+    import synth
+
+    wl = synth.LLAMA1B
+    k, B, T = wl.k, 16, wl.T
+    lengths = synth.example_lengths(wl.n_examples)[:B]
+    tot = int(lengths.sum())
+    offs = np.concatenate([[0], np.cumsum(lengths.astype(np.int64))[:-1]])
+    off_t = torch.from_numpy(offs.astype(np.int64)).to(dev)
+    len_t = torch.from_numpy(lengths.astype(np.int32)).to(dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1)
+    sep, shared, by_layer = [], [], {}
+    for m, md in enumerate(wl.modules):
+        layer, kind = md.name.split(".")[0], md.name.split(".")[-1]
+        a = torch.randn((tot, md.d_in), generator=gen, device=dev, dtype=torch.bfloat16)
+        g = torch.randn((tot, md.d_out), generator=gen, device=dev, dtype=torch.bfloat16)
+        R, S = synth.projection_pair(wl, m)
+        Rt = torch.from_numpy(R.view(np.int16)).view(torch.bfloat16).to(dev)
+        St = torch.from_numpy(S.view(np.int16)).view(torch.bfloat16).to(dev)
+        sep.append(P.Module(a, g, Rt, St, m * k * k))
+        group = {"q": "qkv", "k": "qkv", "v": "qkv", "gate": "gu", "up": "gu"}.get(kind)
+        a_sh = by_layer.setdefault((layer, group), a) if group else a
+        shared.append(P.Module(a_sh, g, Rt, St, m * k * k))
+    rows = torch.empty((B, wl.D), dtype=torch.float32, device=dev)
+    ws = P.Workspace(dev)
+    elems = sum(md.d_in + md.d_out for md in wl.modules)
+    uniq = sum(md.d_out + (md.d_in if md.name.split(".")[-1] in ("q", "gate", "o", "down") else 0)
+               for md in wl.modules)
+    rs = sum((md.d_in + md.d_out) * k * 2 for md in wl.modules)
+    out = {"modules": len(wl.modules), "batch": B, "valid_tokens": tot,
+           "lengths": "uniform integers in [256, 2048], seed 4, first 16", "D": wl.D}
+    for name, mods, e in (("separate_inputs", sep, elems), ("shared_qkv_gateup_inputs", shared, uniq)):
+        ms = _timeit(lambda: P.attr_project(mods, k, B, T, rows, row_offset=off_t, length=len_t,
+                                            ws=ws, stream=stream), stream, 5)
+        byts = tot * e * 2 + rs + B * wl.D * 4
+        out[name] = {"ms": ms, "examples_per_s": B / (ms * 1e-3), "bytes": byts,
+                     "GBps": byts / ms / 1e6, "frac_hbm": byts / ms / 1e6 / HBM_PEAK_GBPS}
+    del sep, shared, by_layer, rows
+    torch.cuda.empty_cache()
+    return out
+
+
+def _other_rows(stream, dev):
+    """Timings of the 1B-shaped projection, of the preconditioner rows on the
+    10^6 x 8192 low-rank-plus-noise store and of the 4M-row store scan (Q
+    sweep: Q <= 64 runs the streaming plan, HBM-bound; Q >= 128 the GEMM plan,
+    MFMA-bound), each against its roofline."""
+    import torch
+    import paper_2606_11660_amd as P
+    out = {"projection_llama1b_shaped": _llama1b_projection(stream, dev)}
     N, D = 1_000_000, 8192
     gen = torch.Generator(device=dev)
     gen.manual_seed(3)
@@ -199,9 +253,14 @@ def _other_rows(stream, dev):
 def _profile_row(row, dev):
     """One row of the path on its own, sized for counter runs (rocprofv3
     --pmc): `syrk` / `full_apply` on a 131072 x 8192 low-rank-plus-noise
-    store, `scan16` / `scan1024` on a 1M x 8192 unit fp16 store with top-100."""
+    store, `scan16` / `scan1024` on a 1M x 8192 unit fp16 store with top-100,
+    `llama1b` the 1B-shaped projection row (timed, printed as JSON)."""
     import torch
     import paper_2606_11660_amd as P
+    if row == "llama1b":
+        stream = torch.cuda.Stream(device=dev)
+        print(json.dumps({"profile_row": row, "result": _llama1b_projection(stream, dev)}))
+        return
     D = 8192
     gen = torch.Generator(device=dev)
     gen.manual_seed(3)
@@ -257,7 +316,7 @@ def main():
     ap.add_argument("--quick", action="store_true", help="skip the preconditioner / store-scan rows")
     ap.add_argument("--copy-reference", action="store_true",
                     help="only run the 1 GiB copy used to calibrate traffic counters")
-    ap.add_argument("--profile-row", choices=["syrk", "full_apply", "scan16", "scan1024"],
+    ap.add_argument("--profile-row", choices=["syrk", "full_apply", "scan16", "scan1024", "llama1b"],
                     help="only run one row of the path once, for counter runs")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
