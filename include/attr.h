@@ -184,7 +184,9 @@ attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows
  * section "Attribution Pipelines".  With few queries the scan streams the
  * store once and the score matrix never reaches memory; with many fp16
  * queries (n_q >= 128) it is computed chunk by chunk into the workspace
- * (~256 MB per chunk) and selected exactly from there.
+ * (~256 MB per chunk, plus one maximum per 64 rows) and selected exactly
+ * from there; after the first chunk only 64-row segments that can still
+ * beat a query's running k-th best score are written and read.
  *
  *   Q, ldq       device [n_q, D];  G, ldg: device [n_g, D]; both `dtype`
  *                (ATTR_F16 or ATTR_F32); D a multiple of 64 (fp16) or 32

@@ -498,14 +498,23 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
 // Chunks of at most 4096 rows are sorted whole.  NaN and -inf scores are
 // never selected; lists are padded with (-inf, -1).  Chunk lists are merged
 // by the common merge kernel.
-constexpr int RS_CAP = 4096;  // candidates sorted per (query, chunk)
-constexpr int RS_SMP = 2048;  // threshold samples
+constexpr int RS_CAP = 2048;  // candidates sorted per (query, chunk)
+constexpr int RS_SMP = 1024;  // threshold samples
+constexpr int RS_SEG = 64;    // chunk rows per score segment (one maximum each)
+constexpr int RS_MAXSEG = 131072 / RS_SEG;  // segments of the largest chunk
+
+// v of another lane of the same row of 16 (DPP control C, full masks)
+template <int C>
+__device__ inline float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), C, 0xf, 0xf, false));
+}
 
 template <typename Tag>
 __global__ __launch_bounds__(256) void score_gemm_kernel(
     const _Float16* __restrict__ Q, int64_t n_q, int64_t ldq, const _Float16* __restrict__ G,
     int64_t nc, int64_t ldg, int n_qt, int n_items, int per_xcd, int n_st,
-    float* __restrict__ S, int64_t lds) {
+    float* __restrict__ S, int64_t lds, float* __restrict__ segmax, int64_t n_seg,
+    const float* __restrict__ thr, int use_bound) {
   __shared__ GemmSmem sm;
   // XCD x (workgroup b goes to XCD b % 8) takes a contiguous range of
   // (query tile fastest, row tile) items: the query tiles of one row tile
@@ -519,20 +528,49 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(
   nr = nr > GT ? GT : nr;
   const i32x4 dq = make_desc(Q + q0 * ldq, (uint32_t)(nq * ldq * 2));
   const i32x4 dg = make_desc(G + c0 * ldg, (uint32_t)(nr * ldg * 2));
+  // the tile's query bounds, staged in LDS (the main loop's barriers publish them)
+  __shared__ float tb[GT];
+  tb[threadIdx.x] = use_bound && q0 + threadIdx.x < n_q ? thr[q0 + threadIdx.x] : -__builtin_inff();
   GemmCore<Tag> core;
   core.zero();
   core.run(sm, dq, ldq, dg, dg, ldg, n_st, n_st);
+  // Epilogue.  A wave's 128 columns are two 64-row segments of the chunk
+  // (accumulator columns j < 4 and j >= 4); the 16 lanes that share a query
+  // row reduce each segment's maximum, which is stored for the selection.
+  // With a bound from earlier chunks (running k-th best score of the query),
+  // a segment whose maximum is below it cannot contribute and is not written.
+  const int lane = threadIdx.x & 63;
+  const int64_t seg0 = c0 / RS_SEG + 2 * ((threadIdx.x >> 6) & 1);
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = GemmCore<Tag>::row_of(i, r);
+      float m[2];
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        float v = -__builtin_inff();
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          if (GemmCore<Tag>::col_of(4 * g + jj) < nr) v = fmaxf(v, core.acc[i][4 * g + jj][r]);
+        // rotations within each row of 16 lanes (DPP row_ror 8, 4, 2, 1)
+        v = fmaxf(v, dpp_f<0x128>(v));
+        v = fmaxf(v, dpp_f<0x124>(v));
+        v = fmaxf(v, dpp_f<0x122>(v));
+        v = fmaxf(v, dpp_f<0x121>(v));
+        m[g] = v;
+      }
       if (row < nq) {
+        const float b = tb[row];
+        if ((lane & 15) == 0) {
+          segmax[(q0 + row) * n_seg + seg0] = m[0];
+          segmax[(q0 + row) * n_seg + seg0 + 1] = m[1];
+        }
         float* dst = S + (q0 + row) * lds + c0;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int col = GemmCore<Tag>::col_of(j);
-          if (col < nr) dst[col] = core.acc[i][j][r];
+          if (col < nr && !(m[j >> 2] < b)) dst[col] = core.acc[i][j][r];
         }
       }
     }
@@ -591,20 +629,34 @@ __device__ inline uint64_t block_max_u64(uint64_t v, uint64_t* red) {
 }
 
 __global__ __launch_bounds__(256) void score_rselect_kernel(
-    const float* __restrict__ S, int64_t lds, int64_t nc, int k, int part, int n_parts,
-    int64_t index_base, float* __restrict__ part_s, int64_t* __restrict__ part_i) {
+    const float* __restrict__ S, int64_t lds, const float* __restrict__ segmax, int64_t n_seg,
+    float* __restrict__ thr, int64_t nc, int k, int part, int n_parts, int64_t index_base,
+    float* __restrict__ part_s, int64_t* __restrict__ part_i) {
   __shared__ uint64_t cand[RS_CAP];
-  __shared__ uint32_t smp[RS_SMP];
+  __shared__ uint32_t smp[RS_MAXSEG];  // segment maxima or samples, sorted
+  __shared__ uint16_t segs[RS_MAXSEG];
   __shared__ uint64_t red_u[4];
-  __shared__ int n_cand;
+  __shared__ int n_cand, n_pass;
   const int64_t q = blockIdx.x;
   const int t = threadIdx.x;
   const float* s = S + q * lds;
+  const float* sm = segmax + q * n_seg;
+  const int n_sc = (int)((nc + RS_SEG - 1) / RS_SEG);
   float* ds = part_s + (q * n_parts + part) * (int64_t)k;
   int64_t* di = part_i + (q * n_parts + part) * (int64_t)k;
 
-  // collect every selectable score >= tau (up to RS_CAP of them); returns
-  // how many there are
+  // Bound from this call's earlier chunks, all of lower index: the running
+  // maximum of their k-th scores has k entries at or above it that precede
+  // every row of this chunk, so only scores strictly above it can still
+  // enter the top k.  Segments whose maximum is below it were not written.
+  const float bnd = part > 0 ? thr[q] : -__builtin_inff();
+  const uint32_t bkey = fkey(bnd);
+  const bool has_b = part > 0 && selectable(bkey);
+  const uint32_t floor_key = has_b ? bkey + 1u : 0x00800000u;
+  const float floor_f = fkey_inv(floor_key);  // NaN when the bound is +inf: nothing passes
+
+  // collect every selectable score >= tau (up to RS_CAP of them), reading
+  // only the segments whose maximum reaches tau; returns how many there are
   auto take = [&](float v, int64_t j, uint32_t tau) {
     const uint32_t key = fkey(v);
     if (selectable(key) && key >= tau) {
@@ -613,33 +665,79 @@ __global__ __launch_bounds__(256) void score_rselect_kernel(
     }
   };
   auto collect = [&](uint32_t tau) -> int {
+    const float tau_f = fkey_inv(tau);  // the float whose key is tau
     __syncthreads();
-    if (t == 0) n_cand = 0;
-    __syncthreads();
-    // rows of S start 1 KB aligned (lds is a multiple of 256)
-    const f32x4* s4 = reinterpret_cast<const f32x4*>(s);
-    const int64_t n4 = nc >> 2;
-    for (int64_t j4 = t; j4 < n4; j4 += 256) {
-      const f32x4 v = s4[j4];
-      take(v[0], 4 * j4, tau);
-      take(v[1], 4 * j4 + 1, tau);
-      take(v[2], 4 * j4 + 2, tau);
-      take(v[3], 4 * j4 + 3, tau);
+    if (t == 0) {
+      n_cand = 0;
+      n_pass = 0;
     }
-    for (int64_t j = 4 * n4 + t; j < nc; j += 256) take(s[j], j, tau);
+    __syncthreads();
+    for (int g = t; g < n_sc; g += 256)
+      if (sm[g] >= tau_f) segs[atomicAdd(&n_pass, 1)] = (uint16_t)g;
+    __syncthreads();
+    const int np = n_pass;
+    // 16 threads per segment (16 bytes each), SB segments per group in flight
+    constexpr int SB = 4;
+    const int grp = t >> 4, l16 = t & 15;
+    const f32x4* s4 = reinterpret_cast<const f32x4*>(s);  // rows are 1 KB aligned
+    for (int e0 = 0; e0 < np; e0 += 16 * SB) {
+      f32x4 v[SB];
+      int64_t j0[SB];
+#pragma unroll
+      for (int u = 0; u < SB; ++u) {
+        const int e = e0 + 16 * u + grp;
+        j0[u] = e < np ? (int64_t)segs[e] * RS_SEG + 4 * l16 : -1;
+        // a segment's 64 columns lie inside the row (lds is a multiple of 256)
+        v[u] = j0[u] >= 0 ? s4[j0[u] >> 2]
+                          : f32x4{-__builtin_inff(), -__builtin_inff(), -__builtin_inff(),
+                                  -__builtin_inff()};
+      }
+#pragma unroll
+      for (int u = 0; u < SB; ++u) {
+        const float m = fmaxf(fmaxf(v[u][0], v[u][1]), fmaxf(v[u][2], v[u][3]));
+        if (j0[u] >= 0 && m >= tau_f) {
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4)
+            if (j0[u] + e4 < nc) take(v[u][e4], j0[u] + e4, tau);
+        }
+      }
+    }
     __syncthreads();
     return n_cand;
   };
 
   bool ok = false;
   int c = 0;
-  if (nc <= RS_CAP) {
-    c = collect(0x00800000u);  // every selectable score
-    ok = true;
+  if (nc <= RS_CAP || has_b) {
+    c = collect(floor_key);  // everything above the bound
+    ok = c <= RS_CAP;        // fewer than k entries is allowed
   } else {
-    for (int j = t; j < RS_SMP; j += 256) {
-      const uint32_t key = fkey(s[(int64_t)j * nc / RS_SMP]);
-      smp[j] = selectable(key) ? key : 0u;
+    // No bound yet: the k-th largest segment maximum.  k segments reach it,
+    // so at least k scores do; unless one segment holds many of the top
+    // scores, few more than k do.
+    int n_sort = 64;
+    while (n_sort < n_sc) n_sort <<= 1;
+    for (int g = t; g < n_sort; g += 256) {
+      const uint32_t key = g < n_sc ? fkey(sm[g]) : 0u;
+      smp[g] = selectable(key) ? key : 0u;
+    }
+    bitonic_desc(smp, n_sort);
+    const uint32_t tau = k <= n_sc && smp[k - 1] ? smp[k - 1] : floor_key;
+    c = collect(tau);
+    ok = c <= RS_CAP;
+  }
+  if (!ok) {
+    {
+      uint32_t v[RS_SMP / 256];
+#pragma unroll
+      for (int u = 0; u < RS_SMP / 256; ++u) {
+        const int64_t j = (int64_t)(u * 256 + t) * nc / RS_SMP;
+        const bool written = !has_b || sm[j / RS_SEG] >= floor_f;
+        const uint32_t key = written ? fkey(s[j]) : 0u;
+        v[u] = selectable(key) && key >= floor_key ? key : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < RS_SMP / 256; ++u) smp[u * 256 + t] = v[u];
     }
     bitonic_desc(smp, RS_SMP);
     int lo = 0, hi = RS_SMP - 1;
@@ -661,6 +759,7 @@ __global__ __launch_bounds__(256) void score_rselect_kernel(
       rho = (lo + hi) / 2;
     }
   }
+  float kth = -__builtin_inff();
   if (ok) {
     int n_sort = 64;  // power of two >= max(c, k)
     while (n_sort < c || n_sort < k) n_sort <<= 1;
@@ -671,15 +770,19 @@ __global__ __launch_bounds__(256) void score_rselect_kernel(
       ds[j] = e ? fkey_inv((uint32_t)(e >> 32)) : -__builtin_inff();
       di[j] = e ? index_base + (int64_t)(0xffffffffu - (uint32_t)e) : -1;
     }
+    const uint64_t e = cand[k - 1];
+    kth = e ? fkey_inv((uint32_t)(e >> 32)) : -__builtin_inff();
   } else {
-    // exact: the r-th entry is the largest key below the (r-1)-th
+    // exact: the r-th entry is the largest key (above the floor) below the
+    // (r-1)-th
     uint64_t prev = ~0ull;
     for (int r = 0; r < k; ++r) {
       uint64_t best = 0ull;
       if (prev != 0ull)
         for (int64_t j = t; j < nc; j += 256) {
+          if (has_b && !(sm[j / RS_SEG] >= floor_f)) continue;  // not written
           const uint32_t key = fkey(s[j]);
-          if (selectable(key)) {
+          if (selectable(key) && key >= floor_key) {
             const uint64_t e = rs_key(key, j);
             if (e < prev && e > best) best = e;
           }
@@ -689,9 +792,12 @@ __global__ __launch_bounds__(256) void score_rselect_kernel(
         ds[r] = best ? fkey_inv((uint32_t)(best >> 32)) : -__builtin_inff();
         di[r] = best ? index_base + (int64_t)(0xffffffffu - (uint32_t)best) : -1;
       }
+      if (r == k - 1 && best) kth = fkey_inv((uint32_t)(best >> 32));
       prev = best;
     }
   }
+  // running bound for the next chunk (its GEMM skips segments below it)
+  if (t == 0) thr[q] = has_b && bnd > kth ? bnd : kth;
 }
 
 // ---------------------------------------------------------------------------
@@ -986,7 +1092,9 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     P.n_parts = (int)((n_g + chunk - 1) / chunk);
     P.rows_per_part = chunk;
     P.split = 1;
-    P.spart_bytes = (size_t)n_q * (size_t)chunk * 4;
+    // scores, segment maxima (one per 64 rows), running bound per query
+    P.spart_bytes = (size_t)n_q * (size_t)chunk * 4 + (size_t)n_q * (size_t)(chunk / RS_SEG) * 4 +
+                    (size_t)n_q * 4;
     P.list_entries = (size_t)n_q * (size_t)P.n_parts * (size_t)k;
     return P;
   }
@@ -1043,6 +1151,9 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
   if (n_g > 0 && plan.gemm) {
     const int n_qt = (int)((n_q + GT - 1) / GT);
     const int n_st = plan.n_grp;  // 64-element fp16 stages (128 bytes)
+    const int64_t n_seg = plan.chunk / RS_SEG;
+    float* segmax = spart + n_q * plan.chunk;
+    float* thr = segmax + n_q * n_seg;
     for (int c = 0; c < plan.n_parts; ++c) {
       const int64_t r0 = (int64_t)c * plan.chunk;
       const int64_t nc = n_g - r0 < plan.chunk ? n_g - r0 : plan.chunk;
@@ -1050,10 +1161,11 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
       const int per_xcd = (n_items + 7) / 8;
       hipLaunchKernelGGL(score_gemm_kernel<F16Tag>, dim3((unsigned)(8 * per_xcd)), dim3(256), 0, s,
                          (const _Float16*)Q, n_q, ldq, (const _Float16*)G + r0 * ldg, nc, ldg, n_qt,
-                         n_items, per_xcd, n_st, spart, plan.chunk);
+                         n_items, per_xcd, n_st, spart, plan.chunk, segmax, n_seg,
+                         (const float*)thr, c > 0 ? 1 : 0);
       hipLaunchKernelGGL(score_rselect_kernel, dim3((unsigned)n_q), dim3(256), 0, s,
-                         (const float*)spart, plan.chunk, nc, k, c, plan.n_parts,
-                         index_base + r0, part_s, part_i);
+                         (const float*)spart, plan.chunk, (const float*)segmax, n_seg, thr, nc, k, c,
+                         plan.n_parts, index_base + r0, part_s, part_i);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
