@@ -260,3 +260,42 @@ def test_gemm_plan_misleading_sample():
     want = np.flatnonzero(np.arange(ng) % 4 != 0)[:k]
     np.testing.assert_array_equal(host(ti), np.tile(want, (nq, 1)))
     assert (host(ts) == 1.0).all()
+
+
+def _banded_store(ng, D, chunk, weights, seed):
+    """Rows r of chunk c: weights[c] * e0 + sqrt(1 - weights[c]^2) * (random
+    unit direction orthogonal to e0), fp16."""
+    R = synth.unit_rows(ng, D, seed=seed).astype(np.float64)
+    R[:, 0] = 0
+    R /= np.linalg.norm(R, axis=1, keepdims=True)
+    w = np.asarray(weights, dtype=np.float64)[np.arange(ng) // chunk]
+    G = w[:, None] * np.eye(1, D)[0] + np.sqrt(1 - w ** 2)[:, None] * R
+    return G.astype(np.float16)
+
+
+@pytest.mark.parametrize("order", ["rising", "falling"])
+def test_gemm_plan_running_bound(order):
+    """8192 queries make 8192-row chunks.  Rising: every row of a later chunk
+    beats the bound of the earlier ones (more than 2048 candidates: the
+    sampled threshold above the bound is used).  Falling: nothing after the
+    first chunk beats it (empty chunk lists, segments not written) except one
+    planted copy of a query in the last chunk, which must rank first."""
+    say(f"case: gemm plan running bound, {order} store")
+    nq, D, k, chunk = 8192, 64, 100, 8192
+    ng = 3 * chunk - 100
+    w = [0.1, 0.5, 0.9] if order == "rising" else [0.9, 0.5, 0.1]
+    G = _banded_store(ng, D, chunk, w, seed=61)
+    Q = synth.unit_rows(nq, D, seed=62).astype(np.float64)
+    Q[:, 0] = 0
+    Q = 0.8 * np.eye(1, D)[0] + 0.6 * Q / np.linalg.norm(Q, axis=1, keepdims=True)
+    Q = Q.astype(np.float16)
+    if order == "falling":
+        G[ng - 7] = Q[5]
+    ts, ti = _topk(dev(Q), dev(G), k)
+    sample = np.r_[0:6, 4000:4004, nq - 6:nq]
+    check_topk(host(ts)[sample], host(ti)[sample], O.scores(Q[sample], G), k)
+    if order == "rising":
+        assert (host(ti)[sample] >= 2 * chunk).all()
+    else:
+        assert host(ti)[5, 0] == ng - 7
+        assert (host(ti)[sample][:, 1:] < chunk).all()
