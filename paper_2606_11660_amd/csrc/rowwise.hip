@@ -39,19 +39,43 @@ __device__ inline void load8<__bf16>(const __bf16* p, float (&v)[8]) {
   for (int e = 0; e < 8; ++e) v[e] = (float)a[e];
 }
 
+// Streaming (non-temporal) load of a row chunk read exactly once.
+template <typename T>
+__device__ inline void load8_nt(const T* p, float (&v)[8]);
+template <>
+__device__ inline void load8_nt<float>(const float* p, float (&v)[8]) {
+  const f32x4 a = __builtin_nontemporal_load((const f32x4*)p);
+  const f32x4 b = __builtin_nontemporal_load((const f32x4*)(p + 4));
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+template <>
+__device__ inline void load8_nt<_Float16>(const _Float16* p, float (&v)[8]) {
+  const f16x8 a = __builtin_nontemporal_load((const f16x8*)p);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (float)a[e];
+}
+template <>
+__device__ inline void load8_nt<__bf16>(const __bf16* p, float (&v)[8]) {
+  const i32x4 a = __builtin_nontemporal_load((const i32x4*)p);
+  const bf16x8 b = __builtin_bit_cast(bf16x8, a);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (float)b[e];
+}
+
 template <typename T>
 __device__ inline void store8(T* p, const float (&v)[8]);
 template <>
 __device__ inline void store8<float>(float* p, const float (&v)[8]) {
-  *(f32x4*)p = f32x4{v[0], v[1], v[2], v[3]};
-  *(f32x4*)(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, (f32x4*)p);
+  __builtin_nontemporal_store(f32x4{v[4], v[5], v[6], v[7]}, (f32x4*)(p + 4));
 }
 template <>
 __device__ inline void store8<_Float16>(_Float16* p, const float (&v)[8]) {
   f16x8 a;
 #pragma unroll
   for (int e = 0; e < 8; ++e) a[e] = (_Float16)v[e];
-  *(f16x8*)p = a;
+  __builtin_nontemporal_store(a, (f16x8*)p);
 }
 
 __device__ inline float block_sum256(float v, float* sh) {
@@ -87,7 +111,7 @@ __global__ __launch_bounds__(256) void rowscale_kernel(const TX* __restrict__ X,
     for (int j = 0; j < (CH > 0 ? CH : 1); ++j) {
       const int ch = threadIdx.x + j * 256;
       if (ch < n8) {
-        load8<TX>(x + (int64_t)ch * 8, v[j]);
+        load8_nt<TX>(x + (int64_t)ch * 8, v[j]);
         if (m) {
           float mm[8];
           load8<float>(m + (int64_t)ch * 8, mm);
@@ -149,6 +173,83 @@ __global__ __launch_bounds__(256) void rowscale_kernel(const TX* __restrict__ X,
   }
 }
 
+// Two rows per workgroup (rows 2b and 2b + 1, same column chunks per
+// thread): the scale m is read once for both and twice the bytes are in
+// flight per workgroup.  Same per-row arithmetic and order as above.
+template <typename TX, typename TY, int CH>
+__global__ __launch_bounds__(256) void rowscale2_kernel(const TX* __restrict__ X, int64_t ldx,
+                                                        int64_t n_rows, int64_t D,
+                                                        const float* __restrict__ m, int unit,
+                                                        const float* __restrict__ row_ss,
+                                                        int64_t n_ss, TY* Y, int64_t ldy) {
+  __shared__ float sh[2][4];
+  const int64_t r0 = 2 * (int64_t)blockIdx.x;
+  const bool two = r0 + 1 < n_rows;
+  const int n8 = (int)(D / 8);
+  float v[2][CH][8];
+  float ss[2] = {0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < CH; ++j) {
+    const int ch = threadIdx.x + j * 256;
+    if (ch < n8) {
+      load8_nt<TX>(X + r0 * ldx + (int64_t)ch * 8, v[0][j]);
+      if (two) load8_nt<TX>(X + (r0 + 1) * ldx + (int64_t)ch * 8, v[1][j]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < CH; ++j) {
+    const int ch = threadIdx.x + j * 256;
+    if (ch < n8) {
+      if (m) {
+        float mm[8];
+        load8<float>(m + (int64_t)ch * 8, mm);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          v[0][j][e] *= mm[e];
+          v[1][j][e] *= mm[e];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        ss[0] += v[0][j][e] * v[0][j][e];
+        ss[1] += v[1][j][e] * v[1][j][e];
+      }
+    }
+  }
+  if (row_ss) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      ss[h] = 0.f;
+      if (h == 0 || two)
+        for (int64_t p = 0; p < n_ss; ++p) ss[h] += row_ss[(r0 + h) * n_ss + p];
+    }
+  } else if (unit) {
+    const float a = wave_sum(ss[0]), b = wave_sum(ss[1]);
+    if ((threadIdx.x & 63) == 0) {
+      sh[0][threadIdx.x >> 6] = a;
+      sh[1][threadIdx.x >> 6] = b;
+    }
+    __syncthreads();
+    ss[0] = (sh[0][0] + sh[0][1]) + (sh[0][2] + sh[0][3]);
+    ss[1] = (sh[1][0] + sh[1][1]) + (sh[1][2] + sh[1][3]);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (h == 1 && !two) break;
+    const float sc = row_scale(ss[h], unit);
+    TY* y = Y + (r0 + h) * ldy;
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      const int ch = threadIdx.x + j * 256;
+      if (ch < n8) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[h][j][e] *= sc;
+        store8<TY>(y + (int64_t)ch * 8, v[h][j]);
+      }
+    }
+  }
+}
+
 template <typename TX, typename TY>
 hipError_t launch_rowscale_t(const void* X, int64_t ldx, int64_t n_rows, int64_t D,
                              const float* m, int unit, const float* row_ss, int64_t n_ss,
@@ -159,6 +260,17 @@ hipError_t launch_rowscale_t(const void* X, int64_t ldx, int64_t n_rows, int64_t
   TY* y = (TY*)Y;
 #define ATTR_RS(CH) \
   hipLaunchKernelGGL((rowscale_kernel<TX, TY, CH>), grid, block, 0, s, x, ldx, D, m, unit, row_ss, n_ss, y, ldy)
+  if (m && n8 <= 1024 && n_rows >= 2) {  // the scale is read once per two rows
+    dim3 g2((unsigned)((n_rows + 1) / 2));
+#define ATTR_R2(CH)                                                                        \
+  hipLaunchKernelGGL((rowscale2_kernel<TX, TY, CH>), g2, block, 0, s, x, ldx, n_rows, D, m, \
+                     unit, row_ss, n_ss, y, ldy)
+    if (n8 <= 256) ATTR_R2(1);
+    else if (n8 <= 512) ATTR_R2(2);
+    else ATTR_R2(4);
+#undef ATTR_R2
+    return hipGetLastError();
+  }
   if (n8 <= 256) ATTR_RS(1);
   else if (n8 <= 512) ATTR_RS(2);
   else if (n8 <= 1024) ATTR_RS(4);
@@ -192,7 +304,7 @@ __global__ __launch_bounds__(256) void colsumsq_kernel(const TX* __restrict__ X,
   for (; r + 8 <= r1; r += 8) {
     float v[8][8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) load8<TX>(X + (r + u) * ldx + c0, v[u]);
+    for (int u = 0; u < 8; ++u) load8_nt<TX>(X + (r + u) * ldx + c0, v[u]);
     float f[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {

@@ -60,6 +60,34 @@ def test_diag_apply_fp16_inplace_and_fp32_out():
     np.testing.assert_allclose(host(Y2), O.precond_apply(X, "diag", m, unit_norm=False), rtol=1e-6)
 
 
+@pytest.mark.parametrize("D", [8192, 1000])
+def test_diag_apply_many_rows(D):
+    """4500 rows take the row-walk kernel (1024 workgroups, 4 or 5 rows each,
+    next row prefetched): fp16 in place, fp16 -> fp32, unnormalised; a
+    zero row and a zero scale column."""
+    say(f"case: apply DIAG many rows D={D}")
+    n = 4500
+    rng = np.random.default_rng(D + 1)
+    X = (rng.standard_normal((n, D)) * rng.uniform(0.1, 5, size=(n, 1))).astype(np.float16)
+    X[4499] = 0
+    m = rng.uniform(0.1, 10, size=D).astype(np.float32)
+    m[3] = 0.0
+    Xd, md = dev(X), dev(m)
+    Y32 = torch.empty((n, D), dtype=torch.float32, device="cuda")
+    Yu = torch.empty((n, D), dtype=torch.float32, device="cuda")
+    P.attr_precond_apply(Xd, P.PRECOND_DIAG, md, True, Y32)
+    P.attr_precond_apply(Xd, P.PRECOND_DIAG, md, False, Yu)
+    P.attr_precond_apply(Xd, P.PRECOND_DIAG, md, True, Xd)          # in place, last
+    torch.cuda.synchronize()
+    ref = O.precond_apply(X, "diag", m, unit_norm=True)
+    err32 = row_rel_l2(host(Y32), ref)
+    say("fp32 out max row rel-L2", err32.max())
+    assert err32.max() <= 1e-5
+    assert (host(Y32)[4499] == 0).all() and (host(Xd)[4499] == 0).all()
+    assert _f16_ulp_close(host(Xd), ref, 1.0).all()
+    np.testing.assert_allclose(host(Yu), O.precond_apply(X, "diag", m, unit_norm=False), rtol=1e-6)
+
+
 @pytest.mark.parametrize("dtype", ["f16", "f32"])
 def test_diag_accumulate(dtype):
     say(f"case: accumulate DIAG {dtype}")
