@@ -209,3 +209,43 @@ def test_bench_launch_full_batch_sampled():
     say("full-batch sampled max row rel-L2", err.max())
     assert err.max() <= BF16_DESIGN
     assert np.isfinite(host(out)).all()
+
+
+def test_llama1b_bench_launch_sampled():
+    """The bench's 1B-shaped launch: 16 examples with ragged lengths packed
+    back to back (row_offset / length; 21900 tokens x 112 modules, 33 GB of
+    bf16 inputs) in one call; examples 0, 7 and 15 are recomputed by the
+    oracle from the same device values (read back, exact bf16 -> fp32)."""
+    wl = synth.LLAMA1B
+    B, T, k = 16, wl.T, wl.k
+    lengths = synth.example_lengths(wl.n_examples)[:B]
+    offs = np.concatenate([[0], np.cumsum(lengths.astype(np.int64))[:-1]])
+    tot = int(lengths.sum())
+    say("case: 1B bench launch B=16 packed, tokens", tot)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(77)
+    mods, RS = [], []
+    for m, md in enumerate(wl.modules):
+        a = torch.randn((tot, md.d_in), generator=gen, device="cuda", dtype=torch.bfloat16)
+        g = (torch.randn((tot, md.d_out), generator=gen, device="cuda") * 1e-2).to(torch.bfloat16)
+        R, S = synth.projection_pair(wl, m)
+        mods.append(P.Module(a, g, dev(R), dev(S), m * k * k))
+        RS.append((R, S))
+    out = torch.empty((B, wl.D), dtype=torch.float32, device="cuda")
+    P.attr_project(mods, k, B, T, out, row_offset=torch.from_numpy(offs).cuda(),
+                   length=torch.from_numpy(lengths.astype(np.int32)).cuda())
+    torch.cuda.synchronize()
+    got = host(out)
+    assert np.isfinite(got).all()
+    for i in (0, 7, 15):
+        r0, n_i = int(offs[i]), int(lengths[i])
+        blocks = []
+        for M, (R, S) in zip(mods, RS):
+            a = M.a[r0:r0 + n_i].float().cpu().numpy()[None]
+            g = M.g[r0:r0 + n_i].float().cpu().numpy()[None]
+            blocks.append(O.project(a, g, R, S))
+        err = row_rel_l2(got[i:i + 1], O.project_concat(blocks))
+        say(f"example {i} (length {n_i}) row rel-L2", err[0])
+        assert err[0] <= BF16_DESIGN
+    del mods, out
+    torch.cuda.empty_cache()
