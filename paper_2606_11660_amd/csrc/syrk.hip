@@ -3,12 +3,14 @@
 // table; TrackStar's Fisher fitting step in section "Attribution Pipelines").
 //
 // The contraction runs over rows of X, so the MFMA operands need K = row
-// index contiguous.  Rows are processed in chunks of up to 65536: a
+// index contiguous.  Rows are processed in chunks of up to 262144: a
 // transpose kernel writes the chunk as XT [D, C] (64 x 64 tiles through LDS;
 // rows past the end become zeros), then the 256 x 256 block-tile GEMM core
 // computes only the upper-triangle tiles (tp <= tq) of XT XT^T.  Each chunk
-// is split into J <= 4 K-slices computed by separate workgroups, so that
-// 528 tiles x J slices fill the 256 CUs; slice results go to fp32 partial
+// is split into J <= 16 K-slices computed by separate workgroups (at D =
+// 8192, 528 tiles x 16 slices are 33 whole rounds of the 256 CUs; chunks of
+// 65536 rows left a quarter-full last round and took 5% longer); slice
+// results go to fp32 partial
 // tiles and a reduce kernel adds them, in slice order, into an fp64
 // accumulator.  Precision: fp32 MFMA accumulation over at most 16384 rows,
 // fp64 across slices and chunks, one rounding into H at the end of the call
@@ -22,7 +24,10 @@
 namespace attr {
 namespace {
 
-constexpr int SYRK_CHUNK = 65536;
+#ifndef ATTR_SYRK_CHUNK
+#define ATTR_SYRK_CHUNK 262144  // rows per transpose + SYRK launch (16 K-slices: whole rounds of 256 CUs)
+#endif
+constexpr int SYRK_CHUNK = ATTR_SYRK_CHUNK;
 constexpr int TILE_E = GT * GT;  // elements per tile
 
 // XT[c][r] = X[r0 + r][c] for r < C (zero past n_rows), c < D.  64 x 64
