@@ -134,7 +134,8 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
  * once into H, so results are deterministic.
  *
  *   X, ldx   device [n_rows, D] rows: DIAG takes ATTR_F16, ATTR_BF16 or
- *            ATTR_F32, FULL takes ATTR_F16 or ATTR_BF16; ldx >= D
+ *            ATTR_F32, FULL takes ATTR_F16 or ATTR_BF16; ldx >= D (FULL:
+ *            ldx <= 65536, so that 16384 rows span at most 2 GiB)
  *   D        multiple of 8 (DIAG) or of 64 (FULL); FULL needs D <= 32768
  *   mode     ATTR_PRECOND_DIAG or ATTR_PRECOND_FULL
  *   ws       attr_precond_accumulate_workspace_size(n_rows, D, x_dtype, mode)

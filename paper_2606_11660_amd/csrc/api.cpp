@@ -245,7 +245,7 @@ size_t attr_precond_accumulate_workspace_size(int64_t n_rows, int64_t D, attr_dt
     return align_up((size_t)attr::colsumsq_panels(n_rows, D) * (size_t)D * sizeof(double));
   if (mode == ATTR_PRECOND_FULL) {
     const attr::SyrkPlan P = attr::plan_syrk(n_rows, D);
-    return align_up(P.xt_bytes) + align_up(P.part_bytes) + align_up(P.h64_bytes);
+    return align_up(P.part_bytes) + align_up(P.h64_bytes);
   }
   return 0;
 }
@@ -272,6 +272,8 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
     if (!aligned16(X) || !aligned16(H)) return fail(ATTR_ERR_ALIGNMENT, "X and H must be 16-byte aligned");
     if (full && D % 64) return fail(ATTR_ERR_ALIGNMENT, "FULL needs D a multiple of 64");
     if (full && D > 32768) return fail(ATTR_ERR_UNSUPPORTED, "FULL needs D <= 32768");
+    if (full && ldx > 65536)
+      return fail(ATTR_ERR_UNSUPPORTED, "FULL needs ldx <= 65536 (16384 rows must span < 2 GiB)");
     if (overlap(span_of(X, n_rows, D, ldx, eb), span_of(H, full ? D : 1, D, D, 4)))
       return fail(ATTR_ERR_INVALID_ARG, "X and H overlap");
     if (n_rows == 0) return ATTR_OK;
@@ -284,11 +286,9 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
     hipError_t e;
     if (full) {
       const attr::SyrkPlan P = attr::plan_syrk(n_rows, D);
-      char* b = static_cast<char*>(ws);
-      char* xt = b;
-      char* part = xt + align_up(P.xt_bytes);
+      char* part = static_cast<char*>(ws);
       char* h64 = part + align_up(P.part_bytes);
-      e = attr::launch_syrk(x_dtype == ATTR_BF16, X, ldx, n_rows, D, H, P, xt, part, h64,
+      e = attr::launch_syrk(x_dtype == ATTR_BF16, X, ldx, n_rows, D, H, P, part, h64,
                             static_cast<hipStream_t>(stream));
     } else {
       e = attr::launch_colsumsq((int)x_dtype, X, ldx, n_rows, D, H, static_cast<double*>(ws),

@@ -218,4 +218,175 @@ struct GemmCore {
   }
 };
 
+// The same block tile for K-major operands: C[m][n] += sum_k AT[k][m] BT[k][n]
+// with K-rows of the tile's 256 contiguous columns (A: rows of AT from the
+// tile's first column, stride lda; B likewise).  A stage is 64 K-rows of
+// 512 bytes per operand, loaded by the same direct-to-LDS instructions (two
+// K-rows per instruction); in LDS the 32-byte piece P of K-row r sits at
+// P ^ g(r), g(r) = (r & 3) | ((r >> 3) & 1) << 2, so that the 16 K-rows one
+// fragment read touches fall into distinct banks.  Fragments are read with
+// ds_read_b64_tr_b16, which transposes 4 x 16 blocks of 16-bit values within
+// each 16-lane group: lane i of group rg receives column i of four
+// consecutive K-rows; two such reads give the 8 K-values of an MFMA operand.
+// It issues twice as many LDS reads as the row-major core (512 instead of
+// 1024 bytes each) and needs no transposed copy of the operands.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ inline i32x2 lds_read_tr16(uint32_t byte_addr) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(uintptr_t)byte_addr);
+  return __builtin_bit_cast(i32x2, v);
+}
+__device__ inline int kmajor_swz(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
+
+template <typename Tag>
+struct GemmCoreT {
+  f32x4 acc[8][8];
+
+  __device__ inline void zero() {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // n_st stages of 64 K-rows; K-rows past a descriptor's range read zeros.
+  // Byte offsets within a descriptor must fit 31 bits.
+  __device__ inline void run(GemmSmem& sm, const i32x4& da, int64_t lda, const i32x4& db,
+                             int64_t ldb, int n_st) {
+    if (n_st <= 0) return;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
+    const int wm = wave >> 1, wn = wave & 1;
+    // loads: instruction h (0..7) of a wave covers K-rows 16 wave + 2 h +
+    // lane / 32; the lane's LDS chunk s = lane % 32 receives global chunk
+    // ((s / 2) ^ g(row)) * 2 + s % 2; offsets carry -1024 (h % 4) for the
+    // instruction offset that places four loads behind one M0 write
+    const int lr = lane >> 5, s = lane & 31;
+    uint32_t oa[8], ob[8];
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+      const int row = 16 * wave + 2 * h + lr;
+      const int c = (((s >> 1) ^ kmajor_swz(row)) << 1) | (s & 1);
+      oa[h] = (uint32_t)((int64_t)row * lda * 2 + c * 16) - 1024u * (uint32_t)(h & 3);
+      ob[h] = (uint32_t)((int64_t)row * ldb * 2 + c * 16) - 1024u * (uint32_t)(h & 3);
+    }
+    const uint32_t kst_a = (uint32_t)(64 * lda * 2), kst_b = (uint32_t)(64 * ldb * 2);
+    const uint32_t sa0 = (uint32_t)(uintptr_t)&sm.a[0][0], sb0 = (uint32_t)(uintptr_t)&sm.b[0][0];
+    const uint32_t lds_a = sa0 + (uint32_t)(16 * wave) * 512u;
+    const uint32_t lds_b = sb0 + (uint32_t)(16 * wave) * 512u;
+    auto issue_grp = [&](int st, int g) {
+      const uint32_t sb = (uint32_t)(st & 1) * G_SLOT;
+      set_m0((g < 2 ? lds_a : lds_b) + sb + (uint32_t)(g & 1) * 4096u);
+    };
+    auto issue_u = [&](int st, int g, auto uc) {
+      constexpr int u = decltype(uc)::value;
+      const uint32_t ko = st < n_st ? 0u : 0x80000000u;
+      const int h = 4 * (g & 1) + u;
+      if (g < 2) {
+        lds_dma16_m0<1024 * u>(da, oa[h] + (uint32_t)st * kst_a + ko);
+      } else {
+        lds_dma16_m0<1024 * u>(db, ob[h] + (uint32_t)st * kst_b + ko);
+      }
+    };
+    auto issue_all = [&](int st) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        issue_grp(st, g);
+        issue_u(st, g, std::integral_constant<int, 0>{});
+        issue_u(st, g, std::integral_constant<int, 1>{});
+        issue_u(st, g, std::integral_constant<int, 2>{});
+        issue_u(st, g, std::integral_constant<int, 3>{});
+      }
+    };
+    // fragment of 16-column block t (of the wave's 128) in K-half hk: lane
+    // (rg, i) reads K-rows 32 hk + 8 rg + 4 h + i / 4 (h = 0, 1), columns
+    // 16 t + 4 (i % 4) .. + 3 of its operand half wx
+    const int rg = lane >> 4, i4 = lane & 15;
+    const int gl = (i4 >> 2) | ((rg & 1) << 2);  // g() of every K-row this lane reads
+    const uint32_t rowb = (uint32_t)(8 * rg + (i4 >> 2)) * 512u + 8u * (uint32_t)(i4 & 3);
+    auto frag = [&](uint32_t base, int wx, int t, int hk) -> i32x4 {
+      const uint32_t a0 =
+          base + (uint32_t)(32 * hk) * 512u + rowb + 32u * (uint32_t)((8 * wx + t) ^ gl);
+      const i32x2 lo = lds_read_tr16(a0);
+      const i32x2 hi = lds_read_tr16(a0 + 4u * 512u);
+      return i32x4{lo.x, lo.y, hi.x, hi.y};
+    };
+    // the 16 fragments of a half, two per call, B first (as in GemmCore)
+    auto read_pair = [&](int i, uint32_t pa, uint32_t pb, int hk, i32x4 (&fa)[8], i32x4 (&fb)[8]) {
+      if (i < 4) {
+        fb[2 * i] = frag(pb, wn, 2 * i, hk);
+        fb[2 * i + 1] = frag(pb, wn, 2 * i + 1, hk);
+      } else {
+        fa[2 * i - 8] = frag(pa, wm, 2 * i - 8, hk);
+        fa[2 * i - 7] = frag(pa, wm, 2 * i - 7, hk);
+      }
+    };
+    auto mma_row = [&](int i, const i32x4 (&fa)[8], const i32x4 (&fb)[8]) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = mma16(Tag{}, fa[i], fb[j], acc[i][j]);
+    };
+    i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
+
+    // same pipeline as GemmCore::run
+    issue_all(0);
+    gemm_wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+    issue_all(1);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      h0a[i] = frag(sa0, wm, i, 0);
+      h0b[i] = frag(sb0, wn, i, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      read_pair(i, sa0, sb0, 1, h1a, h1b);
+      __builtin_amdgcn_sched_barrier(0);
+      mma_row(i, h0a, h0b);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int st = 1; st < n_st; ++st) {
+      gemm_wait_vm<0>();
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+      const uint32_t pa = sa0 + (uint32_t)(st & 1) * G_SLOT;
+      const uint32_t pb = sb0 + (uint32_t)(st & 1) * G_SLOT;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, pa, pb, 0, h0a, h0b);
+        if ((i & 1) == 0) {
+          issue_grp(st + 1, i >> 1);
+          issue_u(st + 1, i >> 1, std::integral_constant<int, 0>{});
+        } else {
+          issue_u(st + 1, i >> 1, std::integral_constant<int, 2>{});
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
+        if ((i & 1) == 0) {
+          issue_u(st + 1, i >> 1, std::integral_constant<int, 1>{});
+        } else {
+          issue_u(st + 1, i >> 1, std::integral_constant<int, 3>{});
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, pa, pb, 1, h1a, h1b);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_row(i, h0a, h0b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);
+    gemm_wait_vm<0>();
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+  }
+};
+
 }  // namespace attr

@@ -100,11 +100,11 @@ struct SyrkPlan {
   int J;           // K-slices per chunk
   int64_t Cs;      // rows per slice
   int64_t C;       // rows per chunk (J * Cs)
-  size_t xt_bytes, part_bytes, h64_bytes;
+  size_t part_bytes, h64_bytes;
 };
 SyrkPlan plan_syrk(int64_t n_rows, int64_t D);
 hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, int64_t D, float* H,
-                       const SyrkPlan& P, void* xt, void* part, void* h64, hipStream_t s);
+                       const SyrkPlan& P, void* part, void* h64, hipStream_t s);
 
 int apply_full_nss(int64_t D);
 size_t apply_full_workspace(int64_t n_rows, int64_t D, int unit);

@@ -2,20 +2,20 @@
 // autocorrelation / empirical Fisher preconditioner of the method-family
 // table; TrackStar's Fisher fitting step in section "Attribution Pipelines").
 //
-// The contraction runs over rows of X, so the MFMA operands need K = row
-// index contiguous.  Rows are processed in chunks of up to 262144: a
-// transpose kernel writes the chunk as XT [D, C] (64 x 64 tiles through LDS;
-// rows past the end become zeros), then the 256 x 256 block-tile GEMM core
-// computes only the upper-triangle tiles (tp <= tq) of XT XT^T.  Each chunk
-// is split into J <= 16 K-slices computed by separate workgroups (at D =
-// 8192, 528 tiles x 16 slices are 33 whole rounds of the 256 CUs; chunks of
-// 65536 rows left a quarter-full last round and took 5% longer); slice
-// results go to fp32 partial
-// tiles and a reduce kernel adds them, in slice order, into an fp64
-// accumulator.  Precision: fp32 MFMA accumulation over at most 16384 rows,
-// fp64 across slices and chunks, one rounding into H at the end of the call
-// (the spectrum of H spans ~6 decades on low-rank-plus-noise stores, and long
-// fp32 accumulation visibly perturbs its small eigenvalues).
+// The contraction runs over rows of X (K = row index), so the operands are
+// K-major: the GEMM core for K-major operands reads 64-row x 256-column
+// stages of X itself and transposes them while reading its MFMA fragments
+// out of LDS (no transposed copy of X is written).  Only the upper-triangle
+// tiles (tp <= tq) of X^T X are computed.  Rows are taken in chunks of up to
+// 262144; a chunk is split into K-slices of 16384 rows computed by separate
+// workgroups (at D = 8192, 528 tiles x 16 slices are 33 whole rounds of the
+// 256 CUs; chunks of 65536 rows left a quarter-full last round and took 5%
+// longer), and only the slices that hold rows are launched.  Slice results
+// go to fp32 partial tiles and a reduce kernel adds them, in slice order,
+// into an fp64 accumulator.  Precision: fp32 MFMA accumulation over at most
+// 16384 rows, fp64 across slices and chunks, one rounding into H at the end
+// of the call (the spectrum of H spans ~6 decades on low-rank-plus-noise
+// stores, and long fp32 accumulation visibly perturbs its small eigenvalues).
 // Deterministic: fixed tile, slice and chunk orders, no atomics.
 #include "common.h"
 #include "gemm.h"
@@ -29,41 +29,6 @@ namespace {
 #endif
 constexpr int SYRK_CHUNK = ATTR_SYRK_CHUNK;
 constexpr int TILE_E = GT * GT;  // elements per tile
-
-// XT[c][r] = X[r0 + r][c] for r < C (zero past n_rows), c < D.  64 x 64
-// tiles through LDS; global reads and writes are 16-byte vectors along rows.
-template <typename T>
-__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ X, int64_t ldx,
-                                                        int64_t n_rows, int64_t r0, int64_t D,
-                                                        int64_t C, T* __restrict__ XT) {
-  __shared__ uint16_t tile[64][64 + 2];
-  const int64_t tr = (int64_t)blockIdx.x * 64;  // chunk-row block
-  const int64_t tc = (int64_t)blockIdx.y * 64;  // column block (D is a multiple of 64)
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int lr = (t >> 3) + 32 * h, lc = (t & 7) * 8;
-    const int64_t row = r0 + tr + lr;
-    i32x4 v = {0, 0, 0, 0};
-    if (row < n_rows) v = *(const i32x4*)(X + row * ldx + tc + lc);
-    const uint32_t w[4] = {(uint32_t)v.x, (uint32_t)v.y, (uint32_t)v.z, (uint32_t)v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      tile[lr][lc + 2 * e] = (uint16_t)(w[e] & 0xffffu);
-      tile[lr][lc + 2 * e + 1] = (uint16_t)(w[e] >> 16);
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int oc = (t >> 3) + 32 * h, orr = (t & 7) * 8;  // output row (column of X), 8 chunk rows
-    uint32_t w[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      w[e] = (uint32_t)tile[orr + 2 * e][oc] | ((uint32_t)tile[orr + 2 * e + 1][oc] << 16);
-    *(i32x4*)(XT + (tc + oc) * C + tr + orr) = i32x4{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-  }
-}
 
 // Upper-triangle tile u -> (tp, tq), tp <= tq, row-major over tp.
 __device__ inline void upper_tile(int u, int nt, int& tp, int& tq) {
@@ -107,9 +72,9 @@ __device__ inline void band_tile(int v, int nt, int& tp, int& tq) {
 // band-ordered tile range [x per_xcd, (x + 1) per_xcd), so the workgroups
 // resident on one XCD share row blocks through its L2.
 template <typename Tag, typename T>
-__global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ XT, int64_t C,
-                                                   int64_t D, int nt, int n_up, int J,
-                                                   int per_xcd, int64_t Cs,
+__global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ X, int64_t ldx,
+                                                   int64_t n_rows, int64_t r0, int64_t D, int nt,
+                                                   int n_up, int J, int per_xcd, int64_t Cs,
                                                    float* __restrict__ part) {
   __shared__ GemmSmem sm;
   const int l = (int)(blockIdx.x >> 3);
@@ -119,17 +84,25 @@ __global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ XT, int
   int tp, tq;
   band_tile(v, nt, tp, tq);
   const int u = tp * nt - tp * (tp - 1) / 2 + (tq - tp);  // row-major upper index
-  int64_t np = D - (int64_t)tp * GT, nq = D - (int64_t)tq * GT;
-  np = np > GT ? GT : np;
-  nq = nq > GT ? GT : nq;
-  const T* a = XT + (int64_t)tp * GT * C + (int64_t)j * Cs;
-  const T* b = XT + (int64_t)tq * GT * C + (int64_t)j * Cs;
-  // range: the tile's rows, each C long (the K window is [0, Cs) of that)
-  const i32x4 da = make_desc(a, (uint32_t)((np - 1) * C * 2 + Cs * 2));
-  const i32x4 db = make_desc(b, (uint32_t)((nq - 1) * C * 2 + Cs * 2));
-  GemmCore<Tag> core;
+  // slice j: rows [rs, rs + nr) of X; operand rows start at the tile's
+  // first column.  The descriptor range ends at the slice's last row (or at
+  // the matrix end, column D of row n_rows - 1): K-rows past it read zeros;
+  // columns past D of a row read the next row's values, which only reach
+  // outputs of columns >= D (never stored).
+  const int64_t rs = r0 + (int64_t)j * Cs;
+  int64_t nr = n_rows - rs;
+  nr = nr > Cs ? Cs : nr;
+  auto range = [&](int64_t c0) -> uint32_t {
+    if (nr <= 0) return 0u;
+    const int64_t lim_slice = nr * ldx, lim_mat = (n_rows - 1 - rs) * ldx + (D - c0);
+    return (uint32_t)((lim_slice < lim_mat ? lim_slice : lim_mat) * 2);
+  };
+  const int64_t ca = (int64_t)tp * GT, cb = (int64_t)tq * GT;
+  const i32x4 da = make_desc(X + rs * ldx + ca, range(ca));
+  const i32x4 db = make_desc(X + rs * ldx + cb, range(cb));
+  GemmCoreT<Tag> core;
   core.zero();
-  core.run(sm, da, C, db, db, C, (int)(Cs / GKS), (int)(Cs / GKS));
+  core.run(sm, da, ldx, db, ldx, (int)(Cs / GKS));
   float* dst = part + ((int64_t)j * n_up + u) * TILE_E;
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -193,37 +166,31 @@ SyrkPlan plan_syrk(int64_t n_rows, int64_t D) {
   P.J = J;
   P.Cs = cs;
   P.C = cs * J;
-  P.xt_bytes = (size_t)D * (size_t)P.C * 2;
   P.part_bytes = (size_t)J * (size_t)P.n_up * TILE_E * 4;
   P.h64_bytes = (size_t)P.n_up * TILE_E * 8;
   return P;
 }
 
 hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, int64_t D, float* H,
-                       const SyrkPlan& P, void* xt, void* part, void* h64, hipStream_t s) {
+                       const SyrkPlan& P, void* part, void* h64, hipStream_t s) {
   const int64_t n_e = (int64_t)P.n_up * TILE_E;
   hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n_e + 255) / 256)), dim3(256), 0, s,
                      (double*)h64, n_e);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const int per_xcd = (P.n_up + 7) / 8;  // tiles per XCD and slice
   for (int64_t r0 = 0; r0 < n_rows; r0 += P.C) {
-    dim3 gt((unsigned)(P.C / 64), (unsigned)((D + 63) / 64));
+    const int64_t rows = n_rows - r0 < P.C ? n_rows - r0 : P.C;
+    const int Jc = (int)((rows + P.Cs - 1) / P.Cs);  // slices holding rows
+    dim3 gs((unsigned)(8 * per_xcd * Jc));
     if (bf16)
-      hipLaunchKernelGGL(transpose_kernel<__bf16>, gt, dim3(256), 0, s, (const __bf16*)X, ldx, n_rows,
-                         r0, D, P.C, (__bf16*)xt);
+      hipLaunchKernelGGL((syrk_kernel<Bf16Tag, __bf16>), gs, dim3(256), 0, s, (const __bf16*)X, ldx,
+                         n_rows, r0, D, P.nt, P.n_up, Jc, per_xcd, P.Cs, (float*)part);
     else
-      hipLaunchKernelGGL(transpose_kernel<_Float16>, gt, dim3(256), 0, s, (const _Float16*)X, ldx,
-                         n_rows, r0, D, P.C, (_Float16*)xt);
-    const int per_xcd = (P.n_up + 7) / 8;  // tiles per XCD and slice
-    dim3 gs((unsigned)(8 * per_xcd * P.J));
-    if (bf16)
-      hipLaunchKernelGGL((syrk_kernel<Bf16Tag, __bf16>), gs, dim3(256), 0, s, (const __bf16*)xt, P.C,
-                         D, P.nt, P.n_up, P.J, per_xcd, P.Cs, (float*)part);
-    else
-      hipLaunchKernelGGL((syrk_kernel<F16Tag, _Float16>), gs, dim3(256), 0, s, (const _Float16*)xt,
-                         P.C, D, P.nt, P.n_up, P.J, per_xcd, P.Cs, (float*)part);
+      hipLaunchKernelGGL((syrk_kernel<F16Tag, _Float16>), gs, dim3(256), 0, s, (const _Float16*)X,
+                         ldx, n_rows, r0, D, P.nt, P.n_up, Jc, per_xcd, P.Cs, (float*)part);
     hipLaunchKernelGGL(syrk_reduce_kernel, dim3((unsigned)((n_e + 255) / 256)), dim3(256), 0, s,
-                       (const float*)part, P.J, n_e, (double*)h64);
+                       (const float*)part, Jc, n_e, (double*)h64);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
