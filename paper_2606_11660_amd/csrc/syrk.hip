@@ -113,13 +113,40 @@ __global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ X, int6
 }
 
 // h64[u][e] += sum_j part[j][u][e], slices in order (fragment-order layout).
+// Four elements per thread: the J partial vectors (read once, non-temporal)
+// are all in flight before the sums are formed.
 __global__ __launch_bounds__(256) void syrk_reduce_kernel(const float* __restrict__ part, int J,
                                                           int64_t n_e, double* __restrict__ h64) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= n_e) return;
-  double s = 0.0;
-  for (int j = 0; j < J; ++j) s += (double)part[(int64_t)j * n_e + e];
-  h64[e] += s;
+  const int64_t e4 = (int64_t)blockIdx.x * 256 + threadIdx.x;  // n_e is a multiple of 4
+  if (4 * e4 >= n_e) return;
+  const f32x4* p4 = reinterpret_cast<const f32x4*>(part);
+  const int64_t n4 = n_e / 4;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  int j = 0;
+  for (; j + 8 <= J; j += 8) {
+    f32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(p4 + (int64_t)(j + u) * n4 + e4);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      s0 += (double)v[u].x;
+      s1 += (double)v[u].y;
+      s2 += (double)v[u].z;
+      s3 += (double)v[u].w;
+    }
+  }
+  for (; j < J; ++j) {
+    const f32x4 v = __builtin_nontemporal_load(p4 + (int64_t)j * n4 + e4);
+    s0 += (double)v.x;
+    s1 += (double)v.y;
+    s2 += (double)v.z;
+    s3 += (double)v.w;
+  }
+  double* h = h64 + 4 * e4;
+  h[0] += s0;
+  h[1] += s1;
+  h[2] += s2;
+  h[3] += s3;
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(double* __restrict__ p, int64_t n) {
@@ -189,7 +216,7 @@ hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, in
     else
       hipLaunchKernelGGL((syrk_kernel<F16Tag, _Float16>), gs, dim3(256), 0, s, (const _Float16*)X,
                          ldx, n_rows, r0, D, P.nt, P.n_up, Jc, per_xcd, P.Cs, (float*)part);
-    hipLaunchKernelGGL(syrk_reduce_kernel, dim3((unsigned)((n_e + 255) / 256)), dim3(256), 0, s,
+    hipLaunchKernelGGL(syrk_reduce_kernel, dim3((unsigned)((n_e / 4 + 255) / 256)), dim3(256), 0, s,
                        (const float*)part, Jc, n_e, (double*)h64);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
