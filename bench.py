@@ -254,7 +254,9 @@ def _profile_row(row, dev):
     """One row of the path on its own, sized for counter runs (rocprofv3
     --pmc): `syrk` / `full_apply` on a 131072 x 8192 low-rank-plus-noise
     store, `scan16` / `scan1024` on a 1M x 8192 unit fp16 store with top-100,
-    `llama1b` the 1B-shaped projection row (timed, printed as JSON)."""
+    `diag_acc` / `diag_apply` (DIAG accumulate, DIAG apply + unit norm) on a
+    10^6 x 8192 fp16 store, `llama1b` the 1B-shaped projection row (timed,
+    printed as JSON)."""
     import torch
     import paper_2606_11660_amd as P
     if row == "llama1b":
@@ -264,7 +266,20 @@ def _profile_row(row, dev):
     D = 8192
     gen = torch.Generator(device=dev)
     gen.manual_seed(3)
-    if row in ("syrk", "full_apply"):
+    if row in ("diag_acc", "diag_apply"):
+        N = 1_000_000
+        X = torch.empty((N, D), dtype=torch.float16, device=dev)
+        for i in range(0, N, 65536):
+            n = min(65536, N - i)
+            X[i:i + n] = torch.randn((n, D), generator=gen, device=dev).half()
+        if row == "diag_acc":
+            h = torch.zeros(D, dtype=torch.float32, device=dev)
+            P.attr_precond_accumulate(X, P.PRECOND_DIAG, h)
+        else:
+            m = torch.rand(D, generator=gen, device=dev) + 0.5
+            Y = torch.empty_like(X)
+            P.attr_precond_apply(X, P.PRECOND_DIAG, m, True, Y)
+    elif row in ("syrk", "full_apply"):
         N = 131072
         F = torch.randn((D, 64), generator=gen, device=dev)
         Z = torch.randn((N, 64), generator=gen, device=dev)
@@ -316,7 +331,8 @@ def main():
     ap.add_argument("--quick", action="store_true", help="skip the preconditioner / store-scan rows")
     ap.add_argument("--copy-reference", action="store_true",
                     help="only run the 1 GiB copy used to calibrate traffic counters")
-    ap.add_argument("--profile-row", choices=["syrk", "full_apply", "scan16", "scan1024", "llama1b"],
+    ap.add_argument("--profile-row", choices=["syrk", "full_apply", "scan16", "scan1024", "diag_acc",
+                                              "diag_apply", "llama1b"],
                     help="only run one row of the path once, for counter runs")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
