@@ -35,6 +35,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16
 BATCH = 64
+PROFILE_REPS = 3  # each --profile-row operation runs this often (the first call is cold)
 
 
 def _cpu_baseline(n_sample: int = 6, min_seconds: float = 12.0):
@@ -255,8 +256,8 @@ def _profile_row(row, dev):
     --pmc): `syrk` / `full_apply` on a 131072 x 8192 low-rank-plus-noise
     store, `scan16` / `scan1024` on a 1M x 8192 unit fp16 store with top-100,
     `diag_acc` / `diag_apply` (DIAG accumulate, DIAG apply + unit norm) on a
-    10^6 x 8192 fp16 store, `llama1b` the 1B-shaped projection row (timed,
-    printed as JSON)."""
+    10^6 x 8192 fp16 store, each run PROFILE_REPS times; `llama1b` the
+    1B-shaped projection row (timed, printed as JSON)."""
     import torch
     import paper_2606_11660_amd as P
     if row == "llama1b":
@@ -274,11 +275,13 @@ def _profile_row(row, dev):
             X[i:i + n] = torch.randn((n, D), generator=gen, device=dev).half()
         if row == "diag_acc":
             h = torch.zeros(D, dtype=torch.float32, device=dev)
-            P.attr_precond_accumulate(X, P.PRECOND_DIAG, h)
+            for _ in range(PROFILE_REPS):
+                P.attr_precond_accumulate(X, P.PRECOND_DIAG, h)
         else:
             m = torch.rand(D, generator=gen, device=dev) + 0.5
             Y = torch.empty_like(X)
-            P.attr_precond_apply(X, P.PRECOND_DIAG, m, True, Y)
+            for _ in range(PROFILE_REPS):
+                P.attr_precond_apply(X, P.PRECOND_DIAG, m, True, Y)
     elif row in ("syrk", "full_apply"):
         N = 131072
         F = torch.randn((D, 64), generator=gen, device=dev)
@@ -287,12 +290,14 @@ def _profile_row(row, dev):
         del F, Z
         if row == "syrk":
             H = torch.zeros((D, D), dtype=torch.float32, device=dev)
-            P.attr_precond_accumulate(X, P.PRECOND_FULL, H)
+            for _ in range(PROFILE_REPS):
+                P.attr_precond_accumulate(X, P.PRECOND_FULL, H)
         else:
             B = torch.randn((D, D), generator=gen, device=dev) / D ** 0.5
             M = (B @ B.T + torch.eye(D, device=dev)).contiguous()
             Y = torch.empty_like(X)
-            P.attr_precond_apply(X, P.PRECOND_FULL, M, True, Y)
+            for _ in range(PROFILE_REPS):
+                P.attr_precond_apply(X, P.PRECOND_FULL, M, True, Y)
     else:
         N, nq = 1_000_000, int(row[4:])
         G = torch.empty((N, D), dtype=torch.float16, device=dev)
@@ -303,7 +308,8 @@ def _profile_row(row, dev):
         Q = (q / q.norm(dim=1, keepdim=True)).half()
         ts = torch.empty((nq, 100), dtype=torch.float32, device=dev)
         ti = torch.empty((nq, 100), dtype=torch.int64, device=dev)
-        P.attr_score_topk(Q, G, 100, ts, ti)
+        for _ in range(PROFILE_REPS):
+            P.attr_score_topk(Q, G, 100, ts, ti)
     torch.cuda.synchronize()
     print(json.dumps({"profile_row": row}))
 
