@@ -163,3 +163,19 @@ def test_full_mode_validation(L):
     assert app(FAKE, P.ATTR_F16, 4, 256, 256, P.PRECOND_FULL, H, 1, Y, P.ATTR_F16, 256, None, 0, None) == WORKSPACE
     assert L.attr_precond_apply_workspace_size(4, 256, P.PRECOND_FULL) >= 2 * 256 * 256 * 2
     assert L.attr_precond_apply_workspace_size(4, 256, P.PRECOND_DIAG) == 0
+
+
+def test_build_flags_unprotected_lds_dma_loads():
+    """The build rejects device code where a VALU instruction writes a
+    descriptor SGPR of an inline-asm direct-to-LDS load fewer than five wait
+    states before it (the compiler does not protect loads inside asm)."""
+    from paper_2606_11660_amd.build import lds_dma_hazards
+    bad = "\n".join(["_Zkern:", "\tv_readfirstlane_b32 s6, v38", "\tv_add_u32_e32 v5, v1, v2",
+                     "\tbuffer_load_dwordx4 v5, s[4:7], 0 offen offset:0 lds"])
+    good = "\n".join(["_Zkern:", "\tv_readfirstlane_b32 s6, v38", "\ts_nop 4",
+                      "\tbuffer_load_dwordx4 v5, s[4:7], 0 offen offset:0 lds"])
+    other = "\n".join(["_Zkern:", "\tv_readfirstlane_b32 s9, v38",
+                       "\tbuffer_load_dwordx4 v5, s[4:7], 0 offen offset:0 lds"])
+    assert len(lds_dma_hazards(bad)) == 1
+    assert lds_dma_hazards(good) == []
+    assert lds_dma_hazards(other) == []
