@@ -74,7 +74,7 @@ hipError_t launch_colsumsq(int x_dtype, const void* X, int64_t ldx, int64_t n_ro
 // scoring
 // ---------------------------------------------------------------------------
 struct ScorePlan {
-  int n_qb;              // query blocks (64 queries; 32 for the streaming plan with k > 16)
+  int n_qb;              // query blocks of 64 queries
   int n_grp;             // 128-byte K-groups per row
   int split;             // D-slices (1: fused plan)
   int n_tiles;           // 128-row tiles (split-K plan)

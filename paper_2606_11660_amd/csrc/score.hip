@@ -252,7 +252,7 @@ struct RegList {
   }
 };
 
-template <bool F16, int KMAX, int RING, int GPS>
+template <bool F16, int KMAX, int RING, int GPS, int QPW>
 __global__ __launch_bounds__(256) void score_stream_kernel(
     const char* __restrict__ Q, int64_t n_q, int64_t ldq, const char* __restrict__ G,
     int64_t n_g, int64_t ldg, int n_grp, int k, int64_t rows_per_part, int n_parts, int n_qb,
@@ -265,7 +265,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   constexpr int EB = STag<F16>::bytes;
   constexpr int NS = (KMAX + 63) / 64;
   __shared__ i32x4 ring[RING][(SR + SQ) * CPR];  // store rows, then query rows
-  __shared__ float2 lists[4][16][KMAX];        // per wave, per query: (score, row bits)
+  __shared__ float2 lists[4][QPW][KMAX];       // per wave, per query: (score, row bits)
 
   const uint32_t b = blockIdx.x;
   const int xcd = (int)(b & 7u);
@@ -282,7 +282,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   // wave w holds block queries w, w + 4, ..., w + 60 (slot j = query 4 j + w), so
   // that a partial block spreads its selection work over all four waves
   int nq_w = (int)((nq_blk - wave + 3) / 4);
-  nq_w = nq_w < 0 ? 0 : (nq_w > 16 ? 16 : nq_w);
+  nq_w = nq_w < 0 ? 0 : (nq_w > QPW ? QPW : nq_w);  // the host sizes QPW to the block
   // a store read by a single query block is not kept in L2
   const bool g_nt = n_qb == 1;
 
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   const int total = n_tiles * n_stg;
 
   float2(*wl)[KMAX] = lists[wave];
-  for (int ql = 0; ql < 16; ++ql)
+  for (int ql = 0; ql < QPW; ++ql)
 #pragma unroll
     for (int j = 0; j < NS; ++j)
       if (64 * j + lane < KMAX) wl[ql][64 * j + lane] = float2{-__builtin_inff(), __builtin_bit_cast(float, -1)};
@@ -1070,6 +1070,27 @@ __global__ __launch_bounds__(256) void score_merge_kernel(const float* __restric
 
 }  // namespace
 
+// Streaming-plan launch shape: list capacity KMAX, ring depth RING, K-groups
+// per stage GPS, list slots per wave QPW (a block's queries / 4) and
+// workgroups per CU.  LDS per workgroup = RING x GPS x 16 KB + 4 x QPW x
+// KMAX x 8 B; two workgroups share a CU at <= 80 KB each.  Two per CU hide
+// one another's selection work: at 2M x 8192 fp16 rows and top-100, a
+// three-stage ring at two per CU beat a 256-byte-stage ring at one per CU by
+// 10-15% for 16 and 32 queries; 64 queries at k > 64 need 64 KB of lists and
+// stay at one per CU (32-query blocks, two per CU, read the store twice
+// through L2 and ran ~20% slower).
+struct StreamCfg {
+  int kmax, ring, gps, qpw, per_cu;
+};
+static StreamCfg stream_cfg(int64_t n_q, int k, bool wide) {
+  const int64_t qb = n_q < SQ ? n_q : SQ;
+  if (k <= 32) return {32, 4, 1, 16, 2};
+  if (k <= 64) return qb <= 16 ? StreamCfg{64, 4, 1, 4, 2} : StreamCfg{64, 3, 1, 16, 2};
+  if (qb <= 16) return {128, 4, 1, 4, 2};
+  if (qb <= 32) return {128, 3, 1, 8, 2};
+  return wide ? StreamCfg{128, 3, 2, 16, 1} : StreamCfg{128, 6, 1, 16, 1};
+}
+
 ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes) {
   ScorePlan P{};
   P.n_qb = (int)((n_q + SQB - 1) / SQB);
@@ -1122,12 +1143,12 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     P.spart_bytes = (size_t)split * (size_t)n_g * (size_t)P.n_qb * SQB * 4;
   } else {
     P.split = 1;
-    // streaming plan: 64 queries per workgroup; one workgroup per CU (two for
-    // k <= 32, whose lists are small enough to share the LDS), as many
+    // streaming plan: 64 queries per workgroup; two workgroups per CU when
+    // the ring and the lists fit in half the LDS, else one; as many
     // partitions as workgroups fit at once (an exact multiple of the CU
     // count: 248 workgroups ran ~13% slower than 256 on k <= 32)
-    P.n_qb = (int)((n_q + 63) / 64);
-    int64_t per_wave = (k <= 32 ? 2 : 1) * (int64_t)256;
+    P.n_qb = (int)((n_q + SQ - 1) / SQ);
+    int64_t per_wave = (int64_t)stream_cfg(n_q, k, P.n_grp % 2 == 0).per_cu * 256;
     per_wave = per_wave > 1016 ? 1016 : per_wave;  // the merge takes <= 1024 sources
     int64_t parts = (per_wave + P.n_qb - 1) / P.n_qb;
     const int64_t t64 = (n_g + SR - 1) / SR;
@@ -1172,33 +1193,29 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
   } else if (n_g > 0 && plan.split <= 1) {
     const int parts_pad = (plan.n_parts + 7) / 8 * 8;
     dim3 grid((unsigned)(plan.n_qb * parts_pad)), block(256);
-#define ATTR_SS(F, KM, RG, GP)                                                                   \
-  hipLaunchKernelGGL((score_stream_kernel<F, KM, RG, GP>), grid, block, 0, s, (const char*)Q, n_q,  \
-                     ldq, (const char*)G, n_g, ldg, plan.n_grp, k, plan.rows_per_part, plan.n_parts, \
-                     plan.n_qb, part_s, part_i, index_base)
-    // LDS: ring RING x (GPS x 16 KB) + lists 4 x 16 x KMAX x 8 B <= 160 KB; two
-    // K-groups per stage (256-byte row segments) when the groups pair up
-    const bool wide = plan.n_grp % 2 == 0;
-    if (k <= 32) {  // 80 KB of LDS: two workgroups per CU
-      if (f16) ATTR_SS(true, 32, 4, 1);
-      else ATTR_SS(false, 32, 4, 1);
-    } else if (f16) {
-      if (k <= 64) {
-        if (wide) ATTR_SS(true, 64, 4, 2);
-        else ATTR_SS(true, 64, 8, 1);
-      } else {
-        if (wide) ATTR_SS(true, 128, 3, 2);
-        else ATTR_SS(true, 128, 6, 1);
-      }
-    } else {
-      if (k <= 64) {
-        if (wide) ATTR_SS(false, 64, 4, 2);
-        else ATTR_SS(false, 64, 8, 1);
-      } else {
-        if (wide) ATTR_SS(false, 128, 3, 2);
-        else ATTR_SS(false, 128, 6, 1);
-      }
-    }
+#define ATTR_SS(KM, RG, GP, QW)                                                                  \
+  if (c.kmax == KM && c.ring == RG && c.gps == GP && c.qpw == QW) {                              \
+    launched = true;                                                                             \
+    if (f16)                                                                                     \
+      hipLaunchKernelGGL((score_stream_kernel<true, KM, RG, GP, QW>), grid, block, 0, s,          \
+                         (const char*)Q, n_q, ldq, (const char*)G, n_g, ldg, plan.n_grp, k,      \
+                         plan.rows_per_part, plan.n_parts, plan.n_qb, part_s, part_i, index_base); \
+    else                                                                                         \
+      hipLaunchKernelGGL((score_stream_kernel<false, KM, RG, GP, QW>), grid, block, 0, s,         \
+                         (const char*)Q, n_q, ldq, (const char*)G, n_g, ldg, plan.n_grp, k,      \
+                         plan.rows_per_part, plan.n_parts, plan.n_qb, part_s, part_i, index_base); \
+  }
+    // two K-groups per stage (256-byte row segments) only when the groups pair up
+    const StreamCfg c = stream_cfg(n_q, k, plan.n_grp % 2 == 0);
+    bool launched = false;
+    ATTR_SS(32, 4, 1, 16)
+    ATTR_SS(64, 4, 1, 4)
+    ATTR_SS(64, 3, 1, 16)
+    ATTR_SS(128, 4, 1, 4)
+    ATTR_SS(128, 3, 1, 8)
+    ATTR_SS(128, 3, 2, 16)
+    ATTR_SS(128, 6, 1, 16)
+    if (!launched) return hipErrorInvalidConfiguration;
 #undef ATTR_SS
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -169,7 +169,11 @@ def test_gpt2_store_scan():
                                           (17, 70000, 64, 128, np.float16),
                                           (50, 30000, 256, 32, np.float16),
                                           (50, 30000, 256, 33, np.float16),
-                                          (9, 30000, 64, 64, np.float32)])
+                                          (9, 30000, 64, 64, np.float32),
+                                          (12, 50000, 128, 100, np.float16),
+                                          (16, 20000, 256, 65, np.float16),
+                                          (32, 30000, 128, 128, np.float16),
+                                          (20, 30000, 64, 128, np.float32)])
 def test_streaming_plan(nq, ng, D, k, dt):
     """Shapes large enough for the streaming (LDS-ring) plan: ragged query
     blocks, ragged partitions and tiles, duplicate rows, fp32 and fp16."""
