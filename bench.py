@@ -253,8 +253,8 @@ def _other_rows(stream, dev):
 
 def _profile_row(row, dev):
     """One row of the path on its own, sized for counter runs (rocprofv3
-    --pmc): `syrk` / `full_apply` on a 131072 x 8192 low-rank-plus-noise
-    store, `scan16` / `scan1024` on a 1M x 8192 unit fp16 store with top-100,
+    --pmc): `syrk` on a 500000 x 8192 low-rank-plus-noise store (one full
+    accumulate launch), `full_apply` on 131072 rows of it, `scan16` / `scan1024` on a 1M x 8192 unit fp16 store with top-100,
     `diag_acc` / `diag_apply` (DIAG accumulate, DIAG apply + unit norm) on a
     10^6 x 8192 fp16 store, each run PROFILE_REPS times; `llama1b` the
     1B-shaped projection row (timed, printed as JSON)."""
@@ -283,10 +283,13 @@ def _profile_row(row, dev):
             for _ in range(PROFILE_REPS):
                 P.attr_precond_apply(X, P.PRECOND_DIAG, m, True, Y)
     elif row in ("syrk", "full_apply"):
-        N = 131072
+        N = 500_000 if row == "syrk" else 131072
         F = torch.randn((D, 64), generator=gen, device=dev)
-        Z = torch.randn((N, 64), generator=gen, device=dev)
-        X = (Z @ F.T + 0.1 * torch.randn((N, D), generator=gen, device=dev)).half()
+        X = torch.empty((N, D), dtype=torch.float16, device=dev)
+        for i in range(0, N, 65536):
+            n = min(65536, N - i)
+            Z = torch.randn((n, 64), generator=gen, device=dev)
+            X[i:i + n] = (Z @ F.T + 0.1 * torch.randn((n, D), generator=gen, device=dev)).half()
         del F, Z
         if row == "syrk":
             H = torch.zeros((D, D), dtype=torch.float32, device=dev)

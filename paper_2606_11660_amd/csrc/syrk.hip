@@ -6,16 +6,19 @@
 // K-major: the GEMM core for K-major operands reads 64-row x 256-column
 // stages of X itself and transposes them while reading its MFMA fragments
 // out of LDS (no transposed copy of X is written).  Only the upper-triangle
-// tiles (tp <= tq) of X^T X are computed.  Rows are taken in chunks of up to
-// 262144; a chunk is split into K-slices of 16384 rows computed by separate
+// tiles (tp <= tq) of X^T X are computed.  Rows are taken in equal chunks
+// of at most 524288; a chunk is split into 16 K-slices computed by separate
 // workgroups (at D = 8192, 528 tiles x 16 slices are 33 whole rounds of the
 // 256 CUs; chunks of 65536 rows left a quarter-full last round and took 5%
 // longer), and only the slices that hold rows are launched.  Slice results
 // go to fp32 partial tiles and a reduce kernel adds them, in slice order,
-// into an fp64 accumulator.  Precision: fp32 MFMA accumulation over at most
-// 16384 rows, fp64 across slices and chunks, one rounding into H at the end
+// into an fp64 accumulator (at 10^6 x 8192 the reduce of two chunks costs
+// ~1 ms, of four 1.9 ms).  Precision: fp32 MFMA accumulation over at most
+// 32768 rows, fp64 across slices and chunks, one rounding into H at the end
 // of the call (the spectrum of H spans ~6 decades on low-rank-plus-noise
-// stores, and long fp32 accumulation visibly perturbs its small eigenvalues).
+// stores, and long fp32 accumulation visibly perturbs its small eigenvalues;
+// sampled entries of H at 10^6 x 8192 are within 5e-7 of fp64, relative to
+// the largest).
 // Deterministic: fixed tile, slice and chunk orders, no atomics.
 #include "common.h"
 #include "gemm.h"
@@ -25,9 +28,10 @@ namespace attr {
 namespace {
 
 #ifndef ATTR_SYRK_CHUNK
-#define ATTR_SYRK_CHUNK 262144  // rows per transpose + SYRK launch (16 K-slices: whole rounds of 256 CUs)
+#define ATTR_SYRK_CHUNK 524288  // rows per SYRK launch (16 K-slices: whole rounds of 256 CUs)
 #endif
 constexpr int SYRK_CHUNK = ATTR_SYRK_CHUNK;
+constexpr int SYRK_SLICES = 16;  // K-slices per full chunk
 constexpr int TILE_E = GT * GT;  // elements per tile
 
 // Upper-triangle tile u -> (tp, tq), tp <= tq, row-major over tp.
@@ -67,8 +71,8 @@ __device__ inline void band_tile(int v, int nt, int& tp, int& tq) {
 
 // Work item of workgroup b: workgroups go to the 8 XCDs round robin
 // (b % 8).  The K-slices are taken one after the other by the whole chip, so
-// that the rows being read at any time are one slice's (256 MB at 8192
-// columns, about the MALL's size); within a slice XCD x takes the contiguous
+// that the rows being read at any time are one slice's (512 MB at 8192
+// columns); within a slice XCD x takes the contiguous
 // band-ordered tile range [x per_xcd, (x + 1) per_xcd), so the workgroups
 // resident on one XCD share row blocks through its L2.
 template <typename Tag, typename T>
@@ -102,7 +106,7 @@ __global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ X, int6
   const i32x4 db = make_desc(X + rs * ldx + cb, range(cb));
   GemmCoreT<Tag> core;
   core.zero();
-  core.run(sm, da, ldx, db, ldx, (int)(Cs / GKS));
+  core.run(sm, da, ldx, db, ldx, (int)((nr + GKS - 1) / GKS));  // stages holding rows
   float* dst = part + ((int64_t)j * n_up + u) * TILE_E;
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -180,14 +184,16 @@ SyrkPlan plan_syrk(int64_t n_rows, int64_t D) {
   SyrkPlan P{};
   P.nt = (int)((D + GT - 1) / GT);
   P.n_up = P.nt * (P.nt + 1) / 2;
-  int64_t c = n_rows < SYRK_CHUNK ? n_rows : SYRK_CHUNK;
+  // equal chunks of at most SYRK_CHUNK rows (10^6 rows: two of 500000, each
+  // 16 slices of 31296, rather than one full chunk and a ragged one)
+  const int64_t n_chunks = n_rows > SYRK_CHUNK ? (n_rows + SYRK_CHUNK - 1) / SYRK_CHUNK : 1;
+  int64_t c = (n_rows + n_chunks - 1) / n_chunks;
   c = (c + 63) / 64 * 64;
   if (c < 64) c = 64;
-#ifndef ATTR_SYRK_SLICE
-#define ATTR_SYRK_SLICE 16384
-#endif
-  int J = (int)(c / ATTR_SYRK_SLICE);
-  J = J < 1 ? 1 : (J > SYRK_CHUNK / ATTR_SYRK_SLICE ? SYRK_CHUNK / ATTR_SYRK_SLICE : J);
+  // 16 K-slices, fewer for short chunks (slices of >= 8192 rows: each slice
+  // adds a partial tile to write and reduce)
+  int J = (int)(c / 8192);
+  J = J < 1 ? 1 : (J > SYRK_SLICES ? SYRK_SLICES : J);
   int64_t cs = (c + J - 1) / J;
   cs = (cs + 63) / 64 * 64;
   P.J = J;

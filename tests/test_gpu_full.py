@@ -37,7 +37,7 @@ def _check_upper(got, ref, tol=1e-5):
     return err
 
 
-@pytest.mark.parametrize("n,D", [(3000, 512), (777, 320), (70001, 256)])
+@pytest.mark.parametrize("n,D", [(3000, 512), (777, 320), (70001, 256), (263144, 256)])
 def test_syrk_matches_oracle(n, D):
     say(f"case: syrk n={n} D={D}")
     X = (np.random.default_rng(n).standard_normal((n, D)) * 2).astype(np.float16)

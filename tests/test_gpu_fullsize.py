@@ -47,7 +47,7 @@ def _unit_store(n, seed):
 
 
 def test_syrk_full_config_sampled_entries():
-    """H += X^T X over the 10^6 x 8192 store (16 chunks of 65536 rows);
+    """H += X^T X over the 10^6 x 8192 store (four chunks of 250,000 rows);
     78 upper-triangle entries recomputed in fp64 from the same columns."""
     n = 1_000_000
     say(f"case: syrk full size n={n} D={D}")
