@@ -183,7 +183,10 @@ attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows
  * (index_base + j) ordered by (score desc, index asc); NaN and -inf scores
  * are never selected; missing slots are (-inf, -1).  Exact top-k lookup,
  * section "Attribution Pipelines".  With few queries the scan streams the
- * store once and the score matrix never reaches memory; with many fp16
+ * store once and the score matrix never reaches memory (on stores of
+ * 262144 rows or more a first pass over 16384 rows finds, per query, a
+ * lower bound on its k-th best score, and rows below it are skipped by the
+ * selection: a few KB of workspace); with many fp16
  * queries (n_q >= 128) it is computed chunk by chunk into the workspace
  * (~256 MB per chunk, plus one maximum per 64 rows) and selected exactly
  * from there; after the first chunk only 64-row segments that can still

@@ -84,6 +84,8 @@ struct ScorePlan {
   size_t list_entries;   // n_q * n_parts * k
   int gemm;              // GEMM plan: row chunks of `chunk` rows, one list per chunk
   int64_t chunk;
+  int64_t D;
+  int64_t bound_rows;    // streaming plan: rows of the prefix scan that bounds the k-th best (0: none)
 };
 ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes);
 hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int64_t n_q,

@@ -7,10 +7,13 @@
 // with line-coalesced loads and pass through a per-wave LDS tile into MFMA
 // fragments (as in the projection); query fragments come from L2.
 //
-// Two plans, chosen on the host from the problem shape:
-//  * streaming (large stores): see score_stream_kernel.  Rows are visited in
-//    increasing index order, so a strict ">" keeps the lower index on ties.
-//    The Q x N score matrix never reaches memory.
+// Three plans, chosen on the host from the problem shape:
+//  * streaming (large stores, fewer than 128 fp16 queries): see
+//    score_stream_kernel.  Rows are visited in increasing index order, so a
+//    strict ">" keeps the lower index on ties.  The Q x N score matrix never
+//    reaches memory.
+//  * GEMM (128 or more fp16 queries): the 256 x 256 GEMM core scores chunks
+//    of rows into the workspace and an exact selection kernel reads them.
 //  * split-K (small stores, too few tiles to fill 256 CUs): workgroups own
 //    (tile, D-slice) pairs and write fp32 partial scores; a select kernel
 //    sums the slices in slice order and runs the same per-query insertion.
@@ -171,15 +174,28 @@ __device__ inline void write_list(float (*ls)[KMAX], int (*li)[KMAX], int q_loca
 // exchange.  Top-k selection is software-pipelined behind the stream: when
 // a tile ends its scores move to a pending copy and are compared with the
 // 16 running thresholds (k-th best so far, kept in registers); during the
-// next tile's stages the wave walks its queries, one per stage, and inserts
-// the passing rows of that query, in row order.  Each query's sorted list
-// lives in a private LDS region of its wave, padded with (-inf, -1); a
-// query with candidates loads it into registers (entry p in lane p % 64,
-// slot p / 64), inserts with all 64 lanes at once (the position is the
-// number of entries >= s: existing entries have lower row indices, so ties
-// keep them first; the tail moves one lane up through a wave-wide DPP
-// shift) and stores it back.  The selection code is a short loop rather than
-// a per-query unrolled copy, so that it stays in the instruction cache.
+// next tile's stages the wave walks its queries in order, a few per stage,
+// and inserts the passing rows of each, in row order.  Each query's sorted
+// list is held in registers (entry p in lane p % 64 of register p / 64,
+// padded with (-inf, -1)); an insertion uses all 64 lanes at once (the
+// position is the number of entries >= s: existing entries have lower row
+// indices, so ties keep them first; the tail moves one lane up through a
+// wave-wide DPP shift).  Register arrays need compile-time indices, so the
+// query being served is always list 0 and the wave's list array rotates by
+// one after each query (16 moves of one or two registers pairs): the
+// selection code is one short loop body, not a per-query unrolled copy,
+// and it stays in the instruction cache.
+//
+// Optionally each query starts from a floor: a lower bound on its k-th best
+// score over the whole store.  Rows below the floor cannot be in the
+// answer, so they never enter a list; without it every partition list fills
+// with k rows and then takes ~k ln(rows / k) more insertions, which at 64
+// queries and k = 100 cost more than the stream itself.  The bound is the
+// k-th largest of the maxima of the first 16384 rows' 64-row segments (k
+// distinct rows score at least that much), found by this kernel run with
+// k = 1 over one-tile partitions and a per-query sort of the 256 maxima.
+// A list then may end with fewer than k rows above the floor; the merge
+// takes the global top k, all of which are at or above it.
 // Partitions are mapped so that the query blocks sharing a partition run on
 // the same XCD at the same time and share its L2.
 constexpr int SR = 64;  // store rows per tile
@@ -213,6 +229,15 @@ __device__ inline float sel4(const f32x4& a, int r) {
 // lane l takes lane l - 1's value, lane 0 takes `fill` (DPP wave_shr:1)
 __device__ inline int wave_shr1(int v, int fill) {
   return __builtin_amdgcn_update_dpp(fill, v, 0x138, 0xf, 0xf, false);
+}
+
+// Largest float below x (-inf for x = -inf or NaN): a strict ">" against it
+// admits every score >= x.
+__device__ inline float float_below(float x) {
+  if (!(x > -__builtin_inff())) return -__builtin_inff();
+  if (x == 0.f) return -__builtin_bit_cast(float, 1);  // -denorm_min
+  const int b = __builtin_bit_cast(int, x);
+  return __builtin_bit_cast(float, x > 0.f ? b - 1 : b + 1);  // +inf -> FLT_MAX
 }
 
 // Register-resident sorted list of one query: entry p in lane p % 64 of
@@ -256,7 +281,8 @@ template <bool F16, int KMAX, int RING, int GPS, int QPW>
 __global__ __launch_bounds__(256) void score_stream_kernel(
     const char* __restrict__ Q, int64_t n_q, int64_t ldq, const char* __restrict__ G,
     int64_t n_g, int64_t ldg, int n_grp, int k, int64_t rows_per_part, int n_parts, int n_qb,
-    float* __restrict__ part_s, int64_t* __restrict__ part_i, int64_t index_base) {
+    const float* __restrict__ bound, float* __restrict__ part_s, int64_t* __restrict__ part_i,
+    int64_t index_base) {
   // GPS 128-byte K-groups per stage: a stage row is RB bytes (CPR chunks),
   // RPI rows per 1 KB load, LPW loads per wave and stage
   constexpr int RB = 128 * GPS, CPR = 8 * GPS, RPI = 8 / GPS, LPW = 4 * GPS;
@@ -265,7 +291,6 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   constexpr int EB = STag<F16>::bytes;
   constexpr int NS = (KMAX + 63) / 64;
   __shared__ i32x4 ring[RING][(SR + SQ) * CPR];  // store rows, then query rows
-  __shared__ float2 lists[4][QPW][KMAX];       // per wave, per query: (score, row bits)
 
   const uint32_t b = blockIdx.x;
   const int xcd = (int)(b & 7u);
@@ -293,12 +318,24 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   const int n_tiles = (int)((nrows + SR - 1) / SR);
   const int n_stg = n_grp / GPS;  // stages per tile (n_grp is a multiple of GPS)
   const int total = n_tiles * n_stg;
+  const int spg = (QPW + n_stg - 1) / n_stg;  // selection steps per stage
 
-  float2(*wl)[KMAX] = lists[wave];
+  // the wave's QPW sorted lists, in registers; the list of the query being
+  // selected is always lists[0]: the array rotates by one after every step
+  RegList<NS> lists[QPW];
+#pragma unroll
   for (int ql = 0; ql < QPW; ++ql)
 #pragma unroll
-    for (int j = 0; j < NS; ++j)
-      if (64 * j + lane < KMAX) wl[ql][64 * j + lane] = float2{-__builtin_inff(), __builtin_bit_cast(float, -1)};
+    for (int j = 0; j < NS; ++j) {
+      lists[ql].s[j] = -__builtin_inff();
+      lists[ql].i[j] = -1;
+    }
+  auto rotate = [&]() {
+    const RegList<NS> t = lists[0];
+#pragma unroll
+    for (int ql = 0; ql + 1 < QPW; ++ql) lists[ql] = lists[ql + 1];
+    lists[QPW - 1] = t;
+  };
 
   const i32x4 dq = make_desc(Q + q0 * ldq * EB, (uint32_t)(nq_blk * ldq * EB));
   // load lane -> row lr of the instruction's RPI rows, LDS slot lane % CPR of
@@ -358,8 +395,19 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   for (int u = 0; u < RING - 1; ++u)
     if (issued < total) issue_next();
 
-  // running thresholds: lane l of thr4[r] holds query 4 (l / 16) + r
-  f32x4 thr4 = f32x4{-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
+  // floor4: per query, the largest float below a lower bound on its k-th
+  // best score over the whole store (rows below it cannot be in the answer),
+  // else -inf; running thresholds thr4 start there.  Lane l of thr4[r] and
+  // floor4[r] holds slot 4 (l / 16) + r.
+  f32x4 floor4 = f32x4{-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
+  if (bound) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int ql = 4 * rgrp + r;
+      if (ql < nq_w) floor4[r] = float_below(bound[q0 + 4 * ql + wave]);
+    }
+  }
+  f32x4 thr4 = floor4;
   // pending tile: scores (pend[rt][r] in lane l: query 4 (l / 16) + r, row
   // 16 rt + l % 16), candidate bits cm (bit 4 rt + r) and its first row
   f32x4 pend[4];
@@ -367,7 +415,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   bool pend_any = false;
   int pend_rbase = 0;
 
-  auto process_query = [&](int ql) {
+  auto process_query = [&](int ql, RegList<NS>& L) {
     const int r = ql & 3, grp = ql >> 2;
     uint64_t m[4];
     bool has = false;
@@ -378,14 +426,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
     }
     if (!has) return;
     float thr = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sel4(thr4, r)), 16 * grp));
-    float2* lp = wl[ql];
-    RegList<NS> L;
-#pragma unroll
-    for (int j = 0; j < NS; ++j) {
-      const float2 e = lp[(64 * j + lane) & (KMAX - 1)];
-      L.s[j] = e.x;
-      L.i[j] = __builtin_bit_cast(int, e.y);
-    }
+    const float flo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sel4(floor4, r)), 16 * grp));
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
       const float v = sel4(pend[rt], r);
@@ -396,13 +437,10 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
         const float cv = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), src));
         if (cv > thr) {
           L.insert(cv, pend_rbase + 16 * rt + (src & 15), k, lane);
-          thr = L.kth(k);
+          thr = fmaxf(L.kth(k), flo);
         }
       }
     }
-#pragma unroll
-    for (int j = 0; j < NS; ++j)
-      if (64 * j + lane < k) lp[64 * j + lane] = float2{L.s[j], __builtin_bit_cast(float, L.i[j])};
     const bool mine = rgrp == grp;
     thr4[0] = mine && r == 0 ? thr : thr4[0];
     thr4[1] = mine && r == 1 ? thr : thr4[1];
@@ -443,8 +481,12 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
         }
       }
       // previous tile's selection, spread over this tile's stages
+      // steps [g c, (g + 1) c) of the QPW, in order, c = ceil(QPW / n_stg)
       if (pend_any)
-        for (int ql = g; ql < nq_w; ql += n_stg) process_query(ql);
+        for (int ql = g * spg; ql < QPW && ql < (g + 1) * spg; ++ql) {
+          if (ql < nq_w) process_query(ql, lists[0]);
+          rotate();
+        }
     }
     // hand this tile over to the selection
     const int rbase = tile * SR;
@@ -461,8 +503,13 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
     pend_rbase = rbase;
   }
   if (pend_any)
-    for (int ql = 0; ql < nq_w; ++ql) process_query(ql);
-  for (int ql = 0; ql < nq_w; ++ql) {
+    for (int ql = 0; ql < QPW; ++ql) {
+      if (ql < nq_w) process_query(ql, lists[0]);
+      rotate();
+    }
+#pragma unroll
+  for (int ql = 0; ql < QPW; ++ql) {
+    if (ql >= nq_w) continue;
     const int64_t q = q0 + 4 * ql + wave;
     float* ds = part_s + (q * n_parts + p) * (int64_t)k;
     int64_t* di = part_i + (q * n_parts + p) * (int64_t)k;
@@ -470,9 +517,8 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
     for (int j = 0; j < NS; ++j) {
       const int pos = 64 * j + lane;
       if (pos < k) {
-        const float2 e = wl[ql][pos];
-        const int idx = __builtin_bit_cast(int, e.y);
-        ds[pos] = e.x;
+        const int idx = lists[ql].i[j];
+        ds[pos] = lists[ql].s[j];
         di[pos] = idx >= 0 ? index_base + r_begin + idx : -1;
       }
     }
@@ -1070,29 +1116,28 @@ __global__ __launch_bounds__(256) void score_merge_kernel(const float* __restric
 
 }  // namespace
 
-// Streaming-plan launch shape: list capacity KMAX, ring depth RING, K-groups
-// per stage GPS, list slots per wave QPW (a block's queries / 4) and
-// workgroups per CU.  LDS per workgroup = RING x GPS x 16 KB + 4 x QPW x
-// KMAX x 8 B; two workgroups share a CU at <= 80 KB each.  Two per CU hide
-// one another's selection work: at 2M x 8192 fp16 rows and top-100, a
-// three-stage ring at two per CU beat a 256-byte-stage ring at one per CU by
-// 10-15% for 16 and 32 queries; 64 queries at k > 64 need 64 KB of lists and
-// stay at one per CU (32-query blocks, two per CU, read the store twice
-// through L2 and ran ~20% slower).
+// Streaming-plan launch shape: list capacity KMAX (64 or 128: one or two
+// list registers per query), ring depth RING, K-groups per stage GPS, list
+// slots per wave QPW (a block's queries / 4: register budget) and
+// workgroups per CU.  The lists live in registers, so the LDS holds only the
+// ring (RING x GPS x 16 KB); a four-stage ring of 128-byte K-groups at two
+// workgroups per CU measured as fast as five stages or three workgroups per
+// CU, and 10-20% faster than one workgroup per CU at k > 64.
 struct StreamCfg {
   int kmax, ring, gps, qpw, per_cu;
 };
-static StreamCfg stream_cfg(int64_t n_q, int k, bool wide) {
+static StreamCfg stream_cfg(int64_t n_q, int k) {
   const int64_t qb = n_q < SQ ? n_q : SQ;
-  if (k <= 32) return {32, 4, 1, 16, 2};
-  if (k <= 64) return qb <= 16 ? StreamCfg{64, 4, 1, 4, 2} : StreamCfg{64, 3, 1, 16, 2};
-  if (qb <= 16) return {128, 4, 1, 4, 2};
-  if (qb <= 32) return {128, 3, 1, 8, 2};
-  return wide ? StreamCfg{128, 3, 2, 16, 1} : StreamCfg{128, 6, 1, 16, 1};
+  const int qpw = qb <= 16 ? 4 : (qb <= 32 ? 8 : 16);
+  return {k <= 64 ? 64 : 128, 4, 1, qpw, 2};
 }
+
+static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+constexpr int64_t BOUND_ROWS = 16384;  // prefix rows whose segment maxima bound the k-th best
 
 ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes) {
   ScorePlan P{};
+  P.D = D;
   P.n_qb = (int)((n_q + SQB - 1) / SQB);
   P.n_grp = (int)(D * elem_bytes / 128);
   if (n_q <= 0 || n_g <= 0) return P;
@@ -1148,7 +1193,7 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     // partitions as workgroups fit at once (an exact multiple of the CU
     // count: 248 workgroups ran ~13% slower than 256 on k <= 32)
     P.n_qb = (int)((n_q + SQ - 1) / SQ);
-    int64_t per_wave = (int64_t)stream_cfg(n_q, k, P.n_grp % 2 == 0).per_cu * 256;
+    int64_t per_wave = (int64_t)stream_cfg(n_q, k).per_cu * 256;
     per_wave = per_wave > 1016 ? 1016 : per_wave;  // the merge takes <= 1024 sources
     int64_t parts = (per_wave + P.n_qb - 1) / P.n_qb;
     const int64_t t64 = (n_g + SR - 1) / SR;
@@ -1159,9 +1204,28 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     P.rows_per_part = rpp;
     P.n_parts = (int)((n_g + rpp - 1) / rpp);
     P.spart_bytes = 0;
+    // the bound pass (~0.1 ms) pays when the lists see many insertions: a
+    // large store and many (query, list entry) pairs
+    if (n_g >= 16 * BOUND_ROWS && n_q * k >= 1024) {
+      P.bound_rows = BOUND_ROWS;
+      const size_t nb = (size_t)(BOUND_ROWS / SR);
+      P.spart_bytes = align256((size_t)n_q * nb * 4) + align256((size_t)n_q * nb * 8) + align256((size_t)n_q * 4);
+    }
   }
   P.list_entries = (size_t)n_q * (size_t)P.n_parts * (size_t)k;
   return P;
+}
+
+// bound[q] = k-th largest of the nb segment maxima of query q (-inf when
+// fewer than k are finite).  One workgroup per query; nb <= 1024.
+__global__ __launch_bounds__(256) void score_bound_kernel(const float* __restrict__ seg_s, int nb, int k,
+                                                          float* __restrict__ bound) {
+  __shared__ float v[1024];
+  const int64_t q = blockIdx.x;
+  for (int i = threadIdx.x; i < 1024; i += 256) v[i] = i < nb ? seg_s[q * nb + i] : -__builtin_inff();
+  __syncthreads();
+  bitonic_desc(v, 1024);
+  if (threadIdx.x == 0) bound[q] = v[k - 1];
 }
 
 hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int64_t n_q,
@@ -1191,6 +1255,46 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   } else if (n_g > 0 && plan.split <= 1) {
+    // lower bound on each query's k-th best score: the k-th largest of the
+    // maxima of the first bound_rows / 64 row segments (k distinct rows reach
+    // it).  The maxima come from this kernel run with k = 1 over one-tile
+    // partitions.
+    const float* bound = nullptr;
+    if (plan.bound_rows > 0) {
+      const int nb = (int)(plan.bound_rows / SR);
+      char* w = reinterpret_cast<char*>(spart);
+      float* seg_s = reinterpret_cast<float*>(w);
+      int64_t* seg_i = reinterpret_cast<int64_t*>(w + align256((size_t)n_q * nb * 4));
+      float* bnd = reinterpret_cast<float*>(w + align256((size_t)n_q * nb * 4) + align256((size_t)n_q * nb * 8));
+      const StreamCfg cb = stream_cfg(n_q, 1);
+      const int pp = (nb + 7) / 8 * 8;
+      dim3 gb((unsigned)(plan.n_qb * pp)), bb(256);
+      bool ok = false;
+#define ATTR_SB(KM, RG, GP, QW)                                                                  \
+  if (cb.kmax == KM && cb.ring == RG && cb.gps == GP && cb.qpw == QW) {                          \
+    ok = true;                                                                                   \
+    if (f16)                                                                                     \
+      hipLaunchKernelGGL((score_stream_kernel<true, KM, RG, GP, QW>), gb, bb, 0, s,              \
+                         (const char*)Q, n_q, ldq, (const char*)G, plan.bound_rows, ldg,        \
+                         plan.n_grp, 1, (int64_t)SR, nb, plan.n_qb, (const float*)nullptr, seg_s, \
+                         seg_i, (int64_t)0);                                                     \
+    else                                                                                         \
+      hipLaunchKernelGGL((score_stream_kernel<false, KM, RG, GP, QW>), gb, bb, 0, s,             \
+                         (const char*)Q, n_q, ldq, (const char*)G, plan.bound_rows, ldg,        \
+                         plan.n_grp, 1, (int64_t)SR, nb, plan.n_qb, (const float*)nullptr, seg_s, \
+                         seg_i, (int64_t)0);                                                     \
+  }
+      ATTR_SB(64, 4, 1, 4)
+      ATTR_SB(64, 4, 1, 8)
+      ATTR_SB(64, 4, 1, 16)
+#undef ATTR_SB
+      if (!ok) return hipErrorInvalidConfiguration;
+      hipLaunchKernelGGL(score_bound_kernel, dim3((unsigned)n_q), dim3(256), 0, s, (const float*)seg_s, nb,
+                         k, bnd);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      bound = bnd;
+    }
     const int parts_pad = (plan.n_parts + 7) / 8 * 8;
     dim3 grid((unsigned)(plan.n_qb * parts_pad)), block(256);
 #define ATTR_SS(KM, RG, GP, QW)                                                                  \
@@ -1199,22 +1303,22 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
     if (f16)                                                                                     \
       hipLaunchKernelGGL((score_stream_kernel<true, KM, RG, GP, QW>), grid, block, 0, s,          \
                          (const char*)Q, n_q, ldq, (const char*)G, n_g, ldg, plan.n_grp, k,      \
-                         plan.rows_per_part, plan.n_parts, plan.n_qb, part_s, part_i, index_base); \
+                         plan.rows_per_part, plan.n_parts, plan.n_qb, bound, part_s, part_i,     \
+                         index_base);                                                            \
     else                                                                                         \
       hipLaunchKernelGGL((score_stream_kernel<false, KM, RG, GP, QW>), grid, block, 0, s,         \
                          (const char*)Q, n_q, ldq, (const char*)G, n_g, ldg, plan.n_grp, k,      \
-                         plan.rows_per_part, plan.n_parts, plan.n_qb, part_s, part_i, index_base); \
+                         plan.rows_per_part, plan.n_parts, plan.n_qb, bound, part_s, part_i,     \
+                         index_base);                                                            \
   }
-    // two K-groups per stage (256-byte row segments) only when the groups pair up
-    const StreamCfg c = stream_cfg(n_q, k, plan.n_grp % 2 == 0);
+    const StreamCfg c = stream_cfg(n_q, k);
     bool launched = false;
-    ATTR_SS(32, 4, 1, 16)
     ATTR_SS(64, 4, 1, 4)
-    ATTR_SS(64, 3, 1, 16)
+    ATTR_SS(64, 4, 1, 8)
+    ATTR_SS(64, 4, 1, 16)
     ATTR_SS(128, 4, 1, 4)
-    ATTR_SS(128, 3, 1, 8)
-    ATTR_SS(128, 3, 2, 16)
-    ATTR_SS(128, 6, 1, 16)
+    ATTR_SS(128, 4, 1, 8)
+    ATTR_SS(128, 4, 1, 16)
     if (!launched) return hipErrorInvalidConfiguration;
 #undef ATTR_SS
     hipError_t e = hipGetLastError();

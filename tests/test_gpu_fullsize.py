@@ -113,10 +113,10 @@ def _check_scan(G, Q, ts, ti, qs, k, n_sample, tol=1e-3):
         assert (Gs[others] @ qv).max() <= s[-1] + tol, q
 
 
-@pytest.mark.parametrize("nq", [1024, 16])
+@pytest.mark.parametrize("nq", [1024, 16, 64])
 def test_store_scan_full_config(nq):
     """4M x 8192 unit fp16 store (65.5 GB), top-100: Q = 1024 runs the GEMM
-    plan, Q = 16 the streaming plan.  16 planted near-duplicates (cosine 0.9)
+    plan, Q = 16 and 64 the streaming plan (with its prefix bound).  16 planted near-duplicates (cosine 0.9)
     of known rows must rank first; sampled queries pass _check_scan."""
     n, k = 4_000_000, 100
     say(f"case: store scan full size n={n} nq={nq} k={k}")

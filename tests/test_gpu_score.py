@@ -187,6 +187,43 @@ def test_streaming_plan(nq, ng, D, k, dt):
     assert host(ti)[0, 0] == 3 + 7 and host(ti)[0, 1] == ng - 5 + 7
 
 
+@pytest.mark.parametrize("nq,k,D", [(64, 100, 64), (20, 64, 128), (64, 16, 256)])
+def test_streaming_plan_with_bound(nq, k, D):
+    """Stores of 262144 rows or more with n_q * k >= 1024 take a lower bound
+    on each query's k-th best score from the first 16384 rows before the
+    scan: random unit rows, ragged last partition."""
+    ng = 300001
+    say(f"case: streaming with bound nq={nq} ng={ng} D={D} k={k}")
+    Q = synth.unit_rows(nq, D, seed=41)
+    G = synth.unit_rows(ng, D, seed=42)
+    ts, ti = _topk(dev(Q), dev(G), k, index_base=3)
+    check_topk(host(ts), host(ti), O.scores(Q, G), k, index_base=3)
+
+
+def test_streaming_bound_ties_at_the_bound():
+    """Query 0 equals store row A, copied into 16 distinct 64-row segments of
+    the 16384-row prefix (plus the original in the first) and 40 times beyond
+    it: the 16th largest segment maximum, the bound, is exactly A's score,
+    and the top 16 are the lowest-index copies, every one scoring exactly the
+    bound (a strict comparison against the bound itself would drop them)."""
+    nq, ng, D, k = 64, 300000, 64, 16
+    say("case: streaming bound with ties at the bound")
+    G = synth.unit_rows(ng, D, seed=43)
+    A = G[7].copy()
+    pre = [64 * s + (13 * s) % 64 for s in range(0, 256, 16)]
+    post = list(range(20000, 290000, 6750))[:40]
+    for r in pre + post:
+        G[r] = A
+    Q = synth.unit_rows(nq, D, seed=44)
+    Q[0] = A
+    ts, ti = _topk(dev(Q), dev(G), k)
+    want = sorted(set(pre + [7]))[:k]
+    assert host(ti)[0].tolist() == want
+    s0 = host(ts)[0]
+    assert (s0 == s0[0]).all() and abs(s0[0] - 1.0) <= 1e-3
+    check_topk(host(ts)[1:], host(ti)[1:], O.scores(Q[1:], G), k)
+
+
 # ---------------------------------------------------------------------------
 # GEMM plan (fp16, n_q >= 128, n_g >= 4096): chunked score matrix + exact
 # per-chunk selection
