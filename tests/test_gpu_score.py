@@ -200,6 +200,23 @@ def test_streaming_plan_with_bound(nq, k, D):
     check_topk(host(ts), host(ti), O.scores(Q, G), k, index_base=3)
 
 
+def test_merge_fallback_all_ties():
+    """Every store row equal and the query equal to it: all scores tie, each
+    partition list holds its first k rows, and nearly every list entry ranks
+    at or above the k-th best list head, which overflows the merge's
+    gather-and-sort buffer; the k-round arg-max fallback must still return
+    rows 0..k-1 in index order."""
+    nq, ng, D, k = 4, 40000, 64, 100
+    say("case: merge fallback, all rows tie")
+    row = synth.unit_rows(1, D, seed=45)
+    G = np.repeat(row, ng, axis=0)
+    Q = np.repeat(row, nq, axis=0)
+    ts, ti = _topk(dev(Q), dev(G), k, index_base=11)
+    assert (host(ti) == np.arange(k)[None, :] + 11).all()
+    s = host(ts)
+    assert (s == s[:, :1]).all() and np.abs(s - 1.0).max() <= 1e-3
+
+
 def test_streaming_bound_ties_at_the_bound():
     """Query 0 equals store row A, copied into 16 distinct 64-row segments of
     the 16384-row prefix (plus the original in the first) and 40 times beyond
