@@ -11,6 +11,8 @@
 #include <exception>
 #include <numeric>
 #include <string>
+#include <map>
+#include <tuple>
 #include <vector>
 
 #include "kernels.h"
@@ -55,10 +57,14 @@ bool overlap(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
 // ---------------------------------------------------------------------------
 // projection
 // ---------------------------------------------------------------------------
+struct ProjRun {
+  int ms, slot0, n_groups;  // groups of ms modules sharing a, from slot0
+};
 struct ProjLayout {
   size_t off_tab, off_pk, off_part, total;
   std::vector<int> order;       // slot -> module index
   std::vector<size_t> pk_off;   // per slot, relative to off_pk
+  std::vector<ProjRun> runs;    // one main launch each
   int n_chunks;
 };
 
@@ -66,12 +72,42 @@ ProjLayout project_layout(const attr_module* mods, int32_t n_mods, int eb, int64
                           int64_t T, int k) {
   ProjLayout L;
   const int nk = k / 16;
-  L.order.resize(n_mods);
-  std::iota(L.order.begin(), L.order.end(), 0);
-  // Largest modules first: the dispatcher then starts the longest items first.
-  std::stable_sort(L.order.begin(), L.order.end(), [&](int x, int y) {
-    return mods[x].d_in + mods[x].d_out > mods[y].d_in + mods[y].d_out;
-  });
+  // Modules that read the same input rows (same a, lda and d_in: q/k/v or
+  // gate/up of a transformer layer) form groups of up to kProjGroupMax,
+  // projected together so that a is read once.  Slots: groups by size
+  // (largest first), within a size largest work first, so the dispatcher
+  // starts the longest items first; a group's members take consecutive slots.
+  // (three members at k = 64 would need more than 256 VGPRs: two waves per
+  // SIMD no longer fit, so groups stop at two there)
+  const size_t gmax = nk >= 4 ? 2 : (size_t)attr::kProjGroupMax;
+  std::vector<std::vector<int>> groups;
+  std::map<std::tuple<const void*, int64_t, int64_t>, size_t> open;
+  for (int x = 0; x < n_mods; ++x) {
+    const auto key = std::make_tuple(mods[x].a, (int64_t)mods[x].lda, (int64_t)mods[x].d_in);
+    auto it = open.find(key);
+    if (it != open.end() && groups[it->second].size() < gmax) {
+      groups[it->second].push_back(x);
+    } else {
+      open[key] = groups.size();
+      groups.push_back({x});
+    }
+  }
+  auto cost = [&](const std::vector<int>& gm) {
+    int64_t c = mods[gm[0]].d_in;
+    for (int x : gm) c += mods[x].d_out;
+    return c;
+  };
+  std::stable_sort(groups.begin(), groups.end(),
+                   [&](const std::vector<int>& x, const std::vector<int>& y) {
+                     if (x.size() != y.size()) return x.size() > y.size();
+                     return cost(x) > cost(y);
+                   });
+  for (const auto& gm : groups) {
+    const int ms = (int)gm.size();
+    if (L.runs.empty() || L.runs.back().ms != ms) L.runs.push_back({ms, (int)L.order.size(), 0});
+    ++L.runs.back().n_groups;
+    for (int x : gm) L.order.push_back(x);
+  }
   const int CT = attr::project_chunk_tokens(nk);
   L.n_chunks = (int)((T + CT - 1) / CT);
   L.off_tab = 0;
@@ -222,9 +258,12 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
       hipError_t e = attr::launch_project_pack(bf16, nk, pa, tab, pk, s);
       if (e != hipSuccess) return device_fail(e, "attr_project pack launch");
     }
-    hipError_t e = attr::launch_project_main(bf16, nk, tab, n_mods, L.n_chunks, n_examples, T,
-                                             row_offset, length, part, s);
-    if (e != hipSuccess) return device_fail(e, "attr_project main launch");
+    hipError_t e = hipSuccess;
+    for (const ProjRun& r : L.runs) {
+      e = attr::launch_project_main(bf16, nk, r.ms, tab, r.slot0, r.n_groups, L.n_chunks,
+                                    n_examples, T, row_offset, length, part, s);
+      if (e != hipSuccess) return device_fail(e, "attr_project main launch");
+    }
     e = attr::launch_project_reduce(nk, tab, n_mods, L.n_chunks, n_examples, T, length, part, out,
                                     ldo, s);
     if (e != hipSuccess) return device_fail(e, "attr_project reduce launch");

@@ -45,8 +45,12 @@ size_t project_packed_bytes(int64_t d_in, int64_t d_out, int k, int elem_bytes);
 
 hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab* tab,
                                char* pk_base, hipStream_t s);
-hipError_t launch_project_main(bool bf16, int nk, const ProjTab* tab, int n_slots,
-                               int n_chunks, int64_t n_ex, int64_t T,
+// Modules sharing their input rows (same a, lda, d_in) are projected in
+// groups of up to kProjGroupMax consecutive slots (one read of a per group);
+// one launch per group size ms covers n_groups groups from slot0.
+constexpr int kProjGroupMax = 3;
+hipError_t launch_project_main(bool bf16, int nk, int ms, const ProjTab* tab, int slot0,
+                               int n_groups, int n_chunks, int64_t n_ex, int64_t T,
                                const int64_t* row_offset, const int32_t* length,
                                float* partial, hipStream_t s);
 hipError_t launch_project_reduce(int nk, const ProjTab* tab, int n_slots, int n_chunks,

@@ -136,10 +136,12 @@ __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTa
 // row % 8) and read back as MFMA fragments, both conflict-free.  PD groups
 // of loads are kept in flight in a register ring (the loop is unrolled by
 // PD so ring slots are compile-time registers).
-template <typename Tag, int E, int NK, int TT, int PD>
+// MS > 1: the same token rows against the projections of MS modules that
+// share them (one read of the rows, MS sets of MFMAs).
+template <typename Tag, int E, int NK, int TT, int PD, int MS>
 __device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int d,
-                                    const i32x4* __restrict__ pk, int lane,
-                                    i32x4* __restrict__ xp, f32x4 (&acc)[TT][NK]) {
+                                    const i32x4* const (&pk)[MS], int lane,
+                                    i32x4* __restrict__ xp, f32x4 (&acc)[MS][TT][NK]) {
   constexpr int KS = 4 * E;   // K elements per MFMA step (one 16-byte fragment)
   constexpr int EB = 16 / E;  // element bytes
   constexpr int KG = 2 * KS;  // K elements per group = 128 bytes per row
@@ -155,7 +157,7 @@ __device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int
 
   // Token-row loads run PD groups ahead (HBM latency); the projection
   // fragments (L2 resident) run one group ahead.
-  i32x4 abuf[PD][TT][2], bcur[2][NK], bnxt[2][NK];
+  i32x4 abuf[PD][TT][2], bcur[MS][2][NK], bnxt[MS][2][NK];
   auto issue = [&](int grp, i32x4 (&ab)[TT][2]) {
     const uint32_t off = ld_base + (uint32_t)grp * 128u;
 #pragma unroll
@@ -164,11 +166,13 @@ __device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int
       ab[tt][1] = load16_stream(rsrc, off + tt * tile_stride + half_stride);
     }
   };
-  auto issue_b = [&](int grp, i32x4 (&bb)[2][NK]) {
+  auto issue_b = [&](int grp, i32x4 (&bb)[MS][2][NK]) {
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int m = 0; m < MS; ++m)
 #pragma unroll
-      for (int ct = 0; ct < NK; ++ct) bb[s][ct] = pk[((2 * grp + s) * NK + ct) * kWave + lane];
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int ct = 0; ct < NK; ++ct) bb[m][s][ct] = pk[m][((2 * grp + s) * NK + ct) * kWave + lane];
   };
 #pragma unroll
   for (int u = 0; u < PD - 1; ++u)
@@ -192,23 +196,32 @@ __device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int
           const i32x4 f0 = xp[tt * 128 + rslot0];
           const i32x4 f1 = xp[tt * 128 + rslot1];
 #pragma unroll
-          for (int ct = 0; ct < NK; ++ct) {
-            acc[tt][ct] = mma16(Tag{}, f0, bcur[0][ct], acc[tt][ct]);
-            acc[tt][ct] = mma16(Tag{}, f1, bcur[1][ct], acc[tt][ct]);
-          }
+          for (int m = 0; m < MS; ++m)
+#pragma unroll
+            for (int ct = 0; ct < NK; ++ct) {
+              acc[m][tt][ct] = mma16(Tag{}, f0, bcur[m][0][ct], acc[m][tt][ct]);
+              acc[m][tt][ct] = mma16(Tag{}, f1, bcur[m][1][ct], acc[m][tt][ct]);
+            }
         }
 #pragma unroll
-        for (int s = 0; s < 2; ++s)
+        for (int m = 0; m < MS; ++m)
 #pragma unroll
-          for (int ct = 0; ct < NK; ++ct) bcur[s][ct] = bnxt[s][ct];
+          for (int s = 0; s < 2; ++s)
+#pragma unroll
+            for (int ct = 0; ct < NK; ++ct) bcur[m][s][ct] = bnxt[m][s][ct];
       }
     }
   }
 }
 
-template <bool BF16, int NK>
+// One workgroup per (group, token chunk, example) item.  A group is MS
+// modules (consecutive slots from slot0 + MS * group) that share their
+// input rows a: the a tiles are read once and projected through each
+// member's S; each member's own g rows follow, and each member's k x k
+// partial goes to its slot's item.
+template <bool BF16, int NK, int MS>
 __global__ __launch_bounds__(256) void project_main_kernel(
-    const ProjTab* __restrict__ tab, int n_chunks, int64_t n_ex, int64_t T,
+    const ProjTab* __restrict__ tab, int slot0, int n_chunks, int64_t n_ex, int64_t T,
     const int64_t* __restrict__ row_offset, const int32_t* __restrict__ length,
     float* __restrict__ partial) {
   using E_t = ElemT<BF16>;
@@ -228,15 +241,15 @@ __global__ __launch_bounds__(256) void project_main_kernel(
   const uint32_t i = blk % nex;
   const uint32_t rest = blk / nex;
   const int c = (int)(rest % (uint32_t)n_chunks);
-  const int s = (int)(rest / (uint32_t)n_chunks);
+  const int s0 = slot0 + MS * (int)(rest / (uint32_t)n_chunks);
 
   int64_t len = length ? (int64_t)length[i] : T;
   len = len < 0 ? 0 : (len > T ? T : len);
   const int64_t t0 = (int64_t)c * CT;
   if (t0 >= len) return;  // uniform over the workgroup
 
-  const ProjTab md = tab[s];
   __shared__ i32x4 xpose[4][TT * 128];
+  __shared__ float red[3][KK];
   // The wave index is uniform per wave; readfirstlane lets the compiler keep
   // everything derived from it (token range, buffer resources) in SGPRs.
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -244,75 +257,87 @@ __global__ __launch_bounds__(256) void project_main_kernel(
   const int64_t wt0 = t0 + (int64_t)wave * TPW;
   int64_t ntok = len - wt0;
   ntok = ntok < 0 ? 0 : (ntok > TPW ? TPW : ntok);
+  const int64_t row0 = ntok > 0 ? (row_offset ? row_offset[i] : (int64_t)i * T) + wt0 : 0;
+  i32x4* xp = &xpose[wave][0];
 
-  f32x4 P[NK][NK];
+  f32x4 At[MS][TT][NK];
 #pragma unroll
-  for (int rt = 0; rt < NK; ++rt)
+  for (int m = 0; m < MS; ++m)
 #pragma unroll
-    for (int ct = 0; ct < NK; ++ct) P[rt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+      for (int ct = 0; ct < NK; ++ct) At[m][tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (ntok > 0) {
-    const int64_t row0 = (row_offset ? row_offset[i] : (int64_t)i * T) + wt0;
-    const char* a_ptr = (const char*)md.a + row0 * md.lda * EB;
-    const char* g_ptr = (const char*)md.g + row0 * md.ldg * EB;
-    const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_ptr, (uint32_t)(ntok * md.lda * EB));
-    const __amdgpu_buffer_rsrc_t rg = make_rsrc(g_ptr, (uint32_t)(ntok * md.ldg * EB));
-    const i32x4* pkS = (const i32x4*)md.pk;
-    const i32x4* pkR = pkS + (size_t)(md.d_in / KS) * NK * kWave;
+    const ProjTab m0 = tab[s0];
+    const char* a_ptr = (const char*)m0.a + row0 * m0.lda * EB;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(a_ptr, (uint32_t)(ntok * m0.lda * EB));
+    const i32x4* pkS[MS];
+#pragma unroll
+    for (int m = 0; m < MS; ++m) pkS[m] = (const i32x4*)tab[s0 + m].pk;
+    project_side<Tag, E, NK, TT, Tiles<NK>::PD, MS>(ra, m0.lda, m0.d_in, pkS, lane, xp, At);
+  }
 
-    f32x4 At[TT][NK], Gt[TT][NK];
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt)
+  for (int m = 0; m < MS; ++m) {
+    f32x4 P[NK][NK];
 #pragma unroll
-      for (int ct = 0; ct < NK; ++ct) {
-        At[tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-        Gt[tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-    i32x4* xp = &xpose[wave][0];
-    project_side<Tag, E, NK, TT, Tiles<NK>::PD>(ra, md.lda, md.d_in, pkS, lane, xp, At);
-    project_side<Tag, E, NK, TT, Tiles<NK>::PD>(rg, md.ldg, md.d_out, pkR, lane, xp, Gt);
+    for (int rt = 0; rt < NK; ++rt)
+#pragma unroll
+      for (int ct = 0; ct < NK; ++ct) P[rt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (ntok > 0) {
+      const ProjTab md = tab[s0 + m];
+      const char* g_ptr = (const char*)md.g + row0 * md.ldg * EB;
+      const __amdgpu_buffer_rsrc_t rg = make_rsrc(g_ptr, (uint32_t)(ntok * md.ldg * EB));
+      const i32x4* pkR[1] = {(const i32x4*)md.pk + (size_t)(md.d_in / KS) * NK * kWave};
+      f32x4 Gt[1][TT][NK];
+#pragma unroll
+      for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+        for (int ct = 0; ct < NK; ++ct) Gt[0][tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+      project_side<Tag, E, NK, TT, Tiles<NK>::PD, 1>(rg, md.ldg, md.d_out, pkR, lane, xp, Gt);
 
-    // P[r][c] += sum_tokens Gt[token][r] * At[token][c]; register q of the
-    // stage-1 tiles holds token 4 * (lane / 16) + q, column lane % 16.
+      // P[r][c] += sum_tokens Gt[token][r] * At[token][c]; register q of the
+      // stage-1 tiles holds token 4 * (lane / 16) + q, column lane % 16.
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt)
+      for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+        for (int rt = 0; rt < NK; ++rt)
+#pragma unroll
+          for (int ct = 0; ct < NK; ++ct)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              P[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(Gt[0][tt][rt][q], At[m][tt][ct][q],
+                                                               P[rt][ct], 0, 0, 0);
+    }
+
+    // Fixed-order reduction of the four wave partials: waves 1..3 park their
+    // tiles in LDS, wave 0 adds them in wave order and writes the item.
+    if (m > 0) __syncthreads();  // wave 0 has read the previous member's tiles
+    if (wave > 0) {
 #pragma unroll
       for (int rt = 0; rt < NK; ++rt)
 #pragma unroll
         for (int ct = 0; ct < NK; ++ct)
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            P[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(Gt[tt][rt][q], At[tt][ct][q],
-                                                             P[rt][ct], 0, 0, 0);
-  }
-
-  // Fixed-order reduction of the four wave partials: waves 1..3 park their
-  // tiles in LDS, wave 0 adds them in wave order and writes the item.
-  __shared__ float red[3][KK];
-  if (wave > 0) {
+          for (int q = 0; q < 4; ++q) red[wave - 1][((rt * NK + ct) * 4 + q) * kWave + lane] = P[rt][ct][q];
+    }
+    __syncthreads();
+    if (wave == 0) {
+      float* dst = partial + (((int64_t)(s0 + m) * n_chunks + c) * (int64_t)n_ex + i) * KK;
 #pragma unroll
-    for (int rt = 0; rt < NK; ++rt)
+      for (int rt = 0; rt < NK; ++rt)
 #pragma unroll
-      for (int ct = 0; ct < NK; ++ct)
+        for (int ct = 0; ct < NK; ++ct)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) red[wave - 1][((rt * NK + ct) * 4 + q) * kWave + lane] = P[rt][ct][q];
-  }
-  __syncthreads();
-  if (wave == 0) {
-    float* dst = partial + (int64_t)blk * KK;
-#pragma unroll
-    for (int rt = 0; rt < NK; ++rt)
-#pragma unroll
-      for (int ct = 0; ct < NK; ++ct)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int e = ((rt * NK + ct) * 4 + q) * kWave + lane;
-          float v = P[rt][ct][q];
-          v += red[0][e];
-          v += red[1][e];
-          v += red[2][e];
-          dst[e] = v;
-        }
+          for (int q = 0; q < 4; ++q) {
+            const int e = ((rt * NK + ct) * 4 + q) * kWave + lane;
+            float v = P[rt][ct][q];
+            v += red[0][e];
+            v += red[1][e];
+            v += red[2][e];
+            dst[e] = v;
+          }
+    }
   }
 }
 
@@ -375,24 +400,31 @@ hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab*
   return hipGetLastError();
 }
 
-hipError_t launch_project_main(bool bf16, int nk, const ProjTab* tab, int n_slots,
-                               int n_chunks, int64_t n_ex, int64_t T,
+hipError_t launch_project_main(bool bf16, int nk, int ms, const ProjTab* tab, int slot0,
+                               int n_groups, int n_chunks, int64_t n_ex, int64_t T,
                                const int64_t* row_offset, const int32_t* length,
                                float* partial, hipStream_t s) {
-  const int64_t nblk = (int64_t)n_slots * n_chunks * n_ex;
+  const int64_t nblk = (int64_t)n_groups * n_chunks * n_ex;
+  if (nblk == 0) return hipSuccess;
   dim3 grid((unsigned)nblk), block(256);
-#define ATTR_MAIN(B, N)                                                                    \
-  hipLaunchKernelGGL((project_main_kernel<B, N>), grid, block, 0, s, tab, n_chunks, n_ex, T, \
-                     row_offset, length, partial)
+#define ATTR_MAIN(B, N, M)                                                                      \
+  hipLaunchKernelGGL((project_main_kernel<B, N, M>), grid, block, 0, s, tab, slot0, n_chunks, n_ex, \
+                     T, row_offset, length, partial)
+#define ATTR_MAIN_MS(B, N)               \
+  if (ms == 1) ATTR_MAIN(B, N, 1);       \
+  else if (ms == 2) ATTR_MAIN(B, N, 2);  \
+  else ATTR_MAIN(B, N, 3);
+  if (ms < 1 || ms > kProjGroupMax) return hipErrorInvalidValue;
   if (bf16) {
-    if (nk == 1) ATTR_MAIN(true, 1);
-    else if (nk == 2) ATTR_MAIN(true, 2);
-    else ATTR_MAIN(true, 4);
+    if (nk == 1) { ATTR_MAIN_MS(true, 1) }
+    else if (nk == 2) { ATTR_MAIN_MS(true, 2) }
+    else { ATTR_MAIN_MS(true, 4) }
   } else {
-    if (nk == 1) ATTR_MAIN(false, 1);
-    else if (nk == 2) ATTR_MAIN(false, 2);
-    else ATTR_MAIN(false, 4);
+    if (nk == 1) { ATTR_MAIN_MS(false, 1) }
+    else if (nk == 2) { ATTR_MAIN_MS(false, 2) }
+    else { ATTR_MAIN_MS(false, 4) }
   }
+#undef ATTR_MAIN_MS
 #undef ATTR_MAIN
   return hipGetLastError();
 }

@@ -97,6 +97,55 @@ def test_ragged_lengths_nan_padding(dtype, k):
     assert err.max() <= (BF16_DESIGN if dtype == "bf16" else F32_TOL)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("k", [16, 32, 64])
+def test_shared_inputs_grouped(dtype, k):
+    """Modules reading the same input rows (same a tensor, stride and width)
+    are projected in groups that read a once: three modules share one a
+    (q/k/v-like), two another (gate/up-like), four a third (a group of three,
+    or of two at k = 64, plus the rest), one is alone; the members are
+    interleaved in the module list; ragged lengths with NaN padding.  Parity
+    with the oracle per module, and bitwise equality with the same call on
+    unshared copies of every a."""
+    n, T = 5, 300
+    lengths = [1, 255, 256, 300, 77]
+    spec = [(0, 64, 192), (1, 128, 64), (2, 64, 64), (0, 64, 128), (3, 192, 64),
+            (2, 64, 128), (1, 128, 192), (0, 64, 64), (2, 64, 64), (2, 64, 192)]
+    say(f"case: shared inputs dtype={dtype} k={k}")
+    rng = np.random.default_rng(300 + k)
+    cast = synth.to_bf16_bits if dtype == "bf16" else (lambda v: v.astype(np.float32))
+
+    def padded(x):
+        for i, L in enumerate(lengths):
+            x[i * T:(i + 1) * T] = synth.nan_pad(x[i * T:(i + 1) * T], L)
+        return x
+
+    a_host = {}
+    for aid, d_in, _ in spec:
+        if aid not in a_host:
+            a_host[aid] = padded(cast(rng.standard_normal((n * T, d_in))))
+    mods_host = []
+    for aid, d_in, d_out in spec:
+        g = padded(cast(rng.standard_normal((n * T, d_out)) * 1e-2))
+        R = cast(rng.standard_normal((d_out, k)) / np.sqrt(k))
+        S = cast(rng.standard_normal((d_in, k)) / np.sqrt(k))
+        mods_host.append((a_host[aid], g, R, S))
+    a_dev = {aid: dev(a) for aid, a in a_host.items()}
+    out = torch.full((n, len(spec) * k * k), -7.0, dtype=torch.float32, device="cuda")
+    mods = [P.Module(a_dev[aid], dev(g), dev(R), dev(S), out_col=m * k * k)
+            for m, ((aid, _, _), (_, g, R, S)) in enumerate(zip(spec, mods_host))]
+    L = torch.from_numpy(np.asarray(lengths, dtype=np.int32)).cuda()
+    P.attr_project(mods, k, n, T, out, length=L)
+    torch.cuda.synchronize()
+    shared = host(out)
+    separate = _run_project(mods_host, k, n, T, length=lengths, dtype=dtype)
+    assert np.isfinite(shared).all()
+    assert np.array_equal(shared, separate)
+    err = row_rel_l2(shared, _oracle(mods_host, k, n, T, length=lengths))
+    say("max row rel-L2", err.max())
+    assert err.max() <= (BF16_DESIGN if dtype == "bf16" else F32_TOL)
+
+
 def test_untouched_columns_and_row_offset():
     n, T, k = 5, 40, 16
     say("case: row_offset packed layout, extra output columns")
