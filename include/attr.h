@@ -91,7 +91,10 @@ typedef struct {
  *
  * Token t of example i is row (row_offset ? row_offset[i] : i * T) + t of
  * both a and g.  Tokens t >= len_i are never read, so padding may hold any
- * bit pattern including NaN.
+ * bit pattern including NaN.  Modules that pass the same a pointer with the
+ * same lda and d_in (the q/k/v or gate/up projections of one layer) have
+ * their shared rows read once for up to three of them (two at k = 64); the
+ * results are the same bits as with separate copies of a.
  *
  *   mods       (host) [n_mods] module descriptors; 1 <= n_mods <= 4096
  *   in_dtype   ATTR_BF16 (bf16 MFMA, fp32 accumulate) or ATTR_F32 (fp32 MFMA)
