@@ -15,8 +15,9 @@
 //  * GEMM (128 or more fp16 queries): the 256 x 256 GEMM core scores chunks
 //    of rows into the workspace and an exact selection kernel reads them.
 //  * split-K (small stores, too few tiles to fill 256 CUs): workgroups own
-//    (tile, D-slice) pairs and write fp32 partial scores; a select kernel
-//    sums the slices in slice order and runs the same per-query insertion.
+//    (tile, D-slice) pairs and write fp32 partial scores; one workgroup per
+//    query and part of the rows sums the slices in slice order and selects
+//    by a threshold from 16-row segment maxima and a sort.
 // Either way, per-partition sorted lists are merged per query by block-wide
 // arg-max in (score desc, index asc) order, which also merges a previous
 // result when a store is scored chunk by chunk.
@@ -117,40 +118,6 @@ __device__ inline void score_tile(__amdgpu_buffer_rsrc_t rq, int64_t ldq,
           for (int qt = 0; qt < 4; ++qt) qcur[s][qt] = qnxt[s][qt];
       }
     }
-  }
-}
-
-// Sorted per-query list in LDS, owned by one lane.
-template <int KMAX>
-struct TopList {
-  float (*ls)[KMAX];
-  int (*li)[KMAX];
-  int cnt;
-  float thr;
-  __device__ inline void push(int q, int k, float s, int idx) {
-    if (!(s > thr)) return;  // NaN never enters; equal scores keep the lower index
-    int pos = cnt < k ? cnt : k - 1;
-    while (pos > 0 && ls[q][pos - 1] < s) {
-      ls[q][pos] = ls[q][pos - 1];
-      li[q][pos] = li[q][pos - 1];
-      --pos;
-    }
-    ls[q][pos] = s;
-    li[q][pos] = idx;
-    if (cnt < k) ++cnt;
-    if (cnt == k) thr = ls[q][k - 1];
-  }
-};
-
-template <int KMAX>
-__device__ inline void write_list(float (*ls)[KMAX], int (*li)[KMAX], int q_local, int64_t q,
-                                  int p, int n_parts, int k, int64_t index_base,
-                                  float* __restrict__ part_s, int64_t* __restrict__ part_i) {
-  float* ds = part_s + (q * n_parts + p) * (int64_t)k;
-  int64_t* di = part_i + (q * n_parts + p) * (int64_t)k;
-  for (int j = 0; j < k; ++j) {
-    ds[j] = ls[q_local][j];
-    di[j] = li[q_local][j] >= 0 ? index_base + li[q_local][j] : -1;
   }
 }
 
@@ -849,7 +816,8 @@ __global__ __launch_bounds__(256) void score_rselect_kernel(
 // ---------------------------------------------------------------------------
 // split-K plan
 // ---------------------------------------------------------------------------
-// Partial scores of (query block, row tile, D-slice) -> spart[slice][row][q].
+// Partial scores of (query block, row tile, D-slice) -> spart[slice][q][row]
+// (nqp = 64 n_qb query rows of n_g scores per slice).
 template <bool F16>
 __global__ __launch_bounds__(256) void score_splitk_kernel(
     const char* __restrict__ Q, int64_t n_q, int64_t ldq, const char* __restrict__ G,
@@ -890,66 +858,8 @@ __global__ __launch_bounds__(256) void score_splitk_kernel(
       for (int r = 0; r < 4; ++r) {
         const int64_t q = q0 + 16 * qt + 4 * (lane >> 4) + r;
         const int64_t row = r0 + 16 * rt + (lane & 15);
-        if (row < n_g) dst[row * nqp + q] = acc[qt][rt][r];
+        if (row < n_g) dst[q * n_g + row] = acc[qt][rt][r];
       }
-}
-
-// One workgroup per (query block, row partition).  For each chunk of 128
-// rows the 256 threads sum the slices (slice order, per element) with
-// coalesced 16-byte loads into an LDS score tile; then one lane per query
-// inserts the chunk in row order.  spart is [slice][row][nqp], nqp = 64 n_qb.
-template <int KMAX>
-__global__ __launch_bounds__(256) void score_select_kernel(const float* __restrict__ spart,
-                                                           int64_t n_q, int64_t nqp, int64_t n_g,
-                                                           int n_split, int k,
-                                                           int64_t rows_per_part, int n_parts,
-                                                           int n_qb, float* __restrict__ part_s,
-                                                           int64_t* __restrict__ part_i,
-                                                           int64_t index_base) {
-  __shared__ float ls[SQB][KMAX];
-  __shared__ int li[SQB][KMAX];
-  __shared__ float sc[SQB][SCP];
-  const int qb = (int)(blockIdx.x % (uint32_t)n_qb);
-  const int p = (int)(blockIdx.x / (uint32_t)n_qb);
-  const int t = threadIdx.x;
-  for (int e = t; e < SQB * KMAX; e += 256) {
-    ls[e / KMAX][e % KMAX] = -__builtin_inff();
-    li[e / KMAX][e % KMAX] = -1;
-  }
-  __syncthreads();
-  const int64_t q0 = (int64_t)qb * SQB;
-  int64_t nq_blk = n_q - q0;
-  nq_blk = nq_blk > SQB ? SQB : nq_blk;
-  TopList<KMAX> tl{ls, li, 0, -__builtin_inff()};
-  const int64_t r0 = (int64_t)p * rows_per_part;
-  int64_t r1 = r0 + rows_per_part;
-  r1 = r1 > n_g ? n_g : r1;
-  const int64_t plane = n_g * nqp;
-  const int qv = 4 * (t & 15);  // this thread's 4 queries
-  for (int64_t c0 = r0; c0 < r1; c0 += STN) {
-    int64_t nrow = r1 - c0;
-    nrow = nrow > STN ? STN : nrow;
-    for (int jr = t >> 4; jr < nrow; jr += 16) {
-      const f32x4* src = (const f32x4*)(spart + (c0 + jr) * nqp + q0 + qv);
-      f32x4 acc = src[0];
-      int sp = 1;
-      for (; sp + 8 <= n_split; sp += 8) {
-        f32x4 x[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] = src[(sp + u) * plane / 4];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) acc += x[u];
-      }
-      for (; sp < n_split; ++sp) acc += src[sp * plane / 4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) sc[qv + e][jr] = acc[e];
-    }
-    __syncthreads();
-    if (t < nq_blk)
-      for (int j = 0; j < (int)nrow; ++j) tl.push(t, k, sc[t][j], (int)(c0 + j));
-    __syncthreads();
-  }
-  if (t < nq_blk) write_list<KMAX>(ls, li, t, q0 + t, p, n_parts, k, index_base, part_s, part_i);
 }
 
 // ---------------------------------------------------------------------------
@@ -959,6 +869,8 @@ struct Cand {
   float s;
   int64_t i;
 };
+
+__device__ inline Cand cand_none() { return Cand{-__builtin_inff(), -1}; }
 
 __device__ inline bool better(const Cand& a, const Cand& b) {
   if (a.i < 0) return false;
@@ -997,7 +909,7 @@ __global__ __launch_bounds__(64) void score_small_select_kernel(
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     live[m] = lane + 64 * m < n_g;
-    acc[m] = live[m] ? spart[(lane + 64 * m) * nqp + q] : 0.f;
+    acc[m] = live[m] ? spart[q * n_g + lane + 64 * m] : 0.f;
   }
   int sp = 1;
   for (; sp + 8 <= n_split; sp += 8) {
@@ -1006,7 +918,7 @@ __global__ __launch_bounds__(64) void score_small_select_kernel(
     for (int m = 0; m < 4; ++m)
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        x[m][u] = live[m] ? spart[(sp + u) * plane + (lane + 64 * m) * nqp + q] : 0.f;
+        x[m][u] = live[m] ? spart[(sp + u) * plane + q * n_g + lane + 64 * m] : 0.f;
 #pragma unroll
     for (int m = 0; m < 4; ++m)
 #pragma unroll
@@ -1015,7 +927,7 @@ __global__ __launch_bounds__(64) void score_small_select_kernel(
   for (; sp < n_split; ++sp)
 #pragma unroll
     for (int m = 0; m < 4; ++m)
-      if (live[m]) acc[m] += spart[sp * plane + (lane + 64 * m) * nqp + q];
+      if (live[m]) acc[m] += spart[sp * plane + q * n_g + lane + 64 * m];
 #pragma unroll
   for (int m = 0; m < 4; ++m)  // NaN and -inf are never selected
     c[m] = live[m] && acc[m] > -__builtin_inff() ? Cand{acc[m], index_base + lane + 64 * m}
@@ -1066,6 +978,151 @@ __device__ inline void bitonic_cand(Cand* a, int n) {
       }
     }
   __syncthreads();
+}
+
+// Split-K plan with more than 256 rows (a store of fewer than 32768 rows):
+// one workgroup per (query, part of at most 8192 rows).  Pass 1 sums every
+// row's slices (slice order, 32 loads in flight per thread) into LDS and
+// keeps the best row of each 16-row segment; tau, the k-th best of those
+// maxima, is reached by k distinct rows, so the k best of the part are at
+// or above it (with fewer than k segments every row qualifies).  Pass 2
+// gathers the rows at or above tau, and the previous list when merging
+// into a single part, into LDS; a bitonic sort orders them and the first k
+// are the part's list (random stores: ~1-2 k rows): the answer itself for a
+// single part, else a partition list for the merge kernel.  Should more
+// than SPL_CAP rows qualify (massive ties) the list is built by k rounds of
+// block arg-max instead.
+constexpr int SPL_SEG = 16;
+constexpr int SPL_CAP = MERGE_CAP - 128;  // gathered rows (the previous list takes <= 128 more)
+constexpr int SPL_PART = 8192;            // rows per part: their scores stay in LDS
+constexpr int SPL_SLD = 8;                // slices loaded at once
+
+__global__ __launch_bounds__(256) void score_split_topk_kernel(
+    const float* __restrict__ spart, int64_t nqp, int64_t n_g, int n_split, int k, int merge,
+    int64_t index_base, int n_parts, float* __restrict__ part_s, int64_t* __restrict__ part_i,
+    float* top_s, int64_t* top_i) {
+  __shared__ Cand buf[MERGE_CAP];  // segment maxima, then candidates, then (fallback) the list
+  __shared__ float sc[SPL_PART];
+  __shared__ Cand wbest[4];
+  __shared__ int cnt;
+  const int64_t q = blockIdx.x / (uint32_t)n_parts;
+  const int p = (int)(blockIdx.x % (uint32_t)n_parts);
+  const int t = threadIdx.x;
+  const int64_t r0 = (int64_t)p * SPL_PART;
+  int64_t nr = n_g - r0;
+  nr = nr > SPL_PART ? SPL_PART : nr;
+  const int64_t plane = n_g * nqp;
+  const float* base = spart + q * n_g + r0;
+  const int64_t ib = index_base + r0;
+  const bool direct = n_parts == 1;  // the part's list is the answer
+  const bool with_prev = direct && merge;
+  // the scores of rows j0 + 256 u (u < 4), slices summed in order per row
+  auto scores4 = [&](int64_t j0) -> f32x4 {
+    f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < n_split; sp += SPL_SLD) {
+      f32x4 x[SPL_SLD];
+#pragma unroll
+      for (int a = 0; a < SPL_SLD; ++a)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int64_t j = j0 + 256 * u;
+          x[a][u] = j < nr && sp + a < n_split ? base[(sp + a) * plane + j] : 0.f;
+        }
+#pragma unroll
+      for (int a = 0; a < SPL_SLD; ++a) v += x[a];
+    }
+    return v;
+  };
+  // NaN and -inf are never selected
+  auto cand_of = [&](float v, int64_t j) -> Cand {
+    return j < nr && v > -__builtin_inff() ? Cand{v, ib + j} : cand_none();
+  };
+  const int n_seg = (int)((nr + SPL_SEG - 1) / SPL_SEG);  // <= SPL_PART / SPL_SEG
+  for (int64_t jb = 0; jb < nr; jb += 1024) {
+    const f32x4 v = scores4(jb + t);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t j = jb + 256 * u + t;
+      if (j < nr) sc[j] = v[u];
+      Cand c = cand_of(v[u], j);
+#pragma unroll
+      for (int off = 8; off >= 1; off >>= 1) {
+        Cand o;
+        o.s = __shfl_xor(c.s, off, kWave);
+        o.i = __shfl_xor(c.i, off, kWave);
+        if (better(o, c)) c = o;
+      }
+      const int seg = (int)((jb + 256 * u) / SPL_SEG) + t / SPL_SEG;
+      if ((t & (SPL_SEG - 1)) == 0 && seg < n_seg) buf[seg] = c;
+    }
+  }
+  int n1 = 1;
+  while (n1 < n_seg) n1 <<= 1;
+  for (int e = n_seg + t; e < n1; e += 256) buf[e] = cand_none();
+  bitonic_cand(buf, n1);
+  const Cand tau = k <= n_seg ? buf[k - 1] : cand_none();
+  __syncthreads();
+  if (t == 0) cnt = 0;
+  __syncthreads();
+  for (int64_t j = t; j < nr; j += 256) {
+    const Cand c = cand_of(sc[j], j);
+    if (c.i >= 0 && !better(tau, c)) {
+      const int pos = atomicAdd(&cnt, 1);
+      if (pos < SPL_CAP) buf[pos] = c;
+    }
+  }
+  __syncthreads();
+  int n = cnt;
+  float* os = direct ? top_s + q * k : part_s + (q * n_parts + p) * (int64_t)k;
+  int64_t* oi = direct ? top_i + q * k : part_i + (q * n_parts + p) * (int64_t)k;
+  if (n <= SPL_CAP) {
+    if (with_prev) {
+      for (int e = t; e < k; e += 256) {
+        const Cand c{top_s[q * k + e], top_i[q * k + e]};
+        buf[n + e] = c.i >= 0 ? c : cand_none();
+      }
+      n += k;
+    }
+    int n2 = 1;
+    while (n2 < n || n2 < k) n2 <<= 1;
+    for (int e = n + t; e < n2; e += 256) buf[e] = cand_none();
+    bitonic_cand(buf, n2);
+    for (int j = t; j < k; j += 256) {
+      const Cand c = buf[j];
+      os[j] = c.i >= 0 ? c.s : -__builtin_inff();
+      oi[j] = c.i >= 0 ? c.i : -1;
+    }
+    return;
+  }
+  // fallback: round r takes the best candidate strictly after round r - 1's
+  Cand last = cand_none();
+  for (int r = 0; r < k; ++r) {
+    Cand tb = cand_none();
+    for (int64_t j = t; j < nr; j += 256) {
+      const Cand c = cand_of(sc[j], j);
+      if (c.i >= 0 && (r == 0 || better(last, c)) && better(c, tb)) tb = c;
+    }
+    if (with_prev)
+      for (int e = t; e < k; e += 256) {
+        const Cand c{top_s[q * k + e], top_i[q * k + e]};
+        if (c.i >= 0 && (r == 0 || better(last, c)) && better(c, tb)) tb = c;
+      }
+    const Cand wb = wave_best(tb);
+    if ((t & 63) == 0) wbest[t >> 6] = wb;
+    __syncthreads();
+    Cand best = wbest[0];
+#pragma unroll
+    for (int w = 1; w < 4; ++w)
+      if (better(wbest[w], best)) best = wbest[w];
+    if (t == 0) buf[r] = best;
+    last = best;
+    __syncthreads();
+  }
+  for (int j = t; j < k; j += 256) {
+    const Cand c = buf[j];
+    os[j] = c.i >= 0 ? c.s : -__builtin_inff();
+    oi[j] = c.i >= 0 ? c.i : -1;
+  }
 }
 
 // One workgroup per query.  Every source list is sorted, so with d =
@@ -1264,16 +1321,13 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     split = split > cap ? cap : split;
   }
   if (split >= 2) {
+    // partial slices, then one selection workgroup per query straight into
+    // the output (no partition lists): n_g < 256 x 128 rows here
     P.split = (int)split;
     P.n_tiles = (int)n_tiles;
-    // select workgroups own 16-row multiples, enough of them to spread the
-    // slice sums over the chip
-    int64_t parts = (n_g + 15) / 16;
-    parts = parts > 255 ? 255 : parts;
-    int64_t rpp = (n_g + parts - 1) / parts;
-    rpp = (rpp + 15) / 16 * 16;
-    P.rows_per_part = rpp;
-    P.n_parts = (int)((n_g + rpp - 1) / rpp);
+    P.rows_per_part = SPL_PART;
+    P.n_parts = (int)((n_g + SPL_PART - 1) / SPL_PART);
+    if (P.n_parts == 1) P.n_parts = 0;  // one part: its list is the answer (no partition lists)
     P.spart_bytes = (size_t)split * (size_t)n_g * (size_t)P.n_qb * SQB * 4;
   } else {
     P.split = 1;
@@ -1430,17 +1484,12 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
                          merge, index_base, top_s, top_i);
       return hipGetLastError();
     }
-    dim3 g2((unsigned)(plan.n_qb * plan.n_parts)), b2(256);
-    if (k <= 16)
-      hipLaunchKernelGGL(score_select_kernel<16>, g2, b2, 0, s, (const float*)spart, n_q,
-                         (int64_t)plan.n_qb * SQB, n_g, plan.split, k, plan.rows_per_part,
-                         plan.n_parts, plan.n_qb, part_s, part_i, index_base);
-    else
-      hipLaunchKernelGGL(score_select_kernel<128>, g2, b2, 0, s, (const float*)spart, n_q,
-                         (int64_t)plan.n_qb * SQB, n_g, plan.split, k, plan.rows_per_part,
-                         plan.n_parts, plan.n_qb, part_s, part_i, index_base);
+    const int np = plan.n_parts > 0 ? plan.n_parts : 1;
+    hipLaunchKernelGGL(score_split_topk_kernel, dim3((unsigned)(n_q * np)), dim3(256), 0, s,
+                       (const float*)spart, (int64_t)plan.n_qb * SQB, n_g, plan.split, k, merge,
+                       index_base, np, part_s, part_i, top_s, top_i);
     e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || np == 1) return e;
   }
   hipLaunchKernelGGL(score_merge_kernel, dim3((unsigned)n_q), dim3(256), 0, s,
                      (const float*)part_s, (const int64_t*)part_i, n_parts, k, merge, top_s, top_i);

@@ -133,6 +133,57 @@ def test_merge_small_batches_like_the_bench(k):
     assert gi[3, 0] == 5 and gi[3, 1] == 600
 
 
+@pytest.mark.parametrize("nq,ng,D,k,dt,chunk", [(70, 3001, 1024, 100, np.float16, 1000),
+                                                (20, 5000, 2048, 10, np.float32, 5000),
+                                                (64, 4096, 12288, 128, np.float16, 4096),
+                                                (5, 300, 1024, 33, np.float16, 300),
+                                                (64, 20000, 2048, 100, np.float16, 12000),
+                                                (30, 17000, 1024, 10, np.float32, 17000)])
+def test_split_plan_select(nq, ng, D, k, dt, chunk):
+    """Small stores (split-K partial slices, one selection workgroup per
+    query and part of at most 8192 rows, part lists merged when there are
+    several): ragged query blocks and row counts, a NaN row, an exact tie
+    across chunks, chunks merged into the running list."""
+    say(f"case: split plan nq={nq} ng={ng} D={D} k={k} {dt.__name__} chunk={chunk}")
+    Q = synth.unit_rows(nq, D, seed=61, dtype=dt)
+    G = synth.unit_rows(ng, D, seed=62, dtype=dt)
+    G[ng - 2] = G[7]
+    Q[1] = G[7]
+    G[ng // 2] = np.nan
+    Qd, Gd = dev(Q), dev(G)
+    ts = torch.empty((nq, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((nq, k), dtype=torch.int64, device="cuda")
+    for lo in range(0, ng, chunk):
+        P.attr_score_topk(Qd, Gd[lo:lo + chunk], k, ts, ti, index_base=lo, merge=lo > 0)
+    torch.cuda.synchronize()
+    ref = O.scores(Q, G)
+    ref[:, ng // 2] = -np.inf
+    gi = host(ti)
+    assert not (gi == ng // 2).any()
+    check_topk(host(ts), gi, ref, k)
+    assert gi[1, 0] == 7 and gi[1, 1] == ng - 2
+
+
+def test_split_plan_all_ties_fallback():
+    """Every row equal to every query: 2033 or more rows reach the k-th best
+    16-row segment maximum at k = 128, past the gather capacity, so the list
+    comes from k rounds of arg-max; merged with a second call on the same
+    rows (all ties again), the lowest indices win."""
+    nq, ng, D, k = 3, 3000, 2048, 128
+    say("case: split plan, all ties")
+    row = synth.unit_rows(1, D, seed=63)
+    Gd = dev(np.repeat(row, ng, axis=0))
+    Qd = dev(np.repeat(row, nq, axis=0))
+    ts = torch.empty((nq, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((nq, k), dtype=torch.int64, device="cuda")
+    P.attr_score_topk(Qd, Gd, k, ts, ti, index_base=5000)
+    P.attr_score_topk(Qd, Gd, k, ts, ti, index_base=10, merge=True)
+    torch.cuda.synchronize()
+    assert (host(ti) == np.arange(k)[None, :] + 10).all()
+    sc = host(ts)
+    assert (sc == sc[:, :1]).all() and np.abs(sc - 1.0).max() <= 1e-3
+
+
 def test_fewer_rows_than_k():
     say("case: n_g < k")
     Q = synth.unit_rows(5, 64, seed=17)
