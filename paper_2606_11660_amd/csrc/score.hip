@@ -125,18 +125,19 @@ __device__ inline void score_tile(__amdgpu_buffer_rsrc_t rq, int64_t ldq,
 // streaming plan (large stores)
 // ---------------------------------------------------------------------------
 // A workgroup owns 64 queries (16 per wave) and a contiguous partition of
-// store rows, walked in tiles of 64 rows.  The tile sequence is cut into
-// 128-byte K-groups ("stages"): for every stage the 64 store rows and the 64
-// query rows go straight from memory into a shared LDS ring by
+// store rows, walked in tiles of 64 TR rows (TR = 1 or 2).  The tile
+// sequence is cut into 128-byte K-groups ("stages"): for every stage the
+// tile's store rows and the 64 query rows go straight from memory into a
+// shared LDS ring by
 // direct-to-LDS buffer loads (1 KB, line-coalesced instructions that land in
 // the XOR-swizzled fragment layout), RING - 1 stages ahead.  No vector load
 // feeds a register inside the loop, so the only waits are explicit: every
-// stage costs each wave exactly 4 load instructions, the wait for stage st
-// is vmcnt <= 4 * (stages issued after st), then one barrier (all waves'
-// loads landed; all waves finished the previous stage, whose slot is then
-// refilled).
+// stage costs each wave exactly LPW = 2 (TR + 1) load instructions, the wait
+// for stage st is vmcnt <= LPW * (stages issued after st), then one barrier
+// (all waves' loads landed; all waves finished the previous stage, whose
+// slot is then refilled).
 //
-// Each wave computes its 16 queries (every fourth of the block) x 64 rows,
+// Each wave computes its 16 queries (every fourth of the block) x the tile,
 // so after a tile it holds every score of its own queries and needs no
 // exchange.  Top-k selection is software-pipelined behind the stream: when
 // a tile ends its scores move to a pending copy and are compared with the
@@ -172,15 +173,16 @@ template <int N>
 __device__ inline void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
-// n = 4 m, m in [0, 6]
-__device__ inline void wait_vmcnt_4m(int n) {
-  switch (n) {
-    case 24: wait_vmcnt<24>(); break;
-    case 20: wait_vmcnt<20>(); break;
-    case 16: wait_vmcnt<16>(); break;
-    case 12: wait_vmcnt<12>(); break;
-    case 8: wait_vmcnt<8>(); break;
-    case 4: wait_vmcnt<4>(); break;
+// vmcnt <= n for a run-time n that is a multiple of L (n <= 6 L)
+template <int L>
+__device__ inline void wait_vmcnt_m(int n) {
+  switch (n / L) {
+    case 6: wait_vmcnt<6 * L>(); break;
+    case 5: wait_vmcnt<5 * L>(); break;
+    case 4: wait_vmcnt<4 * L>(); break;
+    case 3: wait_vmcnt<3 * L>(); break;
+    case 2: wait_vmcnt<2 * L>(); break;
+    case 1: wait_vmcnt<L>(); break;
     default: wait_vmcnt<0>(); break;
   }
 }
@@ -244,20 +246,23 @@ struct RegList {
   }
 };
 
-template <bool F16, int KMAX, int RING, int GPS, int QPW>
+template <bool F16, int KMAX, int RING, int GPS, int QPW, int TR>
 __global__ __launch_bounds__(256) void score_stream_kernel(
     const char* __restrict__ Q, int64_t n_q, int64_t ldq, const char* __restrict__ G,
     int64_t n_g, int64_t ldg, int n_grp, int k, int64_t rows_per_part, int n_parts, int n_qb,
     const float* __restrict__ bound, float* __restrict__ part_s, int64_t* __restrict__ part_i,
     int64_t index_base) {
   // GPS 128-byte K-groups per stage: a stage row is RB bytes (CPR chunks),
-  // RPI rows per 1 KB load, LPW loads per wave and stage
-  constexpr int RB = 128 * GPS, CPR = 8 * GPS, RPI = 8 / GPS, LPW = 4 * GPS;
-  static_assert(RING >= 3 && LPW * (RING - 2) <= 24, "wait_vmcnt_4m range");
+  // RPI rows per 1 KB load; tiles of SRT = 64 TR store rows; LPW loads per
+  // wave and stage (16 TR store rows and 16 query rows)
+  constexpr int SRT = SR * TR;
+  constexpr int RB = 128 * GPS, CPR = 8 * GPS, RPI = 8 / GPS, LPW = 2 * GPS * (TR + 1);
+  static_assert(RING >= 3 && RING - 2 <= 6, "wait_vmcnt_m range");
+  static_assert(TR == 1 || TR == 2, "candidate bits: 4 TR row tiles x 4 queries");
   using Tag = typename STag<F16>::tag;
   constexpr int EB = STag<F16>::bytes;
   constexpr int NS = (KMAX + 63) / 64;
-  __shared__ i32x4 ring[RING][(SR + SQ) * CPR];  // store rows, then query rows
+  __shared__ i32x4 ring[RING][(SRT + SQ) * CPR];  // store rows, then query rows
 
   const uint32_t b = blockIdx.x;
   const int xcd = (int)(b & 7u);
@@ -282,7 +287,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   int64_t r_end = r_begin + rows_per_part;
   r_end = r_end > n_g ? n_g : r_end;
   const int64_t nrows = r_end > r_begin ? r_end - r_begin : 0;
-  const int n_tiles = (int)((nrows + SR - 1) / SR);
+  const int n_tiles = (int)((nrows + SRT - 1) / SRT);
   const int n_stg = n_grp / GPS;  // stages per tile (n_grp is a multiple of GPS)
   const int total = n_tiles * n_stg;
   const int spg = (QPW + n_stg - 1) / n_stg;  // selection steps per stage
@@ -310,26 +315,30 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   const int lr = lane / CPR;
   const int ri = lane & 15, rgrp = lane >> 4;
   const uint32_t ring_base = (uint32_t)(uintptr_t)&ring[0][0];
-  constexpr uint32_t SLOT_BYTES = (SR + SQ) * RB;
-  // per-lane byte offsets of this wave's 16 store rows / 16 query rows in
+  constexpr uint32_t SLOT_BYTES = (SRT + SQ) * RB;
+  // per-lane byte offsets of this wave's 16 TR store rows / 16 query rows in
   // groups of RPI rows (stage 0); query slot j is block query 4 j + wave
-  uint32_t goff[2 * GPS], qoff[2 * GPS];
+  uint32_t goff[2 * GPS * TR], qoff[2 * GPS];
+#pragma unroll
+  for (int h = 0; h < 2 * GPS * TR; ++h) {
+    const int lc = (lane % CPR) ^ ((RPI * h + lr) & 7);  // LDS rows 16 TR wave + RPI h + lr
+    goff[h] = (uint32_t)((int64_t)(16 * TR * wave + RPI * h + lr) * ldg * EB + lc * 16);
+  }
 #pragma unroll
   for (int h = 0; h < 2 * GPS; ++h) {
-    const int lc = (lane % CPR) ^ ((RPI * h + lr) & 7);  // LDS rows 16 wave + RPI h + lr
-    goff[h] = (uint32_t)((int64_t)(16 * wave + RPI * h + lr) * ldg * EB + lc * 16);
+    const int lc = (lane % CPR) ^ ((RPI * h + lr) & 7);  // LDS rows SRT + 16 wave + RPI h + lr
     qoff[h] = (uint32_t)((int64_t)(4 * (RPI * h + lr) + wave) * ldq * EB + lc * 16);
   }
-  const uint32_t lds_g = ring_base + (uint32_t)(16 * wave) * RB;
-  const uint32_t lds_q = ring_base + (uint32_t)(SR + 16 * wave) * RB;
+  const uint32_t lds_g = ring_base + (uint32_t)(16 * TR * wave) * RB;
+  const uint32_t lds_q = ring_base + (uint32_t)(SRT + 16 * wave) * RB;
 
   // issue cursor: next stage to load is (it_tile, it_g) into slot islot
   int it_tile = 0, it_g = 0, issued = 0, islot = 0;
   i32x4 dt{0, 0, 0, 0};
   auto tile_desc = [&](int tile) {
-    const int64_t row0 = r_begin + (int64_t)tile * SR;
+    const int64_t row0 = r_begin + (int64_t)tile * SRT;
     int64_t nr = r_end - row0;
-    nr = nr > SR ? SR : nr;
+    nr = nr > SRT ? SRT : nr;
     dt = make_desc(G + row0 * ldg * EB, (uint32_t)(nr * ldg * EB));
   };
   auto issue_next = [&]() {
@@ -337,17 +346,13 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
     const uint32_t go = (uint32_t)it_g * RB;
     if (g_nt) {
 #pragma unroll
-      for (int h = 0; h < 2 * GPS; ++h) {
-        lds_dma16_nt(dt, goff[h] + go, lds_g + sb + 1024u * h);
-        lds_dma16(dq, qoff[h] + go, lds_q + sb + 1024u * h);
-      }
+      for (int h = 0; h < 2 * GPS * TR; ++h) lds_dma16_nt(dt, goff[h] + go, lds_g + sb + 1024u * h);
     } else {
 #pragma unroll
-      for (int h = 0; h < 2 * GPS; ++h) {
-        lds_dma16(dt, goff[h] + go, lds_g + sb + 1024u * h);
-        lds_dma16(dq, qoff[h] + go, lds_q + sb + 1024u * h);
-      }
+      for (int h = 0; h < 2 * GPS * TR; ++h) lds_dma16(dt, goff[h] + go, lds_g + sb + 1024u * h);
     }
+#pragma unroll
+    for (int h = 0; h < 2 * GPS; ++h) lds_dma16(dq, qoff[h] + go, lds_q + sb + 1024u * h);
     ++issued;
     islot = islot == RING - 1 ? 0 : islot + 1;
     if (++it_g == n_stg) {
@@ -377,17 +382,17 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
   f32x4 thr4 = floor4;
   // pending tile: scores (pend[rt][r] in lane l: query 4 (l / 16) + r, row
   // 16 rt + l % 16), candidate bits cm (bit 4 rt + r) and its first row
-  f32x4 pend[4];
+  f32x4 pend[4 * TR];
   uint32_t cm = 0;
   bool pend_any = false;
   int pend_rbase = 0;
 
   auto process_query = [&](int ql, RegList<NS>& L) {
     const int r = ql & 3, grp = ql >> 2;
-    uint64_t m[4];
+    uint64_t m[4 * TR];
     bool has = false;
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
+    for (int rt = 0; rt < 4 * TR; ++rt) {
       m[rt] = __builtin_amdgcn_ballot_w64(rgrp == grp && ((cm >> (4 * rt + r)) & 1u));
       has |= m[rt] != 0;
     }
@@ -395,7 +400,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
     float thr = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sel4(thr4, r)), 16 * grp));
     const float flo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sel4(floor4, r)), 16 * grp));
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
+    for (int rt = 0; rt < 4 * TR; ++rt) {
       const float v = sel4(pend[rt], r);
       uint64_t mm = m[rt];
       while (mm) {
@@ -417,9 +422,9 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
 
   int st = 0, cslot = 0;
   for (int tile = 0; tile < n_tiles; ++tile) {
-    f32x4 acc[4];
+    f32x4 acc[4 * TR];
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rt = 0; rt < 4 * TR; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int g = 0; g < n_stg; ++g, ++st) {
       // stage st landed: at most (loads issued after it) of this wave's
       // loads are still outstanding
@@ -427,7 +432,7 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
       if (after >= RING - 2) {
         wait_vmcnt<LPW * (RING - 2)>();
       } else {
-        wait_vmcnt_4m(LPW * after);
+        wait_vmcnt_m<LPW>(LPW * after);
       }
       // this wave's LDS reads of the previous stage are complete before
       // anyone refills that slot
@@ -438,10 +443,10 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
       cslot = cslot == RING - 1 ? 0 : cslot + 1;
 #pragma unroll
       for (int s2 = 0; s2 < 2 * GPS; ++s2) {
-        const int qrow = SR + 16 * wave + ri;
+        const int qrow = SRT + 16 * wave + ri;
         const i32x4 qf = sl[qrow * CPR + ((4 * s2 + rgrp) ^ (qrow & 7))];
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
+        for (int rt = 0; rt < 4 * TR; ++rt) {
           const int grow = 16 * rt + ri;
           const i32x4 gf = sl[grow * CPR + ((4 * s2 + rgrp) ^ (grow & 7))];
           acc[rt] = mma16(Tag{}, qf, gf, acc[rt]);
@@ -456,11 +461,11 @@ __global__ __launch_bounds__(256) void score_stream_kernel(
         }
     }
     // hand this tile over to the selection
-    const int rbase = tile * SR;
-    const int nvalid = (int)(nrows - rbase > SR ? SR : nrows - rbase);
+    const int rbase = tile * SRT;
+    const int nvalid = (int)(nrows - rbase > SRT ? SRT : nrows - rbase);
     cm = 0;
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
+    for (int rt = 0; rt < 4 * TR; ++rt) {
       pend[rt] = acc[rt];
 #pragma unroll
       for (int r = 0; r < 4; ++r)
@@ -1264,18 +1269,24 @@ __global__ __launch_bounds__(256) void score_merge_kernel(const float* __restric
 
 // Streaming-plan launch shape: list capacity KMAX (64 or 128: one or two
 // list registers per query), ring depth RING, K-groups per stage GPS, list
-// slots per wave QPW (a block's queries / 4: register budget) and
-// workgroups per CU.  The lists live in registers, so the LDS holds only the
-// ring (RING x GPS x 16 KB); a four-stage ring of 128-byte K-groups at two
-// workgroups per CU measured as fast as five stages or three workgroups per
-// CU, and 10-20% faster than one workgroup per CU at k > 64.
+// slots per wave QPW (a block's queries / 4: register budget), workgroups
+// per CU and tile height TR x 64 rows.  The lists live in registers, so the
+// LDS holds only the ring (RING x GPS x (64 TR + 64) rows x 128 B); two
+// workgroups per CU were 10-20% faster than one at k > 64, and 128-row
+// tiles (a three-stage ring of 24 KB slots) beat 64-row tiles (four 16 KB
+// slots) by 4% at 16 queries and 13% at 64 (2M x 8192 fp16: 80% of HBM
+// bandwidth at 64 queries and k <= 64).
 struct StreamCfg {
-  int kmax, ring, gps, qpw, per_cu;
+  int kmax, ring, gps, qpw, per_cu, tr;
 };
 static StreamCfg stream_cfg(int64_t n_q, int k) {
   const int64_t qb = n_q < SQ ? n_q : SQ;
   const int qpw = qb <= 16 ? 4 : (qb <= 32 ? 8 : 16);
-  return {k <= 64 ? 64 : 128, 4, 1, qpw, 2};
+  const int kmax = k <= 64 ? 64 : 128;
+  // 128-row tiles (half the query bytes per store byte through the ring)
+  // except for 16 two-register lists, which would pass 256 VGPRs
+  if (kmax == 128 && qpw == 16) return {kmax, 4, 1, qpw, 2, 1};
+  return {kmax, 3, 1, qpw, 2, 2};
 }
 
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
@@ -1339,11 +1350,12 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     int64_t per_wave = (int64_t)stream_cfg(n_q, k).per_cu * 256;
     per_wave = per_wave > 1016 ? 1016 : per_wave;  // the merge takes <= 1024 sources
     int64_t parts = (per_wave + P.n_qb - 1) / P.n_qb;
-    const int64_t t64 = (n_g + SR - 1) / SR;
+    const int64_t srt = (int64_t)SR * stream_cfg(n_q, k).tr;  // rows per tile
+    const int64_t t64 = (n_g + srt - 1) / srt;
     parts = parts > t64 ? t64 : parts;
     parts = parts > per_wave ? per_wave : (parts < 1 ? 1 : parts);
     int64_t rpp = (n_g + parts - 1) / parts;
-    rpp = (rpp + SR - 1) / SR * SR;
+    rpp = (rpp + srt - 1) / srt * srt;
     P.rows_per_part = rpp;
     P.n_parts = (int)((n_g + rpp - 1) / rpp);
     P.spart_bytes = 0;
@@ -1414,15 +1426,15 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
       dim3 gb((unsigned)(plan.n_qb * pp)), bb(256);
       bool ok = false;
 #define ATTR_SB(KM, RG, GP, QW)                                                                  \
-  if (cb.kmax == KM && cb.ring == RG && cb.gps == GP && cb.qpw == QW) {                          \
+  if (cb.qpw == QW) {                                                                          \
     ok = true;                                                                                   \
     if (f16)                                                                                     \
-      hipLaunchKernelGGL((score_stream_kernel<true, KM, RG, GP, QW>), gb, bb, 0, s,              \
+      hipLaunchKernelGGL((score_stream_kernel<true, KM, RG, GP, QW, 1>), gb, bb, 0, s,           \
                          (const char*)Q, n_q, ldq, (const char*)G, plan.bound_rows, ldg,        \
                          plan.n_grp, 1, (int64_t)SR, nb, plan.n_qb, (const float*)nullptr, seg_s, \
                          seg_i, (int64_t)0);                                                     \
     else                                                                                         \
-      hipLaunchKernelGGL((score_stream_kernel<false, KM, RG, GP, QW>), gb, bb, 0, s,             \
+      hipLaunchKernelGGL((score_stream_kernel<false, KM, RG, GP, QW, 1>), gb, bb, 0, s,          \
                          (const char*)Q, n_q, ldq, (const char*)G, plan.bound_rows, ldg,        \
                          plan.n_grp, 1, (int64_t)SR, nb, plan.n_qb, (const float*)nullptr, seg_s, \
                          seg_i, (int64_t)0);                                                     \
@@ -1440,28 +1452,28 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
     }
     const int parts_pad = (plan.n_parts + 7) / 8 * 8;
     dim3 grid((unsigned)(plan.n_qb * parts_pad)), block(256);
-#define ATTR_SS(KM, RG, GP, QW)                                                                  \
-  if (c.kmax == KM && c.ring == RG && c.gps == GP && c.qpw == QW) {                              \
+#define ATTR_SS(KM, RG, GP, QW, TRR)                                                             \
+  if (c.kmax == KM && c.ring == RG && c.gps == GP && c.qpw == QW && c.tr == TRR) {               \
     launched = true;                                                                             \
     if (f16)                                                                                     \
-      hipLaunchKernelGGL((score_stream_kernel<true, KM, RG, GP, QW>), grid, block, 0, s,          \
+      hipLaunchKernelGGL((score_stream_kernel<true, KM, RG, GP, QW, TRR>), grid, block, 0, s,     \
                          (const char*)Q, n_q, ldq, (const char*)G, n_g, ldg, plan.n_grp, k,      \
                          plan.rows_per_part, plan.n_parts, plan.n_qb, bound, part_s, part_i,     \
                          index_base);                                                            \
     else                                                                                         \
-      hipLaunchKernelGGL((score_stream_kernel<false, KM, RG, GP, QW>), grid, block, 0, s,         \
+      hipLaunchKernelGGL((score_stream_kernel<false, KM, RG, GP, QW, TRR>), grid, block, 0, s,    \
                          (const char*)Q, n_q, ldq, (const char*)G, n_g, ldg, plan.n_grp, k,      \
                          plan.rows_per_part, plan.n_parts, plan.n_qb, bound, part_s, part_i,     \
                          index_base);                                                            \
   }
     const StreamCfg c = stream_cfg(n_q, k);
     bool launched = false;
-    ATTR_SS(64, 4, 1, 4)
-    ATTR_SS(64, 4, 1, 8)
-    ATTR_SS(64, 4, 1, 16)
-    ATTR_SS(128, 4, 1, 4)
-    ATTR_SS(128, 4, 1, 8)
-    ATTR_SS(128, 4, 1, 16)
+    ATTR_SS(64, 3, 1, 4, 2)
+    ATTR_SS(64, 3, 1, 8, 2)
+    ATTR_SS(64, 3, 1, 16, 2)
+    ATTR_SS(128, 3, 1, 4, 2)
+    ATTR_SS(128, 3, 1, 8, 2)
+    ATTR_SS(128, 4, 1, 16, 1)
     if (!launched) return hipErrorInvalidConfiguration;
 #undef ATTR_SS
     hipError_t e = hipGetLastError();
