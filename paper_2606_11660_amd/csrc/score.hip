@@ -246,8 +246,11 @@ struct RegList {
   }
 };
 
+// At least two waves per SIMD (two workgroups per CU): the compiler keeps
+// every configuration within 256 VGPRs (64 queries with two-register lists
+// and 128-row tiles would otherwise take 268 and run one workgroup per CU).
 template <bool F16, int KMAX, int RING, int GPS, int QPW, int TR>
-__global__ __launch_bounds__(256) void score_stream_kernel(
+__global__ __launch_bounds__(256, 2) void score_stream_kernel(
     const char* __restrict__ Q, int64_t n_q, int64_t ldq, const char* __restrict__ G,
     int64_t n_g, int64_t ldg, int n_grp, int k, int64_t rows_per_part, int n_parts, int n_qb,
     const float* __restrict__ bound, float* __restrict__ part_s, int64_t* __restrict__ part_i,
@@ -1274,8 +1277,8 @@ __global__ __launch_bounds__(256) void score_merge_kernel(const float* __restric
 // LDS holds only the ring (RING x GPS x (64 TR + 64) rows x 128 B); two
 // workgroups per CU were 10-20% faster than one at k > 64, and 128-row
 // tiles (a three-stage ring of 24 KB slots) beat 64-row tiles (four 16 KB
-// slots) by 4% at 16 queries and 13% at 64 (2M x 8192 fp16: 80% of HBM
-// bandwidth at 64 queries and k <= 64).
+// slots) by 4% at 16 queries and 13% at 64 (2M x 8192 fp16: 78-83% of HBM
+// bandwidth at 16 to 64 queries and k up to 128).
 struct StreamCfg {
   int kmax, ring, gps, qpw, per_cu, tr;
 };
@@ -1283,9 +1286,7 @@ static StreamCfg stream_cfg(int64_t n_q, int k) {
   const int64_t qb = n_q < SQ ? n_q : SQ;
   const int qpw = qb <= 16 ? 4 : (qb <= 32 ? 8 : 16);
   const int kmax = k <= 64 ? 64 : 128;
-  // 128-row tiles (half the query bytes per store byte through the ring)
-  // except for 16 two-register lists, which would pass 256 VGPRs
-  if (kmax == 128 && qpw == 16) return {kmax, 4, 1, qpw, 2, 1};
+  // 128-row tiles: half the query bytes per store byte through the ring
   return {kmax, 3, 1, qpw, 2, 2};
 }
 
@@ -1473,7 +1474,7 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
     ATTR_SS(64, 3, 1, 16, 2)
     ATTR_SS(128, 3, 1, 4, 2)
     ATTR_SS(128, 3, 1, 8, 2)
-    ATTR_SS(128, 4, 1, 16, 1)
+    ATTR_SS(128, 3, 1, 16, 2)
     if (!launched) return hipErrorInvalidConfiguration;
 #undef ATTR_SS
     hipError_t e = hipGetLastError();
