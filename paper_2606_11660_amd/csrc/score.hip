@@ -1299,6 +1299,7 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
   P.n_qb = (int)((n_q + SQB - 1) / SQB);
   P.n_grp = (int)(D * elem_bytes / 128);
   if (n_q <= 0 || n_g <= 0) return P;
+  // (the streaming plan at 128-384 queries measured 1.2-2.8x slower)
   if (elem_bytes == 2 && D % GKS == 0 && n_q >= 128 && n_g >= 4096) {
     // GEMM plan: score chunks of at most ~256 MB (MALL-resident between the
     // GEMM and the selection) and 128K rows, at most 255 chunks (the merge
