@@ -238,15 +238,16 @@ def test_streaming_plan(nq, ng, D, k, dt):
     assert host(ti)[0, 0] == 3 + 7 and host(ti)[0, 1] == ng - 5 + 7
 
 
-@pytest.mark.parametrize("nq,k,D", [(64, 100, 64), (20, 64, 128), (64, 16, 256)])
-def test_streaming_plan_with_bound(nq, k, D):
+@pytest.mark.parametrize("nq,k,D,dt", [(64, 100, 64, np.float16), (20, 64, 128, np.float16),
+                                       (64, 16, 256, np.float16), (24, 65, 64, np.float32)])
+def test_streaming_plan_with_bound(nq, k, D, dt):
     """Stores of 262144 rows or more with n_q * k >= 1024 take a lower bound
     on each query's k-th best score from the first 16384 rows before the
     scan: random unit rows, ragged last partition."""
     ng = 300001
-    say(f"case: streaming with bound nq={nq} ng={ng} D={D} k={k}")
-    Q = synth.unit_rows(nq, D, seed=41)
-    G = synth.unit_rows(ng, D, seed=42)
+    say(f"case: streaming with bound nq={nq} ng={ng} D={D} k={k} {dt.__name__}")
+    Q = synth.unit_rows(nq, D, seed=41, dtype=dt)
+    G = synth.unit_rows(ng, D, seed=42, dtype=dt)
     ts, ti = _topk(dev(Q), dev(G), k, index_base=3)
     check_topk(host(ts), host(ti), O.scores(Q, G), k, index_base=3)
 
