@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define ATTR_ABI_VERSION 1
+#define ATTR_ABI_VERSION 2
 
 typedef enum {
   ATTR_OK = 0,
@@ -79,6 +79,15 @@ typedef struct {
   int64_t lda, ldg;  /* row strides in elements, >= d_in / d_out, multiples of 8 */
   int64_t d_in, d_out;  /* multiples of 64 (bf16) or 32 (fp32); at most 65536 */
   int64_t out_col;   /* first column of this module's k*k block in `out` */
+  /* Optional optimizer-state normalisation (Figure 1 caption: Adafactor
+   * second moments): the factored second moment v_ij = v_out[i] v_in[j] /
+   * sum(v_out) of the module's weight; each per-example gradient is divided
+   * elementwise by sqrt(v) before projection (entries where v is 0 or a
+   * factor is not positive become 0; no epsilon).  Device fp32 [d_out] and
+   * [d_in], both NULL for no normalisation.  Applied by scaling the rows of
+   * R and S while they are packed, so the projection itself costs the same. */
+  const float* v_out;
+  const float* v_in;
 } attr_module;
 
 /* Double-sided projection (Figure 1 caption; Appendix B "Gradients"): for

@@ -10,7 +10,8 @@ or fp16) inputs.  Each function cites the passage of the paper it follows:
 
 * the double-sided per-module random projection of linear-layer gradients
   (Figure 1 caption; Appendix B, paragraph "Gradients"), with the compressed
-  gradient P_i = sum_t (R^T g_t)(S^T a_t)^T;
+  gradient P_i = sum_t (R^T g_t)(S^T a_t)^T, optionally of the gradient
+  normalised by a factored (Adafactor) second moment (Figure 1 caption);
 * unit normalisation ("grad-cosine", section "Attribution Pipelines" and the
   method-family table), the empirical-Fisher / autocorrelation
   preconditioner ("Flat (full) autocorrelation" in the method-family table;
@@ -31,7 +32,7 @@ import numpy as np
 
 __all__ = [
     "as_f64", "bf16_bits_to_f64", "to_f16", "project_explicit", "project",
-    "project_concat", "unit_normalize", "accumulate_diag", "accumulate_full",
+    "factored_second_moment", "project_normalized", "project_concat", "unit_normalize", "accumulate_diag", "accumulate_full",
     "finalize_diag", "finalize_full", "precond_apply", "scores",
     "score_topk", "merge_topk", "PAD_SCORE", "PAD_INDEX",
 ]
@@ -120,6 +121,45 @@ def project(a: np.ndarray, g: np.ndarray, R: np.ndarray, S: np.ndarray,
         gt = as_f64(g[i, :L[i]]) @ Rf         # len x k, R^T g_t per token
         at = as_f64(a[i, :L[i]]) @ Sf         # len x k, S^T a_t per token
         out[i] = (gt.T @ at).reshape(-1)
+    return out
+
+
+def factored_second_moment(v_out: np.ndarray, v_in: np.ndarray) -> np.ndarray:
+    """Factored (Adafactor) second-moment estimate of a d_out x d_in weight:
+    V = v_out v_in^T / sum(v_out), from its row factor v_out and column
+    factor v_in (Figure 1 caption: Adafactor second moments as a
+    normalisation option).  Non-positive factors are read as 0.  Float64."""
+    r = np.maximum(np.asarray(v_out, dtype=np.float64), 0.0)
+    c = np.maximum(np.asarray(v_in, dtype=np.float64), 0.0)
+    tot = r.sum()
+    return np.outer(r, c) / tot if tot > 0 else np.zeros((r.size, c.size))
+
+
+def project_normalized(a: np.ndarray, g: np.ndarray, R: np.ndarray, S: np.ndarray,
+                       v_out: np.ndarray, v_in: np.ndarray,
+                       length: Optional[Sequence[int]] = None) -> np.ndarray:
+    """Projection of the optimizer-normalised gradient (Figure 1 caption:
+    normalisation by Adafactor second moments, before projection; used by
+    TrackStar, section "Attribution Pipelines").
+
+    For example i: G_i = sum_{t < len_i} g_t a_t^T, then the elementwise
+    normalised gradient N_i = G_i / sqrt(V) with V the factored second moment
+    (``factored_second_moment``), 0 wherever V is 0 (reading: no epsilon),
+    then P_i = R^T N_i S, flattened as in ``project_explicit``.
+    Float64 [n, k*k].
+    """
+    n, T, _ = a.shape
+    L = _lengths(n, T, length)
+    Rf, Sf = as_f64(R), as_f64(S)
+    k = Rf.shape[1]
+    V = factored_second_moment(v_out, v_in)
+    inv = np.zeros_like(V)
+    pos = V > 0
+    inv[pos] = 1.0 / np.sqrt(V[pos])
+    out = np.zeros((n, k * k))
+    for i in range(n):
+        G = as_f64(g[i, :L[i]]).T @ as_f64(a[i, :L[i]])
+        out[i] = (Rf.T @ (G * inv) @ Sf).reshape(-1)
     return out
 
 

@@ -49,7 +49,8 @@ class AttrError(RuntimeError):
 class _CModule(ctypes.Structure):
     _fields_ = [("a", ctypes.c_void_p), ("g", ctypes.c_void_p), ("R", ctypes.c_void_p),
                 ("S", ctypes.c_void_p), ("lda", ctypes.c_int64), ("ldg", ctypes.c_int64),
-                ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64), ("out_col", ctypes.c_int64)]
+                ("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64), ("out_col", ctypes.c_int64),
+                ("v_out", ctypes.c_void_p), ("v_in", ctypes.c_void_p)]
 
 
 _lib = None
@@ -165,20 +166,32 @@ class Module:
 
     a: [..., d_in] activations, g: [..., d_out] output gradients (token rows,
     last dim contiguous); R: [d_out, k], S: [d_in, k] contiguous; out_col:
-    first column of the module's k*k block in the output row.
+    first column of the module's k*k block in the output row.  v_out [d_out]
+    and v_in [d_in] (fp32, optional, both or neither): the factored
+    (Adafactor) second moment that normalises the gradient before projection.
     """
 
     def __init__(self, a: torch.Tensor, g: torch.Tensor, R: torch.Tensor, S: torch.Tensor,
-                 out_col: int):
+                 out_col: int, v_out: Optional[torch.Tensor] = None,
+                 v_in: Optional[torch.Tensor] = None):
         self.a, self.g, self.R, self.S, self.out_col = a, g, R, S, int(out_col)
+        self.v_out, self.v_in = v_out, v_in
 
     def c(self) -> _CModule:
         _, d_in, lda = _rows(self.a)
         _, d_out, ldg = _rows(self.g)
         if not (self.R.is_contiguous() and self.S.is_contiguous()):
             raise ValueError("R and S must be contiguous")
+        vo = vi = None
+        for v, n, name in ((self.v_out, d_out, "v_out"), (self.v_in, d_in, "v_in")):
+            if v is not None and (v.dtype != torch.float32 or not v.is_contiguous() or v.numel() != n):
+                raise ValueError(f"{name} must be a contiguous fp32 vector of {n} elements")
+        if self.v_out is not None:
+            vo = self.v_out.data_ptr()
+        if self.v_in is not None:
+            vi = self.v_in.data_ptr()
         return _CModule(self.a.data_ptr(), self.g.data_ptr(), self.R.data_ptr(), self.S.data_ptr(),
-                        lda, ldg, d_in, d_out, self.out_col)
+                        lda, ldg, d_in, d_out, self.out_col, vo, vi)
 
 
 def _cmods(mods: Sequence[Module]):

@@ -161,6 +161,10 @@ attr_status project_validate(const attr_module* mods, int32_t n_mods, attr_dtype
       return fail(ATTR_ERR_ALIGNMENT, "module %d: lda/ldg must be multiples of %d elements", j, ld_mult);
     if (!aligned16(m.a) || !aligned16(m.g) || !aligned16(m.R) || !aligned16(m.S))
       return fail(ATTR_ERR_ALIGNMENT, "module %d: pointers must be 16-byte aligned", j);
+    if ((m.v_out == nullptr) != (m.v_in == nullptr))
+      return fail(ATTR_ERR_INVALID_ARG, "module %d: v_out and v_in must both be set or both NULL", j);
+    if ((reinterpret_cast<uintptr_t>(m.v_out) | reinterpret_cast<uintptr_t>(m.v_in)) & 3u)
+      return fail(ATTR_ERR_ALIGNMENT, "module %d: v_out / v_in must be 4-byte aligned", j);
     if (m.lda * 256 * eb >= (1ll << 31) || m.ldg * 256 * eb >= (1ll << 31))
       return fail(ATTR_ERR_UNSUPPORTED, "module %d: row stride too large", j);
     if (m.out_col < 0 || m.out_col + kk > ldo)
@@ -254,6 +258,8 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
         e.pk_off = (int64_t)L.pk_off[s0 + j];
         e.d_in = (int32_t)m.d_in;
         e.d_out = (int32_t)m.d_out;
+        e.v_out = m.v_out;
+        e.v_in = m.v_in;
       }
       hipError_t e = attr::launch_project_pack(bf16, nk, pa, tab, pk, s);
       if (e != hipSuccess) return device_fail(e, "attr_project pack launch");

@@ -27,6 +27,8 @@ struct PackEntry {
   const void* g;
   const void* R;
   const void* S;
+  const float* v_out;  // optional factored second moment (both or neither)
+  const float* v_in;
   int64_t lda, ldg, out_col, pk_off;
   int32_t d_in, d_out;
 };

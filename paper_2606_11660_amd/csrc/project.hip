@@ -55,6 +55,15 @@ struct Tiles {
   static constexpr int PD = ATTR_PROJ_PD;
 };
 
+// bf16 bit pattern <-> float (bf16 is the upper half of an fp32 pattern);
+// float -> bf16 rounds to nearest even, NaN stays NaN
+__device__ inline float bf16_value(uint16_t h) { return __builtin_bit_cast(float, (uint32_t)h << 16); }
+__device__ inline uint16_t bf16_rne(float x) {
+  const uint32_t b = __builtin_bit_cast(uint32_t, x);
+  if ((b & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((b >> 16) | 0x40u);
+  return (uint16_t)((b + 0x7fffu + ((b >> 16) & 1u)) >> 16);
+}
+
 // ---------------------------------------------------------------------------
 // pack: S [d_in, k] and R [d_out, k] (row-major) into MFMA B fragments.
 // Fragment (step ks, column tile ct) is 64 lanes x 16 bytes; lane
@@ -87,6 +96,33 @@ __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTa
     t.d_out = pe.d_out;
     tab[args.slot0 + j] = t;
   }
+  // Optimizer-state normalisation (factored second moment v = v_out v_in^T
+  // / sum(v_out)): G / sqrt(v) = D_out G D_in with D_out = diag(sqrt(sum /
+  // v_out)), D_in = diag(v_in^{-1/2}), so R^T (G / sqrt(v)) S = (D_out R)^T
+  // G (D_in S): R's row i and S's row j are scaled here; a factor that is
+  // not positive zeroes its row.  The sum runs in fp64 in a fixed order.
+  const bool norm = pe.v_out != nullptr;
+  double vsum = 0.0;
+  if (norm) {
+    __shared__ double red[256];
+    double acc = 0.0;
+    for (int i = threadIdx.x; i < pe.d_out; i += blockDim.x) {
+      const float x = pe.v_out[i];
+      acc += x > 0.f ? (double)x : 0.0;
+    }
+    red[threadIdx.x] = acc;
+    for (int w = 128; w >= 1; w >>= 1) {
+      __syncthreads();
+      if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    }
+    __syncthreads();
+    vsum = red[0];
+  }
+  auto row_scale = [&](int side, int row) -> float {
+    const float x = side == 0 ? pe.v_in[row] : pe.v_out[row];
+    if (!(x > 0.f)) return 0.f;
+    return (float)(side == 0 ? 1.0 / sqrt((double)x) : sqrt(vsum / (double)x));
+  };
   for (int side = 0; side < 2; ++side) {
     const int d = side == 0 ? pe.d_in : pe.d_out;
     const char* src = (const char*)(side == 0 ? pe.S : pe.R);
@@ -104,6 +140,10 @@ __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTa
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           h[e] = *(const uint16_t*)(src + ((size_t)(row0 + e) * K + col) * 2);
+        if (norm) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) h[e] = bf16_rne(bf16_value(h[e]) * row_scale(side, row0 + e));
+        }
         v.x = (int32_t)(h[0] | ((uint32_t)h[1] << 16));
         v.y = (int32_t)(h[2] | ((uint32_t)h[3] << 16));
         v.z = (int32_t)(h[4] | ((uint32_t)h[5] << 16));
@@ -113,6 +153,11 @@ __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTa
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           w[e] = *(const int32_t*)(src + ((size_t)(row0 + e) * K + col) * 4);
+        if (norm) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            w[e] = __builtin_bit_cast(int32_t, __builtin_bit_cast(float, w[e]) * row_scale(side, row0 + e));
+        }
         v.x = w[0];
         v.y = w[1];
         v.z = w[2];

@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.attr_abi_version() == 1
+    assert L.attr_abi_version() == 2
     assert L.attr_status_string(0) == b"ATTR_OK"
     assert L.attr_status_string(4) == b"ATTR_ERR_WORKSPACE"
     assert L.attr_last_error() == b""

@@ -146,6 +146,60 @@ def test_shared_inputs_grouped(dtype, k):
     assert err.max() <= (BF16_DESIGN if dtype == "bf16" else F32_TOL)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("k", [16, 64])
+def test_optimizer_state_normalisation(dtype, k):
+    """Gradients normalised by a factored (Adafactor) second moment before
+    projection, next to a module without normalisation in the same call;
+    factors include a zero and a negative entry (their rows/columns drop
+    out); ragged lengths with NaN padding.  bf16: the scaled R/S are
+    rounded to bf16 once more, so the bar is the bf16 tolerance."""
+    n, T = 4, 300
+    lengths = [1, 300, 128, 257]
+    shapes = [(64, 192), (128, 64), (64, 128)]
+    say(f"case: optimizer-state normalisation dtype={dtype} k={k}")
+    mods_host = _random_modules(shapes, n, T, k, dtype, seed=400 + k, lengths=lengths)
+    rng = np.random.default_rng(500 + k)
+    facs = []
+    for m, (d_in, d_out) in enumerate(shapes):
+        if m == 1:
+            facs.append(None)
+            continue
+        vo = rng.uniform(0.05, 3.0, d_out).astype(np.float32)
+        vi = rng.uniform(0.05, 3.0, d_in).astype(np.float32)
+        vo[3], vo[7], vi[5] = 0.0, -2.0, 0.0
+        facs.append((vo, vi))
+    out = torch.full((n, len(shapes) * k * k), -7.0, dtype=torch.float32, device="cuda")
+    mods = []
+    for m, ((a, g, R, S), f) in enumerate(zip(mods_host, facs)):
+        vo, vi = (None, None) if f is None else (dev(f[0]), dev(f[1]))
+        mods.append(P.Module(dev(a), dev(g), dev(R), dev(S), out_col=m * k * k, v_out=vo, v_in=vi))
+    P.attr_project(mods, k, n, T, out, length=torch.from_numpy(np.asarray(lengths, dtype=np.int32)).cuda())
+    torch.cuda.synchronize()
+    got = host(out)
+    blocks = []
+    for (a, g, R, S), f in zip(mods_host, facs):
+        a3, g3 = a.reshape(n, T, -1), g.reshape(n, T, -1)
+        blocks.append(O.project(a3, g3, R, S, length=lengths) if f is None else
+                      O.project_normalized(a3, g3, R, S, f[0], f[1], length=lengths))
+    ref = O.project_concat(blocks)
+    assert np.isfinite(got).all()
+    err = row_rel_l2(got, ref)
+    say("max row rel-L2", err.max())
+    assert err.max() <= (BF16_TOL if dtype == "bf16" else F32_TOL)
+
+
+def test_optimizer_state_factors_both_or_neither():
+    a = torch.zeros((4, 64), dtype=torch.float32, device="cuda")
+    g = torch.zeros((4, 64), dtype=torch.float32, device="cuda")
+    R = torch.zeros((64, 16), dtype=torch.float32, device="cuda")
+    S = torch.zeros((64, 16), dtype=torch.float32, device="cuda")
+    out = torch.zeros((1, 256), dtype=torch.float32, device="cuda")
+    m = P.Module(a, g, R, S, 0, v_out=torch.ones(64, device="cuda"), v_in=None)
+    with pytest.raises(P.AttrError):
+        P.attr_project([m], 16, 1, 4, out)
+
+
 def test_untouched_columns_and_row_offset():
     n, T, k = 5, 40, 16
     say("case: row_offset packed layout, extra output columns")

@@ -134,6 +134,58 @@ def test_projection_bilinear_additive_and_padding_invariant():
     assert np.isfinite(O.project_explicit(an, gn, R, S, length=L)).all()
 
 
+# ----------------------------------------------------------------------------
+# optimizer-state (factored second moment) normalisation before projection
+# ----------------------------------------------------------------------------
+def _small_module(seed, n=3, T=6, d_in=24, d_out=40, k=16):
+    rng = np.random.default_rng(seed)
+    a = rng.standard_normal((n, T, d_in))
+    g = rng.standard_normal((n, T, d_out))
+    R = rng.standard_normal((d_out, k))
+    S = rng.standard_normal((d_in, k))
+    return rng, a, g, R, S
+
+
+def test_normalized_uniform_factors_scale_plain_projection():
+    """v_out = alpha 1, v_in = beta 1: V = beta / d_out everywhere, so the
+    normalised projection is sqrt(d_out / beta) times the plain one."""
+    _, a, g, R, S = _small_module(31)
+    d_out = g.shape[-1]
+    Pn = O.project_normalized(a, g, R, S, np.full(d_out, 3.0), np.full(a.shape[-1], 0.25))
+    np.testing.assert_allclose(Pn, math.sqrt(d_out / 0.25) * O.project(a, g, R, S), rtol=1e-12)
+
+
+def test_normalized_matching_rank_one_moment_gives_sign_matrix():
+    """One token, g = u, a = w, and factors u^2, w^2: the normalised
+    gradient is sqrt(sum u^2) sign(u) sign(w)^T, so P = sqrt(sum u^2)
+    (R^T sign u)(S^T sign w)^T."""
+    rng, _, _, R, S = _small_module(32)
+    u = rng.standard_normal(R.shape[0])
+    w = rng.standard_normal(S.shape[0])
+    P = O.project_normalized(w[None, None, :], u[None, None, :], R, S, u ** 2, w ** 2)
+    ref = math.sqrt((u ** 2).sum()) * np.outer(R.T @ np.sign(u), S.T @ np.sign(w))
+    np.testing.assert_allclose(P[0], ref.reshape(-1), rtol=1e-10)
+
+
+def test_normalized_invariances_and_zero_factors():
+    """Scaling v_out leaves V unchanged; scaling v_in by mu scales P by
+    mu^-1/2; a zero factor makes the result independent of that gradient row
+    (output side) or column (input side)."""
+    rng, a, g, R, S = _small_module(33)
+    vo = rng.uniform(0.5, 2.0, g.shape[-1])
+    vi = rng.uniform(0.5, 2.0, a.shape[-1])
+    P = O.project_normalized(a, g, R, S, vo, vi)
+    np.testing.assert_allclose(O.project_normalized(a, g, R, S, 7.0 * vo, vi), P, rtol=1e-12)
+    np.testing.assert_allclose(O.project_normalized(a, g, R, S, vo, 4.0 * vi), P / 2.0, rtol=1e-12)
+    vo0, vi0 = vo.copy(), vi.copy()
+    vo0[5], vi0[3] = 0.0, -1.0
+    g2, a2 = g.copy(), a.copy()
+    g2[..., 5] = rng.standard_normal(g2[..., 5].shape)
+    a2[..., 3] = rng.standard_normal(a2[..., 3].shape)
+    np.testing.assert_allclose(O.project_normalized(a2, g2, R, S, vo0, vi0),
+                               O.project_normalized(a, g, R, S, vo0, vi0), rtol=1e-12, atol=1e-12)
+
+
 def test_bf16_decoding_exact():
     vals = np.array([1.0, -2.5, 3.140625, 0.0, 65280.0, 1e-2], dtype=np.float32)
     bits = synth.to_bf16_bits(vals)
