@@ -45,8 +45,9 @@ def test_version_and_status_strings(L):
     assert L.attr_last_error() == b""
 
 
-def _mod(d_in=64, d_out=64, lda=None, ldg=None, out_col=0, a=FAKE, g=FAKE, R=FAKE, S=FAKE):
-    return P._CModule(a, g, R, S, lda or d_in, ldg or d_out, d_in, d_out, out_col)
+def _mod(d_in=64, d_out=64, lda=None, ldg=None, out_col=0, a=FAKE, g=FAKE, R=FAKE, S=FAKE,
+         v_out=None, v_in=None):
+    return P._CModule(a, g, R, S, lda or d_in, ldg or d_out, d_in, d_out, out_col, v_out, v_in)
 
 
 def _project(L, mods, dtype=P.ATTR_BF16, k=16, n=4, T=32, out=FAKE, ldo=256, ws=None, wsb=0):
@@ -71,6 +72,9 @@ def test_project_validation(L):
     assert _project(L, [_mod()], T=0) == INVALID
     assert _project(L, [_mod()], out=0) == INVALID
     assert _project(L, [_mod()], ldo=100) == INVALID
+    assert _project(L, [_mod(v_out=FAKE)]) == INVALID                # normalisation factors: both or neither
+    assert _project(L, [_mod(v_in=FAKE)]) == INVALID
+    assert _project(L, [_mod(v_out=FAKE + 2, v_in=FAKE)]) == ALIGN
     # all arguments valid, no workspace: rejected before any launch
     assert _project(L, [_mod()], ws=None, wsb=0) == WORKSPACE
     need = L.attr_project_workspace_size((P._CModule * 1)(_mod()), 1, P.ATTR_BF16, 4, 32, 16)
