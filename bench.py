@@ -116,7 +116,8 @@ def _llama1b_projection(stream, dev):
     the valid tokens' a/g rows, R/S once and the fp32 rows.  The second
     variant points q/k/v at one input tensor and gate/up at another (the
     model's real sharing): its unique bytes are 0.870 of the first, and the
-    rate is reported over those unique bytes."""
+    rate is reported over those unique bytes.  The third adds optimizer-state
+    normalisation (factored second moments per module) to the second."""
     import numpy as np
     import torch
     import paper_2606_11660_amd as P
@@ -131,7 +132,7 @@ def _llama1b_projection(stream, dev):
     len_t = torch.from_numpy(lengths.astype(np.int32)).to(dev)
     gen = torch.Generator(device=dev)
     gen.manual_seed(1)
-    sep, shared, by_layer = [], [], {}
+    sep, shared, normed, by_layer = [], [], [], {}
     for m, md in enumerate(wl.modules):
         layer, kind = md.name.split(".")[0], md.name.split(".")[-1]
         a = torch.randn((tot, md.d_in), generator=gen, device=dev, dtype=torch.bfloat16)
@@ -143,6 +144,9 @@ def _llama1b_projection(stream, dev):
         group = {"q": "qkv", "k": "qkv", "v": "qkv", "gate": "gu", "up": "gu"}.get(kind)
         a_sh = by_layer.setdefault((layer, group), a) if group else a
         shared.append(P.Module(a_sh, g, Rt, St, m * k * k))
+        vo = torch.rand(md.d_out, generator=gen, device=dev) + 0.5
+        vi = torch.rand(md.d_in, generator=gen, device=dev) + 0.5
+        normed.append(P.Module(a_sh, g, Rt, St, m * k * k, v_out=vo, v_in=vi))
     rows = torch.empty((B, wl.D), dtype=torch.float32, device=dev)
     ws = P.Workspace(dev)
     elems = sum(md.d_in + md.d_out for md in wl.modules)
@@ -151,13 +155,14 @@ def _llama1b_projection(stream, dev):
     rs = sum((md.d_in + md.d_out) * k * 2 for md in wl.modules)
     out = {"modules": len(wl.modules), "batch": B, "valid_tokens": tot,
            "lengths": "uniform integers in [256, 2048], seed 4, first 16", "D": wl.D}
-    for name, mods, e in (("separate_inputs", sep, elems), ("shared_qkv_gateup_inputs", shared, uniq)):
+    for name, mods, e in (("separate_inputs", sep, elems), ("shared_qkv_gateup_inputs", shared, uniq),
+                          ("shared_inputs_adafactor_normalised", normed, uniq)):
         ms = _timeit(lambda: P.attr_project(mods, k, B, T, rows, row_offset=off_t, length=len_t,
                                             ws=ws, stream=stream), stream, 5)
         byts = tot * e * 2 + rs + B * wl.D * 4
         out[name] = {"ms": ms, "examples_per_s": B / (ms * 1e-3), "bytes": byts,
                      "GBps": byts / ms / 1e6, "frac_hbm": byts / ms / 1e6 / HBM_PEAK_GBPS}
-    del sep, shared, by_layer, rows
+    del sep, shared, normed, by_layer, rows
     torch.cuda.empty_cache()
     return out
 
