@@ -167,6 +167,38 @@ def _llama1b_projection(stream, dev):
     return out
 
 
+def _kfac_factors_1b_layer(stream, dev):
+    """K-FAC factors of one 1B-shaped layer over a 16-example batch's valid
+    tokens (21900, packed): A for the layer's four distinct inputs (q/k/v
+    share one, gate/up another; 3 x 2048 + 8192 wide) and Gamma for its
+    seven outputs (5 x 2048 + 2 x 8192), each a FULL accumulate on the
+    packed bf16 token rows.  Algorithmic flops N d (d + 1) per factor."""
+    import numpy as np
+    import torch
+    import paper_2606_11660_amd as P
+    import synth
+
+    lengths = synth.example_lengths(synth.LLAMA1B.n_examples)[:16]
+    tot = int(lengths.sum())
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(6)
+    widths = [2048, 2048, 2048, 8192] + [2048] * 5 + [8192, 8192]
+    rows = [torch.randn((tot, d), generator=gen, device=dev, dtype=torch.bfloat16) for d in widths]
+    Hs = {d: torch.zeros((d, d), dtype=torch.float32, device=dev) for d in set(widths)}
+    ws = P.Workspace(dev)
+
+    def run():
+        for X in rows:
+            P.attr_precond_accumulate(X, P.PRECOND_FULL, Hs[X.shape[1]], ws=ws, stream=stream)
+    ms = _timeit(run, stream, 3)
+    fl = sum(tot * d * (d + 1) for d in widths)
+    del rows, Hs
+    torch.cuda.empty_cache()
+    return {"tokens": tot, "factors": len(widths), "widths": widths, "ms": ms,
+            "TFLOPs": fl / ms / 1e9, "frac_mfma": fl / ms / 1e9 / MFMA_PEAK_TFLOPS,
+            "flops": "sum over factors of tokens*d*(d+1), upper triangles incl. diagonal"}
+
+
 def _other_rows(stream, dev):
     """Timings of the 1B-shaped projection, of the preconditioner rows on the
     10^6 x 8192 low-rank-plus-noise store and of the 4M-row store scan (Q
@@ -174,7 +206,8 @@ def _other_rows(stream, dev):
     MFMA-bound), each against its roofline."""
     import torch
     import paper_2606_11660_amd as P
-    out = {"projection_llama1b_shaped": _llama1b_projection(stream, dev)}
+    out = {"projection_llama1b_shaped": _llama1b_projection(stream, dev),
+           "kfac_factors_1b_layer": _kfac_factors_1b_layer(stream, dev)}
     N, D = 1_000_000, 8192
     gen = torch.Generator(device=dev)
     gen.manual_seed(3)
@@ -265,9 +298,10 @@ def _profile_row(row, dev):
     1B-shaped projection row (timed, printed as JSON)."""
     import torch
     import paper_2606_11660_amd as P
-    if row == "llama1b":
+    if row in ("llama1b", "kfac"):
         stream = torch.cuda.Stream(device=dev)
-        print(json.dumps({"profile_row": row, "result": _llama1b_projection(stream, dev)}))
+        fn = _llama1b_projection if row == "llama1b" else _kfac_factors_1b_layer
+        print(json.dumps({"profile_row": row, "result": fn(stream, dev)}))
         return
     D = 8192
     gen = torch.Generator(device=dev)
@@ -345,7 +379,7 @@ def main():
     ap.add_argument("--quick", action="store_true", help="skip the preconditioner / store-scan rows")
     ap.add_argument("--copy-reference", action="store_true",
                     help="only run the 1 GiB copy used to calibrate traffic counters")
-    ap.add_argument("--profile-row", choices=["syrk", "full_apply", "scan16", "scan1024", "diag_acc",
+    ap.add_argument("--profile-row", choices=["syrk", "full_apply", "scan16", "scan1024", "diag_acc", "kfac",
                                               "diag_apply", "llama1b"],
                     help="only run one row of the path once, for counter runs")
     args = ap.parse_args()

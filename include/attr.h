@@ -142,7 +142,7 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
  * Accumulation is additive across calls, so a store can be processed in
  * chunks; divide by the total row count afterwards.  Within a call, partial
  * sums are formed in fp32 (DIAG: 8-row groups; FULL: matrix-core products
- * over at most 16384 rows), combined in fp64 in a fixed order and rounded
+ * over at most 32768 rows), combined in fp64 in a fixed order and rounded
  * once into H, so results are deterministic.
  *
  *   X, ldx   device [n_rows, D] rows: DIAG takes ATTR_F16, ATTR_BF16 or

@@ -32,9 +32,9 @@ import numpy as np
 
 __all__ = [
     "as_f64", "bf16_bits_to_f64", "to_f16", "project_explicit", "project",
-    "factored_second_moment", "project_normalized", "project_concat", "unit_normalize", "accumulate_diag", "accumulate_full",
-    "finalize_diag", "finalize_full", "precond_apply", "scores",
-    "score_topk", "merge_topk", "PAD_SCORE", "PAD_INDEX",
+    "factored_second_moment", "project_normalized", "project_concat", "unit_normalize",
+    "accumulate_diag", "accumulate_full", "kfac_factors", "finalize_diag", "finalize_full",
+    "precond_apply", "scores", "score_topk", "merge_topk", "PAD_SCORE", "PAD_INDEX",
 ]
 
 PAD_SCORE = -np.inf
@@ -197,6 +197,26 @@ def accumulate_full(X: np.ndarray) -> np.ndarray:
     autocorrelation / empirical Fisher of the method-family table)."""
     X = as_f64(X)
     return X.T @ X
+
+
+def kfac_factors(a: np.ndarray, g: np.ndarray,
+                 length: Optional[Sequence[int]] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """K-FAC factors of one linear module over the valid tokens of a batch
+    (Figure 1 caption: K-FAC among the Hessian approximations; the factors
+    are the input and output-gradient second moments whose Kronecker product
+    approximates the module's Fisher): A = sum_i sum_{t < len_i} a_t a_t^T
+    (d_in x d_in) and Gamma = sum g_t g_t^T (d_out x d_out), unscaled.
+    a: [n, T, d_in], g: [n, T, d_out]; padding is never read.  Float64."""
+    n, T, _ = a.shape
+    L = _lengths(n, T, length)
+    A = np.zeros((a.shape[-1], a.shape[-1]))
+    Gm = np.zeros((g.shape[-1], g.shape[-1]))
+    for i in range(n):
+        ai = as_f64(a[i, :L[i]])
+        gi = as_f64(g[i, :L[i]])
+        A += ai.T @ ai
+        Gm += gi.T @ gi
+    return A, Gm
 
 
 def finalize_diag(h: np.ndarray, n_rows: int) -> np.ndarray:

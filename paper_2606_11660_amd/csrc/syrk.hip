@@ -191,8 +191,13 @@ SyrkPlan plan_syrk(int64_t n_rows, int64_t D) {
   c = (c + 63) / 64 * 64;
   if (c < 64) c = 64;
   // 16 K-slices, fewer for short chunks (slices of >= 8192 rows: each slice
-  // adds a partial tile to write and reduce)
+  // adds a partial tile to write and reduce), but enough for two workgroups
+  // per CU when the matrix has few tiles (D = 2048: 36 tiles), with slices
+  // of >= 1024 rows
   int J = (int)(c / 8192);
+  const int fill = (512 + P.n_up - 1) / P.n_up;
+  const int Jmax_short = (int)(c / 1024);
+  if (J < fill) J = fill < Jmax_short ? fill : Jmax_short;
   J = J < 1 ? 1 : (J > SYRK_SLICES ? SYRK_SLICES : J);
   int64_t cs = (c + J - 1) / J;
   cs = (cs + 63) / 64 * 64;

@@ -47,6 +47,32 @@ def test_syrk_matches_oracle(n, D):
     assert err <= 1e-5
 
 
+def test_kfac_factors_from_packed_token_rows():
+    """K-FAC factors (A = sum a a^T, Gamma = sum g g^T over the valid tokens)
+    of two modules of a ragged batch: each is the FULL accumulate of the
+    module's token rows packed back to back (bf16); compared with the
+    oracle's factors of the padded batch.  The 2048-wide case has few
+    upper tiles, so the accumulate splits its rows into more slices."""
+    rng = np.random.default_rng(71)
+    n, T = 4, 1200
+    lengths = [300, 17, 1200, 512]
+    mods = [(256, 512), (2048, 128)]
+    say("case: K-FAC factors from packed token rows")
+    for d_in, d_out in mods:
+        a = synth.to_bf16_bits(rng.standard_normal((n, T, d_in)))
+        g = synth.to_bf16_bits(rng.standard_normal((n, T, d_out)))
+        a_pk = np.concatenate([a[i, :lengths[i]] for i in range(n)])
+        g_pk = np.concatenate([g[i, :lengths[i]] for i in range(n)])
+        an = np.stack([synth.nan_pad(a[i], lengths[i]) for i in range(n)])
+        gn = np.stack([synth.nan_pad(g[i], lengths[i]) for i in range(n)])
+        A, Gm = O.kfac_factors(an, gn, length=lengths)
+        for X, ref in ((a_pk, A), (g_pk, Gm)):
+            Xt = torch.from_numpy(X.view(np.int16)).view(torch.bfloat16).cuda()
+            err = _check_upper(_syrk(Xt), ref)
+            say(f"d={ref.shape[0]} max rel err {err:.2e}")
+            assert err <= 1e-5
+
+
 def test_syrk_additive_bf16_and_chunks():
     say("case: syrk additive over calls, bf16")
     n, D = 5000, 384

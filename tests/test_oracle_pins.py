@@ -262,6 +262,36 @@ def test_accumulate_brute_force():
     assert np.linalg.eigvalsh(H).min() > -1e-9
 
 
+def test_kfac_factors_brute_force_and_single_token_kronecker():
+    """K-FAC factors: per-token outer products summed by brute force over the
+    valid tokens (padding ignored); and with a single token the Kronecker
+    product Gamma (x) A equals vec(G) vec(G)^T for G = g a^T, row-major vec
+    (the factorisation is exact for one rank-one gradient)."""
+    rng = np.random.default_rng(34)
+    n, T, d_in, d_out = 3, 5, 6, 4
+    a = rng.standard_normal((n, T, d_in))
+    g = rng.standard_normal((n, T, d_out))
+    L = [5, 2, 0]
+    an = np.stack([synth.nan_pad(a[i], L[i]) for i in range(n)])
+    gn = np.stack([synth.nan_pad(g[i], L[i]) for i in range(n)])
+    A, Gm = O.kfac_factors(an, gn, length=L)
+    Ab = np.zeros((d_in, d_in))
+    Gb = np.zeros((d_out, d_out))
+    for i in range(n):
+        for t in range(L[i]):
+            for p in range(d_in):
+                for q in range(d_in):
+                    Ab[p, q] += a[i, t, p] * a[i, t, q]
+            for p in range(d_out):
+                for q in range(d_out):
+                    Gb[p, q] += g[i, t, p] * g[i, t, q]
+    np.testing.assert_allclose(A, Ab, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(Gm, Gb, rtol=1e-12, atol=1e-12)
+    A1, G1 = O.kfac_factors(a[:1, :1], g[:1, :1])
+    G = np.outer(g[0, 0], a[0, 0])
+    np.testing.assert_allclose(np.kron(G1, A1), np.outer(G.reshape(-1), G.reshape(-1)), rtol=1e-12)
+
+
 def test_diag_whitening_unit_second_moment():
     # After the diagonal preconditioner every coordinate has mean square 1.
     rng = np.random.default_rng(18)
