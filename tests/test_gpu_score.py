@@ -49,6 +49,51 @@ def test_tiny_pipeline_end_to_end():
     assert np.abs(host(ts) - rs).max() <= 1e-5
 
 
+def test_on_the_fly_scoring_without_a_store():
+    """On-the-fly scoring (training gradients scored against the queries as
+    they are produced, no store kept): per batch of 16 examples, project ->
+    unit-normalise to fp16 -> score with the running top-k merged; after four
+    batches the lists match the oracle's top-k over all 64 examples."""
+    say("case: on-the-fly scoring")
+    rng = np.random.default_rng(81)
+    k_proj, T, B, nb, nq, k = 16, 64, 16, 4, 12, 8
+    shapes = [(64, 128), (128, 64), (64, 64)]
+    D = len(shapes) * k_proj * k_proj
+    RS = [(synth.to_bf16_bits(rng.standard_normal((d_out, k_proj)) / 4),
+           synth.to_bf16_bits(rng.standard_normal((d_in, k_proj)) / 4)) for d_in, d_out in shapes]
+
+    def batch(nex):
+        return [(synth.to_bf16_bits(rng.standard_normal((nex * T, d_in))),
+                 synth.to_bf16_bits(rng.standard_normal((nex * T, d_out)) * 1e-2)) for d_in, d_out in shapes]
+
+    def rows_fp16(ag):
+        out = torch.empty((ag[0][0].shape[0] // T, D), dtype=torch.float32, device="cuda")
+        mods = [P.Module(dev(a), dev(g), dev(R), dev(S), m * k_proj * k_proj)
+                for m, ((a, g), (R, S)) in enumerate(zip(ag, RS))]
+        P.attr_project(mods, k_proj, out.shape[0], T, out)
+        y = torch.empty(out.shape, dtype=torch.float16, device="cuda")
+        P.attr_precond_apply(out, P.PRECOND_NONE, None, True, y)
+        return y
+
+    def oracle_rows(ag):
+        blocks = [O.project(a.reshape(-1, T, a.shape[1]), g.reshape(-1, T, g.shape[1]), R, S)
+                  for (a, g), (R, S) in zip(ag, RS)]
+        return O.to_f16(O.unit_normalize(O.project_concat(blocks)))
+
+    qb = batch(nq)
+    Qd = rows_fp16(qb)
+    ts = torch.empty((nq, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((nq, k), dtype=torch.int64, device="cuda")
+    train = []
+    for b in range(nb):
+        tb = batch(B)
+        train.append(tb)
+        P.attr_score_topk(Qd, rows_fp16(tb), k, ts, ti, index_base=b * B, merge=b > 0)
+    torch.cuda.synchronize()
+    Gr = np.concatenate([oracle_rows(tb) for tb in train])
+    check_topk(host(ts), host(ti), O.scores(oracle_rows(qb), Gr), k)
+
+
 @pytest.mark.parametrize("k", [1, 10, 100])
 def test_random_unit_rows_f16(k):
     nq, ng, D = 70, 1000, 128            # two query blocks, ragged store tile
