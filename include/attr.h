@@ -128,6 +128,26 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
                          float* out, int64_t ldo, void* ws, size_t ws_bytes,
                          void* stream);
 
+/* Per-token compressed gradients (Figure 1 caption: attribution scores are
+ * per-token or per-sequence): the same projection without the token sum.
+ * For every valid token t of example i and module m the k x k block
+ *     P_{i,t,m} = (R^T g_t)(S^T a_t)^T
+ * is written row-major into out[row * ldo + out_col + r * k + c], where row
+ * = (row_offset ? row_offset[i] : i * T) + t is the token's own row in a
+ * and g.  Rows of tokens t >= len_i and columns outside the module blocks
+ * are not touched; rows >= n_rows are not written (size `out` to cover
+ * every valid token's row).  Summing a token's blocks over t gives
+ * attr_project's row; unit normalisation and scoring of the token rows use
+ * attr_precond_apply and attr_score_topk.  Arguments as attr_project, plus
+ *   out, ldo, n_rows  device fp32 [n_rows, ldo]
+ *   ws        attr_project_workspace_size(...) bytes (the same query)
+ */
+attr_status attr_project_tokens(const attr_module* mods, int32_t n_mods, attr_dtype in_dtype,
+                                int32_t k, int64_t n_examples, int64_t T,
+                                const int64_t* row_offset, const int32_t* length, float* out,
+                                int64_t ldo, int64_t n_rows, void* ws, size_t ws_bytes,
+                                void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* (2a) attr_precond_accumulate: second-moment statistics of store rows.    */
 /* ------------------------------------------------------------------------ */

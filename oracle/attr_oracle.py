@@ -32,7 +32,7 @@ import numpy as np
 
 __all__ = [
     "as_f64", "bf16_bits_to_f64", "to_f16", "project_explicit", "project",
-    "factored_second_moment", "project_normalized", "project_concat", "unit_normalize",
+    "project_tokens", "factored_second_moment", "project_normalized", "project_concat", "unit_normalize",
     "accumulate_diag", "accumulate_full", "kfac_factors", "finalize_diag", "finalize_full",
     "precond_apply", "scores", "score_topk", "merge_topk", "PAD_SCORE", "PAD_INDEX",
 ]
@@ -121,6 +121,24 @@ def project(a: np.ndarray, g: np.ndarray, R: np.ndarray, S: np.ndarray,
         gt = as_f64(g[i, :L[i]]) @ Rf         # len x k, R^T g_t per token
         at = as_f64(a[i, :L[i]]) @ Sf         # len x k, S^T a_t per token
         out[i] = (gt.T @ at).reshape(-1)
+    return out
+
+
+def project_tokens(a: np.ndarray, g: np.ndarray, R: np.ndarray, S: np.ndarray,
+                   length: Optional[Sequence[int]] = None) -> np.ndarray:
+    """Per-token compressed gradients (Figure 1 caption: attribution scores
+    are per-token or per-sequence): for token t of example i the k x k block
+    (R^T g_t)(S^T a_t)^T, flattened like ``project_explicit``; the
+    per-example projection is their sum over valid tokens.  Float64
+    [n, T, k*k], rows of tokens t >= len_i zero (never read)."""
+    n, T, _ = a.shape
+    L = _lengths(n, T, length)
+    Rf, Sf = as_f64(R), as_f64(S)
+    k = Rf.shape[1]
+    out = np.zeros((n, T, k * k))
+    for i in range(n):
+        for t in range(L[i]):
+            out[i, t] = np.outer(Rf.T @ as_f64(g[i, t]), Sf.T @ as_f64(a[i, t])).reshape(-1)
     return out
 
 

@@ -23,7 +23,8 @@ import torch
 
 __all__ = [
     "AttrError", "ATTR_F32", "ATTR_BF16", "ATTR_F16", "PRECOND_NONE", "PRECOND_DIAG",
-    "PRECOND_FULL", "Module", "lib", "lib_path", "attr_project", "attr_precond_accumulate",
+    "PRECOND_FULL", "Module", "lib", "lib_path", "attr_project", "attr_project_tokens",
+    "attr_precond_accumulate",
     "attr_precond_apply", "attr_score_topk", "attr_project_workspace_size",
     "attr_precond_accumulate_workspace_size", "attr_precond_apply_workspace_size",
     "attr_score_topk_workspace_size", "finalize_diag", "finalize_full", "Workspace",
@@ -78,6 +79,9 @@ def lib() -> ctypes.CDLL:
     L.attr_project.restype = ctypes.c_int
     L.attr_project.argtypes = [ctypes.POINTER(_CModule), i32, ctypes.c_int, i32, i64, i64, vp, vp,
                                vp, i64, vp, sz, vp]
+    L.attr_project_tokens.restype = ctypes.c_int
+    L.attr_project_tokens.argtypes = [ctypes.POINTER(_CModule), i32, ctypes.c_int, i32, i64, i64, vp,
+                                      vp, vp, i64, i64, vp, sz, vp]
     L.attr_precond_accumulate_workspace_size.restype = sz
     L.attr_precond_accumulate_workspace_size.argtypes = [i64, i64, ctypes.c_int, ctypes.c_int]
     L.attr_precond_accumulate.restype = ctypes.c_int
@@ -224,6 +228,30 @@ def attr_project(mods: Sequence[Module], k: int, n_examples: int, T: int,
         raise ValueError("length must be contiguous int32")
     _check(L.attr_project(cm, len(mods), in_dtype, k, n_examples, T, _ptr(row_offset), _ptr(length),
                           out.data_ptr(), out.stride(0), wsp, wsn, _stream(stream)))
+    return out
+
+
+def attr_project_tokens(mods: Sequence[Module], k: int, n_examples: int, T: int,
+                        out: torch.Tensor, row_offset: Optional[torch.Tensor] = None,
+                        length: Optional[torch.Tensor] = None, ws: Optional[Workspace] = None,
+                        stream=None) -> torch.Tensor:
+    """Per-token blocks (R^T g_t)(S^T a_t)^T into out[token row, out_col:out_col+k*k]."""
+    if not mods:
+        raise ValueError("need at least one module")
+    in_dtype = _dtype(mods[0].a)
+    cm = _cmods(mods)
+    L = lib()
+    if out.dtype != torch.float32 or out.dim() != 2 or out.stride(1) != 1:
+        raise ValueError("out must be fp32 [rows, ldo] with contiguous rows")
+    need = L.attr_project_workspace_size(cm, len(mods), in_dtype, n_examples, T, k)
+    wsp, wsn = _ws(ws, out.device).get(need)
+    if row_offset is not None and (row_offset.dtype != torch.int64 or not row_offset.is_contiguous()):
+        raise ValueError("row_offset must be contiguous int64")
+    if length is not None and (length.dtype != torch.int32 or not length.is_contiguous()):
+        raise ValueError("length must be contiguous int32")
+    _check(L.attr_project_tokens(cm, len(mods), in_dtype, k, n_examples, T, _ptr(row_offset),
+                                 _ptr(length), out.data_ptr(), out.stride(0), out.shape[0], wsp, wsn,
+                                 _stream(stream)))
     return out
 
 

@@ -213,13 +213,18 @@ size_t attr_project_workspace_size(const attr_module* mods, int32_t n_mods, attr
   }
 }
 
-attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_dtype, int32_t k,
-                         int64_t n_examples, int64_t T, const int64_t* row_offset,
-                         const int32_t* length, float* out, int64_t ldo, void* ws,
-                         size_t ws_bytes, void* stream) {
+// tok: per-token blocks into out rows [0, n_rows) (attr_project_tokens),
+// else per-example rows (attr_project).
+static attr_status project_impl(const attr_module* mods, int32_t n_mods, attr_dtype in_dtype,
+                                int32_t k, int64_t n_examples, int64_t T,
+                                const int64_t* row_offset, const int32_t* length, float* out,
+                                int64_t ldo, void* ws, size_t ws_bytes, void* stream, bool tok,
+                                int64_t n_rows) {
   try {
     g_err.clear();
     attr_status st = project_validate(mods, n_mods, in_dtype, k, n_examples, T, out, ldo);
+    if (st != ATTR_OK) return st;
+    if (tok && n_rows < 0) return fail(ATTR_ERR_INVALID_ARG, "n_rows=%lld is negative", (long long)n_rows);
     if (st != ATTR_OK) return st;
     if (n_examples == 0) return ATTR_OK;
     const int eb = dtype_bytes(in_dtype);
@@ -267,9 +272,11 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
     hipError_t e = hipSuccess;
     for (const ProjRun& r : L.runs) {
       e = attr::launch_project_main(bf16, nk, r.ms, tab, r.slot0, r.n_groups, L.n_chunks,
-                                    n_examples, T, row_offset, length, part, s);
+                                    n_examples, T, row_offset, length, tok ? out : part, s, tok,
+                                    ldo, n_rows);
       if (e != hipSuccess) return device_fail(e, "attr_project main launch");
     }
+    if (tok) return ATTR_OK;
     e = attr::launch_project_reduce(nk, tab, n_mods, L.n_chunks, n_examples, T, length, part, out,
                                     ldo, s);
     if (e != hipSuccess) return device_fail(e, "attr_project reduce launch");
@@ -279,6 +286,23 @@ attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_
   } catch (...) {
     return fail(ATTR_ERR_INVALID_ARG, "attr_project: unknown host exception");
   }
+}
+
+attr_status attr_project(const attr_module* mods, int32_t n_mods, attr_dtype in_dtype, int32_t k,
+                         int64_t n_examples, int64_t T, const int64_t* row_offset,
+                         const int32_t* length, float* out, int64_t ldo, void* ws,
+                         size_t ws_bytes, void* stream) {
+  return project_impl(mods, n_mods, in_dtype, k, n_examples, T, row_offset, length, out, ldo, ws,
+                      ws_bytes, stream, false, 0);
+}
+
+attr_status attr_project_tokens(const attr_module* mods, int32_t n_mods, attr_dtype in_dtype,
+                                int32_t k, int64_t n_examples, int64_t T,
+                                const int64_t* row_offset, const int32_t* length, float* out,
+                                int64_t ldo, int64_t n_rows, void* ws, size_t ws_bytes,
+                                void* stream) {
+  return project_impl(mods, n_mods, in_dtype, k, n_examples, T, row_offset, length, out, ldo, ws,
+                      ws_bytes, stream, true, n_rows);
 }
 
 // ---------------------------------------------------------------------------

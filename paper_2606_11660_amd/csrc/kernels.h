@@ -51,10 +51,12 @@ hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab*
 // groups of up to kProjGroupMax consecutive slots (one read of a per group);
 // one launch per group size ms covers n_groups groups from slot0.
 constexpr int kProjGroupMax = 3;
+// tok: per-token blocks written straight into `partial` = the output [n_rows, ldo]
 hipError_t launch_project_main(bool bf16, int nk, int ms, const ProjTab* tab, int slot0,
                                int n_groups, int n_chunks, int64_t n_ex, int64_t T,
                                const int64_t* row_offset, const int32_t* length,
-                               float* partial, hipStream_t s);
+                               float* partial, hipStream_t s, bool tok = false, int64_t ldo = 0,
+                               int64_t n_rows = 0);
 hipError_t launch_project_reduce(int nk, const ProjTab* tab, int n_slots, int n_chunks,
                                  int64_t n_ex, int64_t T, const int32_t* length,
                                  const float* partial, float* out, int64_t ldo,

@@ -264,11 +264,15 @@ __device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int
 // input rows a: the a tiles are read once and projected through each
 // member's S; each member's own g rows follow, and each member's k x k
 // partial goes to its slot's item.
-template <bool BF16, int NK, int MS>
+// TOK: per-token blocks instead of the token sum: token t's (R^T g_t)(S^T
+// a_t)^T is written to row (first row of the example) + t of `partial`
+// (then the caller's output, row stride ldo, n_rows rows), at the module's
+// out_col; no partials, no reduction.
+template <bool BF16, int NK, int MS, bool TOK>
 __global__ __launch_bounds__(256) void project_main_kernel(
     const ProjTab* __restrict__ tab, int slot0, int n_chunks, int64_t n_ex, int64_t T,
     const int64_t* __restrict__ row_offset, const int32_t* __restrict__ length,
-    float* __restrict__ partial) {
+    float* __restrict__ partial, int64_t ldo, int64_t n_rows) {
   using E_t = ElemT<BF16>;
   using Tag = typename E_t::tag;
   constexpr int EB = E_t::bytes;
@@ -341,19 +345,41 @@ __global__ __launch_bounds__(256) void project_main_kernel(
         for (int ct = 0; ct < NK; ++ct) Gt[0][tt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
       project_side<Tag, E, NK, TT, Tiles<NK>::PD, 1>(rg, md.ldg, md.d_out, pkR, lane, xp, Gt);
 
-      // P[r][c] += sum_tokens Gt[token][r] * At[token][c]; register q of the
-      // stage-1 tiles holds token 4 * (lane / 16) + q, column lane % 16.
+      if constexpr (TOK) {
+        // register q of the stage-1 tiles holds token 16 tt + 4 (lane / 16) +
+        // q of the wave, column lane % 16: g~[t][r] comes from lane r % 16 of
+        // the same 16-lane group (every lane shuffles, only valid tokens store)
 #pragma unroll
-      for (int tt = 0; tt < TT; ++tt)
+        for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
-        for (int rt = 0; rt < NK; ++rt)
+          for (int q = 0; q < 4; ++q) {
+            const int tw = 16 * tt + 4 * (lane >> 4) + q;
+            const bool ok = tw < ntok && row0 + tw < n_rows;
+            float* orow = partial + (row0 + (ok ? tw : 0)) * ldo + md.out_col + (lane & 15);
 #pragma unroll
-          for (int ct = 0; ct < NK; ++ct)
+            for (int r = 0; r < 16 * NK; ++r) {
+              const float gr = __shfl(Gt[0][tt][r >> 4][q], r & 15, 16);
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-              P[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(Gt[0][tt][rt][q], At[m][tt][ct][q],
-                                                               P[rt][ct], 0, 0, 0);
+              for (int ct = 0; ct < NK; ++ct)
+                if (ok) orow[r * 16 * NK + 16 * ct] = gr * At[m][tt][ct][q];
+            }
+          }
+      } else {
+        // P[r][c] += sum_tokens Gt[token][r] * At[token][c]; register q of the
+        // stage-1 tiles holds token 4 * (lane / 16) + q, column lane % 16.
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+          for (int rt = 0; rt < NK; ++rt)
+#pragma unroll
+            for (int ct = 0; ct < NK; ++ct)
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                P[rt][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(Gt[0][tt][rt][q], At[m][tt][ct][q],
+                                                                 P[rt][ct], 0, 0, 0);
+      }
     }
+    if constexpr (TOK) continue;
 
     // Fixed-order reduction of the four wave partials: waves 1..3 park their
     // tiles in LDS, wave 0 adds them in wave order and writes the item.
@@ -448,17 +474,24 @@ hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab*
 hipError_t launch_project_main(bool bf16, int nk, int ms, const ProjTab* tab, int slot0,
                                int n_groups, int n_chunks, int64_t n_ex, int64_t T,
                                const int64_t* row_offset, const int32_t* length,
-                               float* partial, hipStream_t s) {
+                               float* partial, hipStream_t s, bool tok, int64_t ldo,
+                               int64_t n_rows) {
   const int64_t nblk = (int64_t)n_groups * n_chunks * n_ex;
   if (nblk == 0) return hipSuccess;
   dim3 grid((unsigned)nblk), block(256);
-#define ATTR_MAIN(B, N, M)                                                                      \
-  hipLaunchKernelGGL((project_main_kernel<B, N, M>), grid, block, 0, s, tab, slot0, n_chunks, n_ex, \
-                     T, row_offset, length, partial)
-#define ATTR_MAIN_MS(B, N)               \
-  if (ms == 1) ATTR_MAIN(B, N, 1);       \
-  else if (ms == 2) ATTR_MAIN(B, N, 2);  \
-  else ATTR_MAIN(B, N, 3);
+#define ATTR_MAIN(B, N, M, TK)                                                                    \
+  hipLaunchKernelGGL((project_main_kernel<B, N, M, TK>), grid, block, 0, s, tab, slot0, n_chunks,  \
+                     n_ex, T, row_offset, length, partial, ldo, n_rows)
+#define ATTR_MAIN_MS(B, N)                                                   \
+  if (tok) {                                                                 \
+    if (ms == 1) ATTR_MAIN(B, N, 1, true);                                   \
+    else if (ms == 2) ATTR_MAIN(B, N, 2, true);                              \
+    else ATTR_MAIN(B, N, 3, true);                                           \
+  } else {                                                                   \
+    if (ms == 1) ATTR_MAIN(B, N, 1, false);                                  \
+    else if (ms == 2) ATTR_MAIN(B, N, 2, false);                             \
+    else ATTR_MAIN(B, N, 3, false);                                          \
+  }
   if (ms < 1 || ms > kProjGroupMax) return hipErrorInvalidValue;
   if (bf16) {
     if (nk == 1) { ATTR_MAIN_MS(true, 1) }

@@ -83,6 +83,12 @@ def test_project_validation(L):
     assert _project(L, [_mod()], ws=FAKE + 16, wsb=need) == ALIGN   # workspace not 256-aligned
     # zero examples: valid no-op that touches nothing
     assert _project(L, [_mod()], n=0) == OK
+    # per-token variant: same checks, plus the output row count
+    tok = lambda n_rows, out=FAKE: L.attr_project_tokens((P._CModule * 1)(_mod()), 1, P.ATTR_BF16, 16,
+                                                          4, 32, None, None, out, 256, n_rows, None, 0, None)
+    assert tok(-1) == INVALID
+    assert tok(128, out=0) == INVALID
+    assert tok(128) == WORKSPACE
 
 
 def test_project_workspace_size_grows_with_batch(L):

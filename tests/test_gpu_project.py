@@ -200,6 +200,64 @@ def test_optimizer_state_factors_both_or_neither():
         P.attr_project([m], 16, 1, 4, out)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("k", [16, 64])
+@pytest.mark.parametrize("packed", [False, True])
+def test_per_token_blocks(dtype, k, packed):
+    """attr_project_tokens: every valid token's k x k block at the token's
+    own row (padded layout, or packed back to back through row_offset);
+    padded tokens' rows and columns outside the blocks untouched; two modules
+    share their input rows (grouped path); the token rows of an example sum
+    to attr_project's row."""
+    n, T = 3, 300
+    lengths = [1, 300, 77]
+    shapes = [(64, 192), (128, 64), (64, 128)]
+    say(f"case: per-token blocks dtype={dtype} k={k} packed={packed}")
+    mods_host = _random_modules(shapes, n, T, k, dtype, seed=600 + k, lengths=lengths)
+    a0 = mods_host[0][0]
+    mods_host[2] = (a0, mods_host[2][1], mods_host[2][2], mods_host[2][3])   # shares module 0's a
+    D = len(shapes) * k * k
+    if packed:
+        offs = np.concatenate([[0], np.cumsum(lengths)[:-1]]).astype(np.int64)
+        rows = int(sum(lengths))
+        def pack(x):
+            return np.concatenate([x[i * T:i * T + lengths[i]] for i in range(n)])
+        dev_mods_src = [(pack(a), pack(g), R, S) for a, g, R, S in mods_host]
+        ro = torch.from_numpy(offs).cuda()
+    else:
+        rows = n * T
+        dev_mods_src = mods_host
+        ro = None
+    a_dev = {}
+    mods = []
+    for m, (a, g, R, S) in enumerate(dev_mods_src):
+        key = id(mods_host[m][0])
+        if key not in a_dev:
+            a_dev[key] = dev(a)
+        mods.append(P.Module(a_dev[key], dev(g), dev(R), dev(S), out_col=m * k * k))
+    L = torch.from_numpy(np.asarray(lengths, dtype=np.int32)).cuda()
+    out = torch.full((rows, D + 5), -7.0, dtype=torch.float32, device="cuda")
+    P.attr_project_tokens(mods, k, n, T, out, row_offset=ro, length=L)
+    ex = torch.empty((n, D), dtype=torch.float32, device="cuda")
+    P.attr_project(mods, k, n, T, ex, row_offset=ro, length=L)
+    torch.cuda.synchronize()
+    got = host(out)
+    ref = O.project_concat([O.project_tokens(a.reshape(n, T, -1), g.reshape(n, T, -1), R, S,
+                                             length=lengths).reshape(n * T, -1)
+                            for a, g, R, S in mods_host]).reshape(n, T, D)
+    tol = BF16_DESIGN if dtype == "bf16" else F32_TOL
+    assert (got[:, D:] == -7.0).all()
+    for i in range(n):
+        r0 = int(offs[i]) if packed else i * T
+        blk = got[r0:r0 + lengths[i], :D]
+        err = row_rel_l2(blk, ref[i, :lengths[i]])
+        assert err.max() <= tol, (i, err.max())
+        if not packed:
+            assert (got[r0 + lengths[i]:r0 + T] == -7.0).all()
+        np.testing.assert_allclose(blk.astype(np.float64).sum(0), host(ex)[i], rtol=1e-4,
+                                   atol=1e-4 * np.abs(host(ex)[i]).max())
+
+
 def test_untouched_columns_and_row_offset():
     n, T, k = 5, 40, 16
     say("case: row_offset packed layout, extra output columns")

@@ -146,6 +146,24 @@ def _small_module(seed, n=3, T=6, d_in=24, d_out=40, k=16):
     return rng, a, g, R, S
 
 
+def test_project_tokens_rank_one_blocks_summing_to_the_example():
+    """Per-token blocks: each k x k block has rank one (its singular values
+    past the first vanish), a token's block equals the example projection of
+    that token alone, the valid blocks sum to the per-example projection,
+    and padded tokens give zero rows."""
+    rng, a, g, R, S = _small_module(35)
+    L = [6, 2, 0]
+    an = np.stack([synth.nan_pad(a[i], L[i]) for i in range(3)])
+    gn = np.stack([synth.nan_pad(g[i], L[i]) for i in range(3)])
+    Pt = O.project_tokens(an, gn, R, S, length=L)
+    k = R.shape[1]
+    sv = np.linalg.svd(Pt[0, 3].reshape(k, k), compute_uv=False)
+    assert sv[1] <= 1e-12 * sv[0]
+    np.testing.assert_allclose(Pt[1, 1], O.project(a[1:2, 1:2], g[1:2, 1:2], R, S)[0], rtol=1e-12)
+    np.testing.assert_allclose(Pt.sum(axis=1), O.project(an, gn, R, S, length=L), rtol=1e-10, atol=1e-12)
+    assert (Pt[1, 2:] == 0).all() and (Pt[2] == 0).all()
+
+
 def test_normalized_uniform_factors_scale_plain_projection():
     """v_out = alpha 1, v_in = beta 1: V = beta / d_out everywhere, so the
     normalised projection is sqrt(d_out / beta) times the plain one."""
