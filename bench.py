@@ -477,6 +477,14 @@ def main():
     scan_ms = scan_ev[0].elapsed_time(scan_ev[1]) / reps
     scan_bytes = n_store * D * 2 + wl.n_queries * D * 2
 
+    # ---------------- per-token blocks of the same batch (reported separately) ----------------
+    tok_rows = torch.empty((B * T, D), dtype=torch.float32, device=dev)
+    tok_ms = _timeit(lambda: P.attr_project_tokens(mods, k, B, T, tok_rows, ws=ws_p, stream=stream),
+                     stream, 5)
+    del tok_rows
+    tok_bytes = B * T * wl.elems_per_token() * 2 + B * T * D * 4 + sum(
+        (md.d_in + md.d_out) * k * 2 for md in wl.modules)
+
     # algorithmic bytes of one projection call: a/g rows once, R/S once, fp32 rows out
     per_example = T * wl.elems_per_token() * 2 + D * 4
     rs_bytes = sum((md.d_in + md.d_out) * k * 2 for md in wl.modules)
@@ -508,6 +516,9 @@ def main():
         "store_scan": {"queries": wl.n_queries, "rows": n_store, "D": D, "k": wl.topk,
                        "ms": scan_ms, "pairs_per_s": wl.n_queries * n_store / (scan_ms * 1e-3),
                        "GBps": scan_bytes / (scan_ms * 1e-3) / 1e9},
+        "per_token_projection": {"tokens": B * T, "ms": tok_ms, "bytes": tok_bytes,
+                                 "GBps": tok_bytes / tok_ms / 1e6,
+                                 "frac_hbm": tok_bytes / tok_ms / 1e6 / HBM_PEAK_GBPS},
     }
     del mods, store, rows32
     torch.cuda.empty_cache()

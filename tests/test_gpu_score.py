@@ -94,6 +94,42 @@ def test_on_the_fly_scoring_without_a_store():
     check_topk(host(ts), host(ti), O.scores(oracle_rows(qb), Gr), k)
 
 
+def test_per_token_attribution():
+    """Per-token attribution: the training batch's per-token compressed
+    gradients (attr_project_tokens, packed valid tokens), unit-normalised to
+    fp16, scored against per-sequence queries; the top tokens per query
+    match the oracle's top-k over all valid tokens."""
+    say("case: per-token attribution")
+    rng = np.random.default_rng(82)
+    k_proj, T, nq, k = 16, 96, 6, 10
+    lengths = [96, 40, 73, 1]
+    n = len(lengths)
+    shapes = [(64, 128), (128, 64)]
+    D = len(shapes) * k_proj * k_proj
+    RS = [(synth.to_bf16_bits(rng.standard_normal((d_out, k_proj)) / 4),
+           synth.to_bf16_bits(rng.standard_normal((d_in, k_proj)) / 4)) for d_in, d_out in shapes]
+    ag = [(synth.to_bf16_bits(rng.standard_normal((n, T, d_in))),
+           synth.to_bf16_bits(rng.standard_normal((n, T, d_out)))) for d_in, d_out in shapes]
+    offs = np.concatenate([[0], np.cumsum(lengths)[:-1]]).astype(np.int64)
+    tot = int(sum(lengths))
+    mods = []
+    for m, ((a, g), (R, S)) in enumerate(zip(ag, RS)):
+        a_pk = np.concatenate([a[i, :lengths[i]] for i in range(n)])
+        g_pk = np.concatenate([g[i, :lengths[i]] for i in range(n)])
+        mods.append(P.Module(dev(a_pk), dev(g_pk), dev(R), dev(S), m * k_proj * k_proj))
+    rows = torch.empty((tot, D), dtype=torch.float32, device="cuda")
+    P.attr_project_tokens(mods, k_proj, n, T, rows, row_offset=torch.from_numpy(offs).cuda(),
+                          length=torch.from_numpy(np.asarray(lengths, dtype=np.int32)).cuda())
+    G16 = torch.empty((tot, D), dtype=torch.float16, device="cuda")
+    P.attr_precond_apply(rows, P.PRECOND_NONE, None, True, G16)
+    Q = synth.unit_rows(nq, D, seed=83)
+    ts, ti = _topk(dev(Q), G16, k)
+    blocks = [O.project_tokens(a, g, R, S, length=lengths) for (a, g), (R, S) in zip(ag, RS)]
+    tok = O.project_concat([b.reshape(n * T, -1) for b in blocks]).reshape(n, T, D)
+    Gr = O.to_f16(O.unit_normalize(np.concatenate([tok[i, :lengths[i]] for i in range(n)])))
+    check_topk(host(ts), host(ti), O.scores(Q, Gr), k)
+
+
 @pytest.mark.parametrize("k", [1, 10, 100])
 def test_random_unit_rows_f16(k):
     nq, ng, D = 70, 1000, 128            # two query blocks, ragged store tile
