@@ -69,7 +69,7 @@ struct ProjLayout {
 };
 
 ProjLayout project_layout(const attr_module* mods, int32_t n_mods, int eb, int64_t n_ex,
-                          int64_t T, int k) {
+                          int64_t T, int k, bool tok = false) {
   ProjLayout L;
   const int nk = k / 16;
   // Modules that read the same input rows (same a, lda and d_in: q/k/v or
@@ -79,7 +79,9 @@ ProjLayout project_layout(const attr_module* mods, int32_t n_mods, int eb, int64
   // starts the longest items first; a group's members take consecutive slots.
   // (three members at k = 64 would need more than 256 VGPRs: two waves per
   // SIMD no longer fit, so groups stop at two there)
-  const size_t gmax = nk >= 4 ? 2 : (size_t)attr::kProjGroupMax;
+  // (per-token blocks keep one module per item: their row-writing code would
+  // pass 256 VGPRs with two or three)
+  const size_t gmax = tok ? 1 : (nk >= 4 ? 2 : (size_t)attr::kProjGroupMax);
   std::vector<std::vector<int>> groups;
   std::map<std::tuple<const void*, int64_t, int64_t>, size_t> open;
   for (int x = 0; x < n_mods; ++x) {
@@ -228,7 +230,7 @@ static attr_status project_impl(const attr_module* mods, int32_t n_mods, attr_dt
     if (st != ATTR_OK) return st;
     if (n_examples == 0) return ATTR_OK;
     const int eb = dtype_bytes(in_dtype);
-    ProjLayout L = project_layout(mods, n_mods, eb, n_examples, T, k);
+    ProjLayout L = project_layout(mods, n_mods, eb, n_examples, T, k, tok);
     if (!ws || ws_bytes < L.total)
       return fail(ATTR_ERR_WORKSPACE, "attr_project needs %zu workspace bytes, got %zu", L.total,
                   ws ? ws_bytes : (size_t)0);
