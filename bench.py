@@ -77,11 +77,12 @@ def _cpu_baseline(n_sample: int = 6, min_seconds: float = 12.0):
 
 
 
-def _measured_traffic():
-    """HBM bytes per attr_project call from the committed rocprofv3 counter
-    summary (FETCH_SIZE and WRITE_SIZE runs, scaled by the copy-kernel
-    calibration), or None when the projection source has changed since the
-    counters were taken."""
+def _measured_traffic(key="traffic_bytes_per_call"):
+    """HBM bytes per attr_project call (or, with key
+    "per_token_traffic_bytes_per_call", per attr_project_tokens call) from the
+    committed rocprofv3 counter summary (FETCH_SIZE and WRITE_SIZE runs,
+    scaled by the copy-kernel calibration), or None when the projection
+    source has changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "project_gpt2_traffic.txt")
     src = os.path.join(ROOT, "paper_2606_11660_amd", "csrc", "project.hip")
@@ -90,7 +91,7 @@ def _measured_traffic():
         digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
         if fields.get("source_sha256_16", "").strip() != digest:
             return None
-        return int(fields["traffic_bytes_per_call"])
+        return int(fields[key])
     except (OSError, KeyError, ValueError):
         return None
 
@@ -518,7 +519,8 @@ def main():
                        "GBps": scan_bytes / (scan_ms * 1e-3) / 1e9},
         "per_token_projection": {"tokens": B * T, "ms": tok_ms, "bytes": tok_bytes,
                                  "GBps": tok_bytes / tok_ms / 1e6,
-                                 "frac_hbm": tok_bytes / tok_ms / 1e6 / HBM_PEAK_GBPS},
+                                 "frac_hbm": tok_bytes / tok_ms / 1e6 / HBM_PEAK_GBPS,
+                                 "traffic": _measured_traffic("per_token_traffic_bytes_per_call")},
     }
     del mods, store, rows32
     torch.cuda.empty_cache()
