@@ -227,7 +227,6 @@ static attr_status project_impl(const attr_module* mods, int32_t n_mods, attr_dt
     attr_status st = project_validate(mods, n_mods, in_dtype, k, n_examples, T, out, ldo);
     if (st != ATTR_OK) return st;
     if (tok && n_rows < 0) return fail(ATTR_ERR_INVALID_ARG, "n_rows=%lld is negative", (long long)n_rows);
-    if (st != ATTR_OK) return st;
     if (n_examples == 0) return ATTR_OK;
     const int eb = dtype_bytes(in_dtype);
     ProjLayout L = project_layout(mods, n_mods, eb, n_examples, T, k, tok);

@@ -147,7 +147,7 @@ def test_shared_inputs_grouped(dtype, k):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("k", [16, 64])
+@pytest.mark.parametrize("k", [16, 32, 64])
 def test_optimizer_state_normalisation(dtype, k):
     """Gradients normalised by a factored (Adafactor) second moment before
     projection, next to a module without normalisation in the same call;
@@ -201,7 +201,7 @@ def test_optimizer_state_factors_both_or_neither():
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("k", [16, 64])
+@pytest.mark.parametrize("k", [16, 32, 64])
 @pytest.mark.parametrize("packed", [False, True])
 def test_per_token_blocks(dtype, k, packed):
     """attr_project_tokens: every valid token's k x k block at the token's
@@ -256,6 +256,47 @@ def test_per_token_blocks(dtype, k, packed):
             assert (got[r0 + lengths[i]:r0 + T] == -7.0).all()
         np.testing.assert_allclose(blk.astype(np.float64).sum(0), host(ex)[i], rtol=1e-4,
                                    atol=1e-4 * np.abs(host(ex)[i]).max())
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("k", [16, 32])
+def test_per_token_blocks_normalised(dtype, k):
+    """Per-token blocks of optimizer-normalised gradients: each valid token's
+    block equals the oracle's normalised projection of a one-token example
+    (the definition, G_t = g_t a_t^T divided elementwise by sqrt(V)); a
+    module without factors in the same call; padded tokens' rows untouched."""
+    n, T = 3, 200
+    lengths = [200, 1, 45]
+    shapes = [(64, 192), (128, 64)]
+    say(f"case: per-token normalised dtype={dtype} k={k}")
+    mods_host = _random_modules(shapes, n, T, k, dtype, seed=700 + k, lengths=lengths)
+    rng = np.random.default_rng(800 + k)
+    vo = rng.uniform(0.05, 3.0, shapes[0][1]).astype(np.float32)
+    vi = rng.uniform(0.05, 3.0, shapes[0][0]).astype(np.float32)
+    vo[2], vi[9] = 0.0, -1.0
+    D = len(shapes) * k * k
+    mods = [P.Module(dev(a), dev(g), dev(R), dev(S), out_col=m * k * k,
+                     v_out=dev(vo) if m == 0 else None, v_in=dev(vi) if m == 0 else None)
+            for m, (a, g, R, S) in enumerate(mods_host)]
+    out = torch.full((n * T, D), -7.0, dtype=torch.float32, device="cuda")
+    P.attr_project_tokens(mods, k, n, T, out, length=torch.from_numpy(np.asarray(lengths, dtype=np.int32)).cuda())
+    torch.cuda.synchronize()
+    got = host(out)
+    tok_len = [1 if t < lengths[i] else 0 for i in range(n) for t in range(T)]
+    blocks = []
+    for m, (a, g, R, S) in enumerate(mods_host):
+        a1, g1 = a.reshape(n * T, 1, -1), g.reshape(n * T, 1, -1)
+        blocks.append(O.project_normalized(a1, g1, R, S, vo, vi, length=tok_len) if m == 0 else
+                      O.project(a1, g1, R, S, length=tok_len))
+    ref = O.project_concat(blocks).reshape(n, T, D)
+    # bf16: the scaled R/S are rounded to bf16 once more (as in attr_project)
+    tol = BF16_TOL if dtype == "bf16" else F32_TOL
+    for i in range(n):
+        blk = got[i * T:i * T + lengths[i]]
+        err = row_rel_l2(blk, ref[i, :lengths[i]])
+        say(f"example {i}: max row rel-L2 {err.max():.2e}")
+        assert err.max() <= tol, (i, err.max())
+        assert (got[i * T + lengths[i]:(i + 1) * T] == -7.0).all()
 
 
 def test_untouched_columns_and_row_offset():
