@@ -423,6 +423,8 @@ def main():
     n_store = max(args.steps, 1) * B
     store = torch.empty((n_store, D), dtype=torch.float16, device=dev)
     rows32 = torch.empty((B, D), dtype=torch.float32, device=dev)
+    rows32b = [rows32, torch.empty((B, D), dtype=torch.float32, device=dev)]
+    stream2 = torch.cuda.Stream(device=dev)
     Qrows = torch.empty((wl.n_queries, D), dtype=torch.float16, device=dev)
     top_s = torch.empty((wl.n_queries, wl.topk), dtype=torch.float32, device=dev)
     top_i = torch.empty((wl.n_queries, wl.topk), dtype=torch.int64, device=dev)
@@ -433,34 +435,50 @@ def main():
         P.attr_precond_apply(rows32, P.PRECOND_NONE, None, True, Qrows[:B], ws=ws_a, stream=stream)
     stream.synchronize()
 
-    def step(i):
-        slot = store[(i % (n_store // B)) * B:((i % (n_store // B)) + 1) * B]
-        P.attr_project(mods, k, B, T, rows32, ws=ws_p, stream=stream)
-        P.attr_precond_apply(rows32, P.PRECOND_NONE, None, True, slot, ws=ws_a, stream=stream)
-        P.attr_score_topk(Qrows, slot, wl.topk, top_s, top_i, index_base=(i % (n_store // B)) * B,
-                          merge=i > 0, ws=ws_s, stream=stream)
+    # A step is projection (on `stream`) -> unit norm into the store slot ->
+    # top-k merge against the queries (both on `stream2`).  Two fp32 row
+    # buffers let the projection of batch i + 1 run while batch i is
+    # normalised and scored: the projection into buffer b waits for the norm
+    # that last read b, the norm waits for its projection.
+    proj_done = [torch.cuda.Event() for _ in range(2)]
+    norm_done = [torch.cuda.Event() for _ in range(2)]
+    for e in norm_done:
+        e.record(stream2)
 
-    with torch.cuda.stream(stream):
-        for i in range(args.warmup):
-            step(i)
+    def steps(i0, n, ev=None):
+        for i in range(i0, i0 + n):
+            b = i % 2
+            slot_i = i % (n_store // B)
+            slot = store[slot_i * B:(slot_i + 1) * B]
+            stream.wait_event(norm_done[b])
+            if ev is not None:
+                ev[i - i0][0].record(stream)
+            P.attr_project(mods, k, B, T, rows32b[b], ws=ws_p, stream=stream)
+            if ev is not None:
+                ev[i - i0][1].record(stream)
+            proj_done[b].record(stream)
+            stream2.wait_event(proj_done[b])
+            P.attr_precond_apply(rows32b[b], P.PRECOND_NONE, None, True, slot, ws=ws_a, stream=stream2)
+            norm_done[b].record(stream2)
+            P.attr_score_topk(Qrows, slot, wl.topk, top_s, top_i, index_base=slot_i * B,
+                              merge=i > 0, ws=ws_s, stream=stream2)
+
+    steps(0, args.warmup)
     stream.synchronize()
+    stream2.synchronize()
     torch.cuda.synchronize()
 
     # ---------------- timed region ----------------
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
+    for e in norm_done:
+        e.record(stream2)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    with torch.cuda.stream(stream):
-        for i in range(args.steps):
-            slot = store[i * B:(i + 1) * B]
-            ev[i][0].record(stream)
-            P.attr_project(mods, k, B, T, rows32, ws=ws_p, stream=stream)
-            ev[i][1].record(stream)
-            P.attr_precond_apply(rows32, P.PRECOND_NONE, None, True, slot, ws=ws_a, stream=stream)
-            P.attr_score_topk(Qrows, slot, wl.topk, top_s, top_i, index_base=i * B, merge=i > 0,
-                              ws=ws_s, stream=stream)
+    # the timed steps fill store slots 0 .. steps - 1 and restart the merge
+    steps(0, args.steps, ev)
     stream.synchronize()
+    stream2.synchronize()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     proj_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
@@ -522,7 +540,7 @@ def main():
                                  "frac_hbm": tok_bytes / tok_ms / 1e6 / HBM_PEAK_GBPS,
                                  "traffic": _measured_traffic("per_token_traffic_bytes_per_call")},
     }
-    del mods, store, rows32
+    del mods, store, rows32, rows32b
     torch.cuda.empty_cache()
     if not args.quick:
         try:
