@@ -164,6 +164,38 @@ def test_project_tokens_rank_one_blocks_summing_to_the_example():
     assert (Pt[1, 2:] == 0).all() and (Pt[2] == 0).all()
 
 
+def test_factored_second_moment_rebuilds_rank_one_from_sums():
+    """Adafactor's factored estimate, built from the row sums and column sums
+    of a non-negative rank-one matrix W = r c^T, is W itself (row sums r_i
+    sum(c), column sums c_j sum(r)); a dropped or wrong normaliser fails."""
+    rng = np.random.default_rng(41)
+    r, c = rng.uniform(0.1, 2.0, 7), rng.uniform(0.1, 2.0, 5)
+    W = np.outer(r, c)
+    V = O.factored_second_moment(W.sum(axis=1), W.sum(axis=0))
+    np.testing.assert_allclose(V, W, rtol=1e-13)
+
+
+def test_factored_second_moment_worked_case():
+    """v_out = (1, 3), v_in = (2, 0, -1): non-positive factors read as 0,
+    V = v_out v_in^T / 4 = [[0.5, 0, 0], [1.5, 0, 0]] by hand; all-zero row
+    factors give V = 0."""
+    V = O.factored_second_moment(np.array([1.0, 3.0]), np.array([2.0, 0.0, -1.0]))
+    np.testing.assert_array_equal(V, np.array([[0.5, 0.0, 0.0], [1.5, 0.0, 0.0]]))
+    assert not O.factored_second_moment(np.zeros(3), np.ones(2)).any()
+
+
+def test_to_f16_rounding_fixed_by_ieee754():
+    """Binary16 rounding to nearest, ties to even (IEEE 754): 2049 and 2051
+    are ties between representable neighbours 2 apart; 65520 is the tie
+    between the largest finite value 65504 and the overflow threshold, so it
+    rounds to infinity; 2^-24 is the smallest subnormal and 2^-25 ties to 0."""
+    x = np.array([2049.0, 2051.0, 65519.0, 65520.0, 2.0 ** -24, 2.0 ** -25, 3 * 2.0 ** -26, -2049.0])
+    with np.errstate(over="ignore"):
+        got = O.to_f16(x).astype(np.float64)
+    want = np.array([2048.0, 2052.0, 65504.0, np.inf, 2.0 ** -24, 0.0, 2.0 ** -24, -2048.0])
+    np.testing.assert_array_equal(got, want)
+
+
 def test_normalized_uniform_factors_scale_plain_projection():
     """v_out = alpha 1, v_in = beta 1: V = beta / d_out everywhere, so the
     normalised projection is sqrt(d_out / beta) times the plain one."""
