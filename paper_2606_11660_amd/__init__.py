@@ -135,28 +135,44 @@ def _rows(t: torch.Tensor) -> Tuple[int, int, int]:
     return rows, width, ld
 
 
+def _torch_stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream))
+
+
 class Workspace:
-    """Grow-only device scratch buffer handed to the library calls."""
+    """Grow-only device scratch buffer handed to the library calls.
+
+    A workspace serves one stream at a time: calls that may overlap on
+    different streams need workspaces of their own (the default workspace is
+    kept per device and stream).  Every use records its stream on the
+    buffer, so a buffer replaced by a larger one is not handed out again by
+    torch's allocator before the work queued on those streams has finished.
+    """
 
     def __init__(self, device=None):
         self.device = torch.device(device or "cuda")
         self.buf: Optional[torch.Tensor] = None
 
-    def get(self, nbytes: int) -> Tuple[Optional[int], int]:
+    def get(self, nbytes: int, stream=None) -> Tuple[Optional[int], int]:
         if nbytes == 0:
             return None, 0
         if self.buf is None or self.buf.numel() < nbytes:
             self.buf = torch.empty(int(nbytes), dtype=torch.uint8, device=self.device)
+        self.buf.record_stream(_torch_stream(stream))
         return self.buf.data_ptr(), self.buf.numel()
 
 
-_default_ws: Dict[str, Workspace] = {}
+_default_ws: Dict[Tuple[str, int], Workspace] = {}
 
 
-def _ws(ws: Optional[Workspace], device) -> Workspace:
+def _ws(ws: Optional[Workspace], device, stream=None) -> Workspace:
     if ws is not None:
         return ws
-    key = str(device)
+    key = (str(device), _stream(stream))
     if key not in _default_ws:
         _default_ws[key] = Workspace(device)
     return _default_ws[key]
@@ -221,7 +237,7 @@ def attr_project(mods: Sequence[Module], k: int, n_examples: int, T: int,
     if out.dtype != torch.float32 or out.dim() != 2 or out.stride(1) != 1:
         raise ValueError("out must be fp32 [n, ldo] with contiguous rows")
     need = L.attr_project_workspace_size(cm, len(mods), in_dtype, n_examples, T, k)
-    wsp, wsn = _ws(ws, out.device).get(need)
+    wsp, wsn = _ws(ws, out.device, stream).get(need, stream)
     if row_offset is not None and (row_offset.dtype != torch.int64 or not row_offset.is_contiguous()):
         raise ValueError("row_offset must be contiguous int64")
     if length is not None and (length.dtype != torch.int32 or not length.is_contiguous()):
@@ -244,7 +260,7 @@ def attr_project_tokens(mods: Sequence[Module], k: int, n_examples: int, T: int,
     if out.dtype != torch.float32 or out.dim() != 2 or out.stride(1) != 1:
         raise ValueError("out must be fp32 [rows, ldo] with contiguous rows")
     need = L.attr_project_workspace_size(cm, len(mods), in_dtype, n_examples, T, k)
-    wsp, wsn = _ws(ws, out.device).get(need)
+    wsp, wsn = _ws(ws, out.device, stream).get(need, stream)
     if row_offset is not None and (row_offset.dtype != torch.int64 or not row_offset.is_contiguous()):
         raise ValueError("row_offset must be contiguous int64")
     if length is not None and (length.dtype != torch.int32 or not length.is_contiguous()):
@@ -271,7 +287,7 @@ def attr_precond_accumulate(X: torch.Tensor, mode: int, H: torch.Tensor,
         raise ValueError("H must be contiguous fp32")
     L = lib()
     need = L.attr_precond_accumulate_workspace_size(n, D, xd, mode)
-    wsp, wsn = _ws(ws, X.device).get(need)
+    wsp, wsn = _ws(ws, X.device, stream).get(need, stream)
     _check(L.attr_precond_accumulate(X.data_ptr(), xd, n, D, ldx, mode, H.data_ptr(), wsp, wsn,
                                      _stream(stream)))
     return H
@@ -292,7 +308,7 @@ def attr_precond_apply(X: torch.Tensor, mode: int, M: Optional[torch.Tensor], un
         raise ValueError("M must be contiguous fp32")
     L = lib()
     need = L.attr_precond_apply_workspace_size(n, D, mode)
-    wsp, wsn = _ws(ws, X.device).get(need)
+    wsp, wsn = _ws(ws, X.device, stream).get(need, stream)
     _check(L.attr_precond_apply(X.data_ptr(), _dtype(X), n, D, ldx, mode, _ptr(M),
                                 1 if unit_normalize else 0, Y.data_ptr(), _dtype(Y), ldy, wsp, wsn,
                                 _stream(stream)))
@@ -348,7 +364,7 @@ def attr_score_topk(Q: torch.Tensor, G: torch.Tensor, k: int, top_score: torch.T
         raise ValueError("top_score / top_index must be contiguous")
     L = lib()
     need = L.attr_score_topk_workspace_size(nq, ng, D, k)
-    wsp, wsn = _ws(ws, Q.device).get(need)
+    wsp, wsn = _ws(ws, Q.device, stream).get(need, stream)
     _check(L.attr_score_topk(Q.data_ptr(), nq, ldq, G.data_ptr(), ng, ldg, _dtype(Q), D, k,
                              index_base, 1 if merge else 0, top_score.data_ptr(),
                              top_index.data_ptr(), wsp, wsn, _stream(stream)))
