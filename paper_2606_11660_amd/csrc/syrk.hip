@@ -13,7 +13,8 @@
 // longer), and only the slices that hold rows are launched.  Slice results
 // go to fp32 partial tiles and a reduce kernel adds them, in slice order,
 // into an fp64 accumulator (at 10^6 x 8192 the reduce of two chunks costs
-// ~1 ms, of four 1.9 ms).  Precision: fp32 MFMA accumulation over at most
+// ~1 ms, of four 1.9 ms); the last chunk's reduce rounds its sums straight
+// into H.  Precision: fp32 MFMA accumulation over at most
 // 32768 rows, fp64 across slices and chunks, one rounding into H at the end
 // of the call (the spectrum of H spans ~6 decades on low-rank-plus-noise
 // stores, and long fp32 accumulation visibly perturbs its small eigenvalues;
@@ -158,23 +159,65 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(double* __restrict__ p, 
   if (e < n) p[e] = 0.0;
 }
 
-// H[p][q] += h64 for p <= q; fragment-order element f of tile u maps to
-// (i, jj, r, thread) with row 128 (w/2) + 16 i + 4 (lane/16) + r and column
-// 128 (w%2) + 16 jj + lane%16.
-__global__ __launch_bounds__(256) void syrk_store_kernel(const double* __restrict__ h64, int nt,
-                                                         int64_t D, float* __restrict__ H) {
+// The last chunk's reduce and the store in one pass: for element f of tile u,
+// s = sum_j part[j][u][f] (fp64, slices in order, as syrk_reduce_kernel), t =
+// h64[u][f] + s when earlier chunks left sums in h64 (else t = s), then
+// H[p][q] = fp32(H[p][q] + t) for p <= q: one rounding into H, with the same
+// operations in the same order as a separate reduce into h64 followed by a
+// store, but without h64's fill, write and re-read on single-chunk calls.
+// Fragment-order element f of tile u maps to (i, jj, r, thread) with row
+// 128 (w/2) + 16 i + 4 (lane/16) + r and column 128 (w%2) + 16 jj + lane%16;
+// four consecutive elements per thread share the row, columns adjacent.
+__global__ __launch_bounds__(256) void syrk_reduce_store_kernel(const float* __restrict__ part, int J,
+                                                                int64_t n_e,
+                                                                const double* __restrict__ h64,
+                                                                int nt, int64_t D,
+                                                                float* __restrict__ H) {
   const int u = blockIdx.y;
+  const int64_t f0 = 4 * ((int64_t)blockIdx.x * 256 + threadIdx.x);  // 0 .. TILE_E
+  const int64_t e4 = ((int64_t)u * TILE_E + f0) / 4;
+  const f32x4* p4 = reinterpret_cast<const f32x4*>(part);
+  const int64_t n4 = n_e / 4;
+  double s[4] = {0.0, 0.0, 0.0, 0.0};
+  int j = 0;
+  for (; j + 8 <= J; j += 8) {
+    f32x4 v[8];
+#pragma unroll
+    for (int w = 0; w < 8; ++w) v[w] = __builtin_nontemporal_load(p4 + (int64_t)(j + w) * n4 + e4);
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      s[0] += (double)v[w].x;
+      s[1] += (double)v[w].y;
+      s[2] += (double)v[w].z;
+      s[3] += (double)v[w].w;
+    }
+  }
+  for (; j < J; ++j) {
+    const f32x4 v = __builtin_nontemporal_load(p4 + (int64_t)j * n4 + e4);
+    s[0] += (double)v.x;
+    s[1] += (double)v.y;
+    s[2] += (double)v.z;
+    s[3] += (double)v.w;
+  }
+  if (h64) {
+    const double* h = h64 + 4 * e4;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) s[c] = h[c] + s[c];
+  }
   int tp, tq;
   upper_tile(u, nt, tp, tq);
-  const int64_t f = (int64_t)blockIdx.x * 256 + threadIdx.x;  // 0 .. TILE_E
-  const int th = (int)(f & 255), w = th >> 6, lane = th & 63;
-  const int irj = (int)(f >> 8);
-  const int r = irj & 3, jj = (irj >> 2) & 7, i = irj >> 5;
-  const int64_t p = (int64_t)tp * GT + 128 * (w >> 1) + 16 * i + 4 * (lane >> 4) + r;
-  const int64_t q = (int64_t)tq * GT + 128 * (w & 1) + 16 * jj + (lane & 15);
-  if (p < D && q < D && p <= q) {
-    float* hp = H + p * D + q;
-    *hp = (float)((double)*hp + h64[(int64_t)u * TILE_E + f]);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int64_t f = f0 + c;
+    const int th = (int)(f & 255), w = th >> 6, lane = th & 63;
+    const int irj = (int)(f >> 8);
+    const int r = irj & 3, jj = (irj >> 2) & 7, i = irj >> 5;
+    const int64_t p = (int64_t)tp * GT + 128 * (w >> 1) + 16 * i + 4 * (lane >> 4) + r;
+    const int64_t q = (int64_t)tq * GT + 128 * (w & 1) + 16 * jj + (lane & 15);
+    if (p < D && q < D && p <= q) {
+      float* hp = H + p * D + q;
+      *hp = (float)((double)*hp + s[c]);
+    }
   }
 }
 
@@ -212,10 +255,15 @@ SyrkPlan plan_syrk(int64_t n_rows, int64_t D) {
 hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, int64_t D, float* H,
                        const SyrkPlan& P, void* part, void* h64, hipStream_t s) {
   const int64_t n_e = (int64_t)P.n_up * TILE_E;
-  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n_e + 255) / 256)), dim3(256), 0, s,
-                     (double*)h64, n_e);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  // h64 carries fp64 sums between chunks; a single-chunk call never uses it
+  const bool multi = n_rows > P.C;
+  hipError_t e;
+  if (multi) {
+    hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n_e + 255) / 256)), dim3(256), 0, s,
+                       (double*)h64, n_e);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const int per_xcd = (P.n_up + 7) / 8;  // tiles per XCD and slice
   for (int64_t r0 = 0; r0 < n_rows; r0 += P.C) {
     const int64_t rows = n_rows - r0 < P.C ? n_rows - r0 : P.C;
@@ -227,14 +275,17 @@ hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, in
     else
       hipLaunchKernelGGL((syrk_kernel<F16Tag, _Float16>), gs, dim3(256), 0, s, (const _Float16*)X,
                          ldx, n_rows, r0, D, P.nt, P.n_up, Jc, per_xcd, P.Cs, (float*)part);
-    hipLaunchKernelGGL(syrk_reduce_kernel, dim3((unsigned)((n_e / 4 + 255) / 256)), dim3(256), 0, s,
-                       (const float*)part, Jc, n_e, (double*)h64);
+    if (r0 + P.C < n_rows)
+      hipLaunchKernelGGL(syrk_reduce_kernel, dim3((unsigned)((n_e / 4 + 255) / 256)), dim3(256), 0, s,
+                         (const float*)part, Jc, n_e, (double*)h64);
+    else
+      hipLaunchKernelGGL(syrk_reduce_store_kernel, dim3(TILE_E / 1024, (unsigned)P.n_up), dim3(256),
+                         0, s, (const float*)part, Jc, n_e, multi ? (const double*)h64 : nullptr,
+                         P.nt, D, H);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(syrk_store_kernel, dim3(TILE_E / 256, (unsigned)P.n_up), dim3(256), 0, s,
-                     (const double*)h64, P.nt, D, H);
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 }  // namespace attr
