@@ -324,14 +324,32 @@ __global__ __launch_bounds__(256) void colsumsq_kernel(const TX* __restrict__ X,
   for (int e = 0; e < 8; ++e) part[panel * D + c0 + e] = acc[e];
 }
 
+// h_j += sum over panels of part[p][j]: a workgroup takes 64 columns, wave w
+// sums panels p = w (mod 4) in increasing order (each panel read as 512
+// contiguous bytes per wave), and the four sums are added in wave order:
+// a fixed order, so the result is deterministic.
 __global__ __launch_bounds__(256) void colsumsq_final_kernel(const double* __restrict__ part,
                                                              int64_t n_panels, int64_t D,
                                                              float* __restrict__ H) {
-  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (j >= D) return;
+  __shared__ double red[4][64];
+  const int w = threadIdx.x >> 6, c = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 64 + c;
   double s = 0.0;
-  for (int64_t p = 0; p < n_panels; ++p) s += part[p * D + j];
-  H[j] = (float)((double)H[j] + s);
+  if (j < D) {
+    int64_t p = w;
+    for (; p + 12 < n_panels; p += 16) {
+      const double v0 = part[p * D + j], v1 = part[(p + 4) * D + j];
+      const double v2 = part[(p + 8) * D + j], v3 = part[(p + 12) * D + j];
+      s += v0;
+      s += v1;
+      s += v2;
+      s += v3;
+    }
+    for (; p < n_panels; p += 4) s += part[p * D + j];
+  }
+  red[w][c] = s;
+  __syncthreads();
+  if (w == 0 && j < D) H[j] = (float)((double)H[j] + (((red[0][c] + red[1][c]) + red[2][c]) + red[3][c]));
 }
 
 }  // namespace
@@ -372,7 +390,7 @@ hipError_t launch_colsumsq(int x_dtype, const void* X, int64_t ldx, int64_t n_ro
     hipLaunchKernelGGL(colsumsq_kernel<_Float16>, grid, block, 0, s, (const _Float16*)X, ldx, n_rows, D, rpp, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 g2((unsigned)((D + 255) / 256));
+  dim3 g2((unsigned)((D + 63) / 64));
   hipLaunchKernelGGL(colsumsq_final_kernel, g2, block, 0, s, (const double*)part, (int64_t)panels, D, H);
   return hipGetLastError();
 }
