@@ -96,6 +96,45 @@ def _measured_traffic(key="traffic_bytes_per_call"):
         return None
 
 
+def _pipeline_events(stream2):
+    """Events ordering the two row buffers of run_pipeline (both start free)."""
+    import torch
+    proj_done = [torch.cuda.Event() for _ in range(2)]
+    norm_done = [torch.cuda.Event() for _ in range(2)]
+    for e in norm_done:
+        e.record(stream2)
+    return proj_done, norm_done
+
+
+def run_pipeline(mods, k, B, T, rows, store, Qrows, topk, top_s, top_i, i0, n, stream, stream2,
+                 ws_p, ws_a, ws_s, proj_done, norm_done, ev=None):
+    """Steps i0 .. i0 + n - 1 of the store build: projection of the batch (on
+    `stream`) -> unit norm into store slot i (on `stream2`) -> top-k merge of
+    the slot against the queries (on `stream2`; step 0 starts the lists).
+    Two fp32 row buffers let the projection of batch i + 1 run while batch i
+    is normalised and scored: the projection into buffer b waits for the norm
+    that last read b, the norm waits for its projection.  ev[i - i0] (optional)
+    brackets step i's projection on `stream`."""
+    import paper_2606_11660_amd as P
+    n_slots = store.shape[0] // B
+    for i in range(i0, i0 + n):
+        b = i % 2
+        slot_i = i % n_slots
+        slot = store[slot_i * B:(slot_i + 1) * B]
+        stream.wait_event(norm_done[b])
+        if ev is not None:
+            ev[i - i0][0].record(stream)
+        P.attr_project(mods, k, B, T, rows[b], ws=ws_p, stream=stream)
+        if ev is not None:
+            ev[i - i0][1].record(stream)
+        proj_done[b].record(stream)
+        stream2.wait_event(proj_done[b])
+        P.attr_precond_apply(rows[b], P.PRECOND_NONE, None, True, slot, ws=ws_a, stream=stream2)
+        norm_done[b].record(stream2)
+        P.attr_score_topk(Qrows, slot, topk, top_s, top_i, index_base=slot_i * B, merge=i > 0,
+                          ws=ws_s, stream=stream2)
+
+
 def _timeit(fn, stream, reps):
     import torch
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -435,33 +474,11 @@ def main():
         P.attr_precond_apply(rows32, P.PRECOND_NONE, None, True, Qrows[:B], ws=ws_a, stream=stream)
     stream.synchronize()
 
-    # A step is projection (on `stream`) -> unit norm into the store slot ->
-    # top-k merge against the queries (both on `stream2`).  Two fp32 row
-    # buffers let the projection of batch i + 1 run while batch i is
-    # normalised and scored: the projection into buffer b waits for the norm
-    # that last read b, the norm waits for its projection.
-    proj_done = [torch.cuda.Event() for _ in range(2)]
-    norm_done = [torch.cuda.Event() for _ in range(2)]
-    for e in norm_done:
-        e.record(stream2)
+    proj_done, norm_done = _pipeline_events(stream2)
 
     def steps(i0, n, ev=None):
-        for i in range(i0, i0 + n):
-            b = i % 2
-            slot_i = i % (n_store // B)
-            slot = store[slot_i * B:(slot_i + 1) * B]
-            stream.wait_event(norm_done[b])
-            if ev is not None:
-                ev[i - i0][0].record(stream)
-            P.attr_project(mods, k, B, T, rows32b[b], ws=ws_p, stream=stream)
-            if ev is not None:
-                ev[i - i0][1].record(stream)
-            proj_done[b].record(stream)
-            stream2.wait_event(proj_done[b])
-            P.attr_precond_apply(rows32b[b], P.PRECOND_NONE, None, True, slot, ws=ws_a, stream=stream2)
-            norm_done[b].record(stream2)
-            P.attr_score_topk(Qrows, slot, wl.topk, top_s, top_i, index_base=slot_i * B,
-                              merge=i > 0, ws=ws_s, stream=stream2)
+        run_pipeline(mods, k, B, T, rows32b, store, Qrows, wl.topk, top_s, top_i, i0, n,
+                     stream, stream2, ws_p, ws_a, ws_s, proj_done, norm_done, ev)
 
     steps(0, args.warmup)
     stream.synchronize()
@@ -471,8 +488,6 @@ def main():
     # ---------------- timed region ----------------
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
-    for e in norm_done:
-        e.record(stream2)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     # the timed steps fill store slots 0 .. steps - 1 and restart the merge

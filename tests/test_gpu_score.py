@@ -490,3 +490,45 @@ def test_gemm_plan_running_bound(order):
     else:
         assert host(ti)[5, 0] == ng - 7
         assert (host(ti)[sample][:, 1:] < chunk).all()
+
+
+def test_bench_two_stream_step_matches_one_stream():
+    """The bench step pipelines over two streams (projection of batch i + 1
+    while batch i is normalised and scored; two fp32 row buffers ordered by
+    events).  Every call is deterministic, so the store rows and the running
+    top-k after 5 pipelined steps equal, bitwise, the same calls issued one
+    after another on one stream."""
+    import bench
+    say("case: two-stream bench step vs one stream, 5 steps")
+    rng = np.random.default_rng(91)
+    k, B, T, steps, topk = 16, 8, 96, 5, 7
+    shapes = [(64, 192), (128, 64), (64, 128)]
+    D = len(shapes) * k * k
+    mods = []
+    for m, (d_in, d_out) in enumerate(shapes):
+        a = torch.from_numpy(synth.to_bf16_bits(rng.standard_normal((B * T, d_in))).view(np.int16)).view(torch.bfloat16).cuda()
+        g = torch.from_numpy(synth.to_bf16_bits(rng.standard_normal((B * T, d_out))).view(np.int16)).view(torch.bfloat16).cuda()
+        R = torch.from_numpy(synth.to_bf16_bits(rng.standard_normal((d_out, k)) / 4).view(np.int16)).view(torch.bfloat16).cuda()
+        S = torch.from_numpy(synth.to_bf16_bits(rng.standard_normal((d_in, k)) / 4).view(np.int16)).view(torch.bfloat16).cuda()
+        mods.append(P.Module(a, g, R, S, m * k * k))
+    Qrows = torch.from_numpy(rng.standard_normal((6, D)).astype(np.float16)).cuda()
+    results = []
+    for two in (True, False):
+        s1 = torch.cuda.Stream()
+        s2 = torch.cuda.Stream() if two else s1
+        store = torch.full((steps * B, D), float("nan"), dtype=torch.float16, device="cuda")
+        rows = [torch.empty((B, D), dtype=torch.float32, device="cuda") for _ in range(2)]
+        top_s = torch.empty((6, topk), dtype=torch.float32, device="cuda")
+        top_i = torch.empty((6, topk), dtype=torch.int64, device="cuda")
+        ws = [P.Workspace("cuda") for _ in range(3)]
+        pd, nd = bench._pipeline_events(s2)
+        bench.run_pipeline(mods, k, B, T, rows, store, Qrows, topk, top_s, top_i, 0, steps, s1, s2,
+                           ws[0], ws[1], ws[2], pd, nd)
+        s1.synchronize()
+        s2.synchronize()
+        results.append((host(store), host(top_s), host(top_i)))
+    (st2, ts2, ti2), (st1, ts1, ti1) = results
+    assert np.isfinite(st2).all()
+    assert np.array_equal(st2.view(np.uint16), st1.view(np.uint16))
+    assert np.array_equal(ts2, ts1) and np.array_equal(ti2, ti1)
+    assert (ti2 >= 0).all() and (ti2 < steps * B).all()
