@@ -424,8 +424,9 @@ def main():
                     help="only run one row of the path once, for counter runs")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the store shards by rows; see the design notes). Run with --gpus 1.",
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(examples and store rows would shard across GPUs, with a top-k merge of "
+              "the per-GPU lists). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
