@@ -298,8 +298,11 @@ def scores(Q: np.ndarray, G: np.ndarray) -> np.ndarray:
 
 def _select(sc: np.ndarray, idx: np.ndarray, k: int) -> Tuple[np.ndarray, np.ndarray]:
     """The k best of one query's candidates ordered by (score desc, index
-    asc); NaN is never selected; missing slots are (-inf, -1)."""
-    ok = ~np.isnan(sc)
+    asc).  NaN and -inf scores are never selected (reading: a candidate
+    with no finite lower bound ranks below every slot's padding value, so
+    it cannot be told apart from an empty slot); +inf ranks first.  Missing
+    slots are (-inf, -1)."""
+    ok = ~np.isnan(sc) & ~np.isneginf(sc)
     sc, idx = sc[ok], idx[ok]
     order = np.lexsort((idx, -sc))        # primary -score, secondary index
     sc, idx = sc[order][:k], idx[order][:k]

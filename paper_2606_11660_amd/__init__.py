@@ -8,9 +8,10 @@ the library's HIP kernels; PyTorch only provides device memory and streams.
 The library must have been built (``python -m paper_2606_11660_amd.build``);
 importing this package without it raises, there is no fallback path.
 
-The one host-side step of the method is ``finalize_full`` / ``finalize_diag``:
-turning the accumulated second moment into H^{-1/2} (an fp64 eigendecomposition
-done once per store, outside the per-row hot path).
+Every wrapper checks the tensors it is given against the sizes it passes
+(shapes, dtypes, devices) and raises ``ValueError`` before calling the
+library, which sees only pointers.  The one host step of the method, turning
+the accumulated second moment into H^{-1/2}, lives in ``finalize``.
 """
 from __future__ import annotations
 
@@ -18,7 +19,6 @@ import ctypes
 import os
 from typing import Dict, Iterable, List, Optional, Sequence, Tuple
 
-import numpy as np
 import torch
 
 __all__ = [
@@ -27,7 +27,7 @@ __all__ = [
     "attr_precond_accumulate",
     "attr_precond_apply", "attr_score_topk", "attr_project_workspace_size",
     "attr_precond_accumulate_workspace_size", "attr_precond_apply_workspace_size",
-    "attr_score_topk_workspace_size", "finalize_diag", "finalize_full", "Workspace",
+    "attr_score_topk_workspace_size", "Workspace",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -135,6 +135,25 @@ def _rows(t: torch.Tensor) -> Tuple[int, int, int]:
     return rows, width, ld
 
 
+def _same_gpu(*tensors: Optional[torch.Tensor]) -> None:
+    """Every given tensor lives on one GPU (the library takes raw pointers)."""
+    ts = [t for t in tensors if t is not None]
+    if not ts:
+        return
+    d = ts[0].device
+    for t in ts:
+        if t.device.type != "cuda" or t.device != d:
+            raise ValueError("every tensor must live on the same GPU device")
+
+
+def _vector(t: Optional[torch.Tensor], n: int, dtype, name: str) -> None:
+    """t is None or a contiguous `dtype` tensor with at least n elements."""
+    if t is None:
+        return
+    if t.dtype != dtype or not t.is_contiguous() or t.numel() < n:
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of at least {n} elements")
+
+
 def _torch_stream(stream):
     if stream is None:
         return torch.cuda.current_stream()
@@ -185,10 +204,11 @@ class Module:
     """One linear module's inputs for ``attr_project``.
 
     a: [..., d_in] activations, g: [..., d_out] output gradients (token rows,
-    last dim contiguous); R: [d_out, k], S: [d_in, k] contiguous; out_col:
-    first column of the module's k*k block in the output row.  v_out [d_out]
-    and v_in [d_in] (fp32, optional, both or neither): the factored
-    (Adafactor) second moment that normalises the gradient before projection.
+    last dim contiguous); R: [d_out, k], S: [d_in, k] contiguous, same dtype
+    as a and g; out_col: first column of the module's k*k block in the output
+    row.  v_out [d_out] and v_in [d_in] (fp32, optional, both or neither): the
+    factored (Adafactor) second moment that normalises the gradient before
+    projection.
     """
 
     def __init__(self, a: torch.Tensor, g: torch.Tensor, R: torch.Tensor, S: torch.Tensor,
@@ -197,26 +217,60 @@ class Module:
         self.a, self.g, self.R, self.S, self.out_col = a, g, R, S, int(out_col)
         self.v_out, self.v_in = v_out, v_in
 
+    def tensors(self):
+        return (self.a, self.g, self.R, self.S, self.v_out, self.v_in)
+
     def c(self) -> _CModule:
         _, d_in, lda = _rows(self.a)
         _, d_out, ldg = _rows(self.g)
         if not (self.R.is_contiguous() and self.S.is_contiguous()):
             raise ValueError("R and S must be contiguous")
-        vo = vi = None
         for v, n, name in ((self.v_out, d_out, "v_out"), (self.v_in, d_in, "v_in")):
             if v is not None and (v.dtype != torch.float32 or not v.is_contiguous() or v.numel() != n):
                 raise ValueError(f"{name} must be a contiguous fp32 vector of {n} elements")
-        if self.v_out is not None:
-            vo = self.v_out.data_ptr()
-        if self.v_in is not None:
-            vi = self.v_in.data_ptr()
         return _CModule(self.a.data_ptr(), self.g.data_ptr(), self.R.data_ptr(), self.S.data_ptr(),
-                        lda, ldg, d_in, d_out, self.out_col, vo, vi)
+                        lda, ldg, d_in, d_out, self.out_col, _ptr(self.v_out), _ptr(self.v_in))
 
 
 def _cmods(mods: Sequence[Module]):
     arr = (_CModule * len(mods))(*[m.c() for m in mods])
     return arr
+
+
+def _check_modules(mods: Sequence[Module], k: int, n_examples: int, T: int,
+                   row_offset: Optional[torch.Tensor], length: Optional[torch.Tensor],
+                   out: torch.Tensor, out_rows_needed: int) -> int:
+    """Validate a projection call's tensors against its sizes; returns the
+    input dtype code."""
+    if not mods:
+        raise ValueError("need at least one module")
+    dt = mods[0].a.dtype
+    if dt not in (torch.float32, torch.bfloat16):
+        raise ValueError("token rows must be fp32 or bf16")
+    if out.dtype != torch.float32 or out.dim() != 2 or out.stride(1) != 1:
+        raise ValueError("out must be fp32 [rows, ldo] with contiguous rows")
+    if out.shape[0] < out_rows_needed:
+        raise ValueError(f"out has {out.shape[0]} rows, the call writes {out_rows_needed}")
+    if n_examples < 0 or T < 1:
+        raise ValueError("n_examples must be >= 0 and T >= 1")
+    _vector(row_offset, n_examples, torch.int64, "row_offset")
+    _vector(length, n_examples, torch.int32, "length")
+    for j, m in enumerate(mods):
+        for name, t in (("a", m.a), ("g", m.g), ("R", m.R), ("S", m.S)):
+            if t.dtype != dt:
+                raise ValueError(f"module {j}: {name} is {t.dtype}, module 0's a is {dt}")
+        na, d_in, _ = _rows(m.a)
+        ng, d_out, _ = _rows(m.g)
+        if tuple(m.R.shape) != (d_out, k) or tuple(m.S.shape) != (d_in, k):
+            raise ValueError(f"module {j}: R must be [{d_out}, {k}] and S [{d_in}, {k}]")
+        if m.out_col < 0 or m.out_col + k * k > out.shape[1]:
+            raise ValueError(f"module {j}: columns [{m.out_col}, {m.out_col + k * k}) exceed "
+                             f"out's width {out.shape[1]}")
+        if row_offset is None and min(na, ng) < n_examples * T:
+            raise ValueError(f"module {j}: a/g hold {min(na, ng)} rows, {n_examples} examples "
+                             f"of {T} tokens need {n_examples * T}")
+    _same_gpu(out, row_offset, length, *[t for m in mods for t in m.tensors()])
+    return _dtype(mods[0].a)
 
 
 def attr_project_workspace_size(mods: Sequence[Module], in_dtype: int, n_examples: int, T: int,
@@ -228,20 +282,18 @@ def attr_project(mods: Sequence[Module], k: int, n_examples: int, T: int,
                  out: torch.Tensor, row_offset: Optional[torch.Tensor] = None,
                  length: Optional[torch.Tensor] = None, ws: Optional[Workspace] = None,
                  stream=None) -> torch.Tensor:
-    """P_{i,m} = sum_{t < len_i} (R^T g_t)(S^T a_t)^T into out[i, out_col:out_col+k*k]."""
-    if not mods:
-        raise ValueError("need at least one module")
-    in_dtype = _dtype(mods[0].a)
+    """P_{i,m} = sum_{t < len_i} (R^T g_t)(S^T a_t)^T into out[i, out_col:out_col+k*k].
+
+    Without row_offset, example i's tokens are rows i*T .. i*T + T - 1 of every
+    a and g; with it (int64 [n_examples], device) they start at row_offset[i]
+    and the caller keeps every valid token inside a and g (device values
+    cannot be checked here).  length: int32 [n_examples] on the device,
+    clamped to [0, T] by the library."""
+    in_dtype = _check_modules(mods, k, n_examples, T, row_offset, length, out, n_examples)
     cm = _cmods(mods)
     L = lib()
-    if out.dtype != torch.float32 or out.dim() != 2 or out.stride(1) != 1:
-        raise ValueError("out must be fp32 [n, ldo] with contiguous rows")
     need = L.attr_project_workspace_size(cm, len(mods), in_dtype, n_examples, T, k)
     wsp, wsn = _ws(ws, out.device, stream).get(need, stream)
-    if row_offset is not None and (row_offset.dtype != torch.int64 or not row_offset.is_contiguous()):
-        raise ValueError("row_offset must be contiguous int64")
-    if length is not None and (length.dtype != torch.int32 or not length.is_contiguous()):
-        raise ValueError("length must be contiguous int32")
     _check(L.attr_project(cm, len(mods), in_dtype, k, n_examples, T, _ptr(row_offset), _ptr(length),
                           out.data_ptr(), out.stride(0), wsp, wsn, _stream(stream)))
     return out
@@ -251,20 +303,13 @@ def attr_project_tokens(mods: Sequence[Module], k: int, n_examples: int, T: int,
                         out: torch.Tensor, row_offset: Optional[torch.Tensor] = None,
                         length: Optional[torch.Tensor] = None, ws: Optional[Workspace] = None,
                         stream=None) -> torch.Tensor:
-    """Per-token blocks (R^T g_t)(S^T a_t)^T into out[token row, out_col:out_col+k*k]."""
-    if not mods:
-        raise ValueError("need at least one module")
-    in_dtype = _dtype(mods[0].a)
+    """Per-token blocks (R^T g_t)(S^T a_t)^T into out[token row, out_col:out_col+k*k];
+    rows at or past out.shape[0] are not written."""
+    in_dtype = _check_modules(mods, k, n_examples, T, row_offset, length, out, 0)
     cm = _cmods(mods)
     L = lib()
-    if out.dtype != torch.float32 or out.dim() != 2 or out.stride(1) != 1:
-        raise ValueError("out must be fp32 [rows, ldo] with contiguous rows")
     need = L.attr_project_workspace_size(cm, len(mods), in_dtype, n_examples, T, k)
     wsp, wsn = _ws(ws, out.device, stream).get(need, stream)
-    if row_offset is not None and (row_offset.dtype != torch.int64 or not row_offset.is_contiguous()):
-        raise ValueError("row_offset must be contiguous int64")
-    if length is not None and (length.dtype != torch.int32 or not length.is_contiguous()):
-        raise ValueError("length must be contiguous int32")
     _check(L.attr_project_tokens(cm, len(mods), in_dtype, k, n_examples, T, _ptr(row_offset),
                                  _ptr(length), out.data_ptr(), out.stride(0), out.shape[0], wsp, wsn,
                                  _stream(stream)))
@@ -274,6 +319,19 @@ def attr_project_tokens(mods: Sequence[Module], k: int, n_examples: int, T: int,
 # ----------------------------------------------------------------------------
 # (2) preconditioning
 # ----------------------------------------------------------------------------
+def _check_precond_matrix(t: Optional[torch.Tensor], mode: int, D: int, name: str) -> None:
+    """DIAG: fp32 [D]; FULL: fp32 [D, D], contiguous."""
+    if mode == PRECOND_NONE:
+        if t is not None:
+            raise ValueError(f"{name} must be None without a preconditioner")
+        return
+    want = (D,) if mode == PRECOND_DIAG else (D, D) if mode == PRECOND_FULL else None
+    if want is None:
+        raise ValueError(f"unknown preconditioner mode {mode}")
+    if t is None or t.dtype != torch.float32 or not t.is_contiguous() or tuple(t.shape) != want:
+        raise ValueError(f"{name} must be a contiguous fp32 tensor of shape {list(want)}")
+
+
 def attr_precond_accumulate_workspace_size(n_rows: int, D: int, x_dtype: int, mode: int) -> int:
     return int(lib().attr_precond_accumulate_workspace_size(n_rows, D, x_dtype, mode))
 
@@ -283,8 +341,10 @@ def attr_precond_accumulate(X: torch.Tensor, mode: int, H: torch.Tensor,
     """H += diag(X^T X) (DIAG, H [D]) or the upper triangle of X^T X (FULL, H [D, D])."""
     n, D, ldx = _rows(X)
     xd = _dtype(X)
-    if H.dtype != torch.float32 or not H.is_contiguous():
-        raise ValueError("H must be contiguous fp32")
+    if mode not in (PRECOND_DIAG, PRECOND_FULL):
+        raise ValueError("attr_precond_accumulate takes PRECOND_DIAG or PRECOND_FULL")
+    _check_precond_matrix(H, mode, D, "H")
+    _same_gpu(X, H)
     L = lib()
     need = L.attr_precond_accumulate_workspace_size(n, D, xd, mode)
     wsp, wsn = _ws(ws, X.device, stream).get(need, stream)
@@ -304,8 +364,8 @@ def attr_precond_apply(X: torch.Tensor, mode: int, M: Optional[torch.Tensor], un
     ny, Dy, ldy = _rows(Y)
     if (ny, Dy) != (n, D):
         raise ValueError("X and Y shapes differ")
-    if M is not None and (M.dtype != torch.float32 or not M.is_contiguous()):
-        raise ValueError("M must be contiguous fp32")
+    _check_precond_matrix(M, mode, D, "M")
+    _same_gpu(X, Y, M)
     L = lib()
     need = L.attr_precond_apply_workspace_size(n, D, mode)
     wsp, wsn = _ws(ws, X.device, stream).get(need, stream)
@@ -313,32 +373,6 @@ def attr_precond_apply(X: torch.Tensor, mode: int, M: Optional[torch.Tensor], un
                                 1 if unit_normalize else 0, Y.data_ptr(), _dtype(Y), ldy, wsp, wsn,
                                 _stream(stream)))
     return Y
-
-
-def finalize_diag(h: torch.Tensor, n_rows: int) -> torch.Tensor:
-    """m = (h / N)^{-1/2} (0 where h is 0), computed in fp64 on the host."""
-    hn = h.detach().double().cpu().numpy() / float(n_rows)
-    m = np.zeros_like(hn)
-    pos = hn > 0
-    m[pos] = 1.0 / np.sqrt(hn[pos])
-    return torch.from_numpy(m.astype(np.float32)).to(h.device)
-
-
-def finalize_full(H: torch.Tensor, n_rows: int) -> torch.Tensor:
-    """M = (H / N)^{-1/2} from the upper triangle of H, in fp64 on the host.
-
-    The eigendecomposition of the symmetrised H / N runs once per store
-    (LAPACK syevd through numpy); eigenvalues at or below
-    lam_max * D * eps64 are dropped (pseudo-inverse square root).
-    """
-    Hu = np.triu(H.detach().double().cpu().numpy())
-    Hs = (Hu + np.triu(Hu, 1).T) / float(n_rows)
-    lam, V = np.linalg.eigh(Hs)
-    floor = max(lam.max(), 0.0) * Hs.shape[0] * np.finfo(np.float64).eps
-    f = np.where(lam > floor, 1.0 / np.sqrt(np.maximum(lam, floor)), 0.0)
-    M = (V * f) @ V.T
-    M = 0.5 * (M + M.T)
-    return torch.from_numpy(M.astype(np.float32)).to(H.device)
 
 
 # ----------------------------------------------------------------------------
@@ -362,6 +396,9 @@ def attr_score_topk(Q: torch.Tensor, G: torch.Tensor, k: int, top_score: torch.T
         raise ValueError("top_score must be fp32 and top_index int64")
     if not (top_score.is_contiguous() and top_index.is_contiguous()):
         raise ValueError("top_score / top_index must be contiguous")
+    if tuple(top_score.shape) != (nq, k) or tuple(top_index.shape) != (nq, k):
+        raise ValueError(f"top_score and top_index must be [{nq}, {k}]")
+    _same_gpu(Q, G, top_score, top_index)
     L = lib()
     need = L.attr_score_topk_workspace_size(nq, ng, D, k)
     wsp, wsn = _ws(ws, Q.device, stream).get(need, stream)

@@ -16,6 +16,7 @@
 #include <vector>
 
 #include "kernels.h"
+#include "syrk_plan.h"
 
 namespace {
 
@@ -314,7 +315,7 @@ size_t attr_precond_accumulate_workspace_size(int64_t n_rows, int64_t D, attr_dt
   if (mode == ATTR_PRECOND_DIAG)
     return align_up((size_t)attr::colsumsq_panels(n_rows, D) * (size_t)D * sizeof(double));
   if (mode == ATTR_PRECOND_FULL) {
-    const attr::SyrkPlan P = attr::plan_syrk(n_rows, D);
+    const attr::SyrkPlan P = attr::plan_syrk(n_rows, D, 0);  // any stride's plan fits in it
     return align_up(P.part_bytes) + align_up(P.h64_bytes);
   }
   return 0;
@@ -343,7 +344,8 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
     if (full && D % 64) return fail(ATTR_ERR_ALIGNMENT, "FULL needs D a multiple of 64");
     if (full && D > 32768) return fail(ATTR_ERR_UNSUPPORTED, "FULL needs D <= 32768");
     if (full && ldx > 65536)
-      return fail(ATTR_ERR_UNSUPPORTED, "FULL needs ldx <= 65536 (16384 rows must span < 2 GiB)");
+      return fail(ATTR_ERR_UNSUPPORTED, "FULL needs ldx <= 65536 (64-row stages of K-slices of at "
+                  "least 16384 rows, each slice spanning at most 2 GiB)");
     if (overlap(span_of(X, n_rows, D, ldx, eb), span_of(H, full ? D : 1, D, D, 4)))
       return fail(ATTR_ERR_INVALID_ARG, "X and H overlap");
     if (n_rows == 0) return ATTR_OK;
@@ -355,7 +357,10 @@ attr_status attr_precond_accumulate(const void* X, attr_dtype x_dtype, int64_t n
     if (n_rows > (1ll << 40)) return fail(ATTR_ERR_UNSUPPORTED, "n_rows too large");
     hipError_t e;
     if (full) {
-      const attr::SyrkPlan P = attr::plan_syrk(n_rows, D);
+      const attr::SyrkPlan P = attr::plan_syrk(n_rows, D, ldx);
+      if (P.Cs * ldx * 2 > (1ll << 31))
+        return fail(ATTR_ERR_UNSUPPORTED, "internal: SYRK slice of %lld rows spans more than 2 GiB",
+                    (long long)P.Cs);
       char* part = static_cast<char*>(ws);
       char* h64 = part + align_up(P.part_bytes);
       e = attr::launch_syrk(x_dtype == ATTR_BF16, X, ldx, n_rows, D, H, P, part, h64,
@@ -426,7 +431,7 @@ attr_status attr_precond_apply(const void* X, attr_dtype x_dtype, int64_t n_rows
     }
     hipError_t e = attr::launch_rowscale((int)x_dtype, (int)y_dtype, X, ldx, n_rows, D,
                                          mode == ATTR_PRECOND_DIAG ? M : nullptr, unit_normalize ? 1 : 0,
-                                         nullptr, 0, Y, ldy, static_cast<hipStream_t>(stream));
+                                         nullptr, nullptr, 0, Y, ldy, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return device_fail(e, "attr_precond_apply launch");
     return ATTR_OK;
   } catch (...) {

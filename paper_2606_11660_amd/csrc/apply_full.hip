@@ -12,7 +12,15 @@
 // K loop runs over A_hi and then over A_lo into the same fp32 accumulators;
 // the epilogue applies 2^-s, writes Y and per-row partial sums of squares
 // (from the fp32 values), which the row-scale kernel turns into the
-// unit-norm scale in a second pass.
+// unit-norm scale in a second pass.  With unit normalisation into an fp16
+// Y, each (row, 128-column segment) is written as y 2^-e with e chosen so
+// that the segment's largest magnitude lands in [2^13, 2^14): the
+// un-normalised rows of a whitened store are not bounded (H^{-1/2}
+// amplifies the directions of the smallest kept eigenvalues by up to
+// ~10^4), so y itself may exceed fp16's range, while the unit row never
+// does.  e goes to the workspace beside the partial sums and the second
+// pass multiplies it back into the row scale; for rows within fp16's normal
+// range the results are the same bits as an unscaled intermediate.
 #include "common.h"
 #include "gemm.h"
 #include "kernels.h"
@@ -71,7 +79,7 @@ __global__ __launch_bounds__(256) void apply_full_kernel(
     const _Float16* __restrict__ X, int64_t n_rows, int64_t ldx, int64_t D,
     const _Float16* __restrict__ Mhi, const _Float16* __restrict__ Mlo,
     const unsigned int* __restrict__ maxbits, YT* __restrict__ Y, int64_t ldy,
-    float* __restrict__ rowss, int n_ss, int n_tn) {
+    float* __restrict__ rowss, int8_t* __restrict__ rowexp, int n_ss, int n_tn) {
   __shared__ GemmSmem sm;
   const int tn = (int)(blockIdx.x % (uint32_t)n_tn);
   const int64_t tm = blockIdx.x / (uint32_t)n_tn;
@@ -95,23 +103,39 @@ __global__ __launch_bounds__(256) void apply_full_kernel(
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = GemmCore<F16Tag>::row_of(i, r);
-      float ss = 0.f;
+      float v[8];
+      float ss = 0.f, mx = 0.f;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int col = GemmCore<F16Tag>::col_of(j);
-        const float v = core.acc[i][j][r] * unscale;
-        if (row < nr && col < nc) {
-          store_y<YT>(Y + (r0 + row) * ldy + c0 + col, v);
-          ss += v * v;
-        }
+        v[j] = row < nr && col < nc ? core.acc[i][j][r] * unscale : 0.f;
+        ss += v[j] * v[j];
+        mx = fmaxf(mx, fabsf(v[j]));
       }
-      // reduce over the 16 lanes that share this row
-      ss += __shfl_xor(ss, 1, kWave);
-      ss += __shfl_xor(ss, 2, kWave);
-      ss += __shfl_xor(ss, 4, kWave);
-      ss += __shfl_xor(ss, 8, kWave);
-      if (rowss && (lane & 15) == 0 && row < nr)
-        rowss[(r0 + row) * n_ss + 2 * tn + (wave & 1)] = ss;
+      // reduce over the 16 lanes that share this row (128 columns)
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        ss += __shfl_xor(ss, o, kWave);
+        mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+      }
+      int e = 0;
+      if (rowexp && mx > 0.f && mx <= 3.4e38f) {
+        int ex;
+        frexpf(mx, &ex);  // mx = f 2^ex, f in [0.5, 1)
+        e = ex - 14;
+        e = e < -120 ? -120 : (e > 120 ? 120 : e);
+      }
+      const float down = ldexpf(1.f, -e);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int col = GemmCore<F16Tag>::col_of(j);
+        if (row < nr && col < nc) store_y<YT>(Y + (r0 + row) * ldy + c0 + col, v[j] * down);
+      }
+      if (rowss && (lane & 15) == 0 && row < nr) {
+        const int64_t at = (r0 + row) * n_ss + 2 * tn + (wave & 1);
+        rowss[at] = ss;
+        if (rowexp) rowexp[at] = (int8_t)e;
+      }
     }
 }
 
@@ -128,7 +152,13 @@ hipError_t launch_apply_full(const void* X, int64_t n_rows, int64_t ldx, int64_t
   _Float16* hi = reinterpret_cast<_Float16*>(base);
   _Float16* lo = reinterpret_cast<_Float16*>(base + mb_al);
   unsigned int* maxbits = reinterpret_cast<unsigned int*>(base + 2 * mb_al);
+  const int n_ss = apply_full_nss(D);
+  const size_t ss_bytes = ((size_t)n_rows * (size_t)n_ss * 4 + 255) / 256 * 256;
   float* rowss = unit ? reinterpret_cast<float*>(base + 2 * mb_al + 256) : nullptr;
+  // segment exponents only where the un-normalised rows pass through fp16
+  int8_t* rowexp = unit && y_dtype == 2
+                       ? reinterpret_cast<int8_t*>(base + 2 * mb_al + 256 + ss_bytes)
+                       : nullptr;
   const int64_t nm = D * D;
   hipLaunchKernelGGL(zero_word_kernel, dim3(1), dim3(1), 0, s, maxbits);
   hipLaunchKernelGGL(absmax_kernel, dim3(1024), dim3(256), 0, s, M, nm, maxbits);
@@ -138,25 +168,32 @@ hipError_t launch_apply_full(const void* X, int64_t n_rows, int64_t ldx, int64_t
   if (e != hipSuccess) return e;
   const int n_tn = (int)((D + GT - 1) / GT);
   const int64_t n_tm = (n_rows + GT - 1) / GT;
-  const int n_ss = apply_full_nss(D);
   dim3 grid((unsigned)(n_tm * n_tn)), block(256);
   if (y_dtype == 2)
     hipLaunchKernelGGL(apply_full_kernel<_Float16>, grid, block, 0, s, (const _Float16*)X, n_rows,
-                       ldx, D, hi, lo, (const unsigned int*)maxbits, (_Float16*)Y, ldy, rowss, n_ss,
-                       n_tn);
+                       ldx, D, hi, lo, (const unsigned int*)maxbits, (_Float16*)Y, ldy, rowss, rowexp,
+                       n_ss, n_tn);
   else
     hipLaunchKernelGGL(apply_full_kernel<float>, grid, block, 0, s, (const _Float16*)X, n_rows, ldx,
-                       D, hi, lo, (const unsigned int*)maxbits, (float*)Y, ldy, rowss, n_ss, n_tn);
+                       D, hi, lo, (const unsigned int*)maxbits, (float*)Y, ldy, rowss, nullptr, n_ss,
+                       n_tn);
   e = hipGetLastError();
   if (e != hipSuccess || !unit) return e;
-  return launch_rowscale(y_dtype, y_dtype, Y, ldy, n_rows, D, nullptr, 1, rowss, n_ss, Y, ldy, s);
+  return launch_rowscale(y_dtype, y_dtype, Y, ldy, n_rows, D, nullptr, 1, rowss, rowexp, n_ss, Y,
+                         ldy, s);
 }
 
 size_t apply_full_workspace(int64_t n_rows, int64_t D, int unit) {
   const size_t mbytes = (size_t)D * (size_t)D * 2;
   const size_t mb_al = (mbytes + 255) / 256 * 256;
   size_t total = 2 * mb_al + 256;
-  if (unit) total += ((size_t)n_rows * (size_t)apply_full_nss(D) * 4 + 255) / 256 * 256;
+  // per (row, 128-column segment): fp32 partial sum of squares and the
+  // int8 exponent of the fp16 intermediate (the latter only for fp16 Y,
+  // but the query has no dtype, so it is always counted)
+  if (unit) {
+    total += ((size_t)n_rows * (size_t)apply_full_nss(D) * 4 + 255) / 256 * 256;
+    total += ((size_t)n_rows * (size_t)apply_full_nss(D) + 255) / 256 * 256;
+  }
   return total;
 }
 

@@ -66,10 +66,13 @@ hipError_t launch_project_reduce(int nk, const ProjTab* tab, int n_slots, int n_
 // row-wise preconditioning / normalisation (NONE and DIAG)
 // ---------------------------------------------------------------------------
 // x_dtype / y_dtype: 0 = fp32, 2 = fp16 (attr_dtype values).
+// row_ss (optional): n_ss partial sums of squares per row that give the
+// norm; seg_e (optional, with row_ss): per row, the exponent e of each
+// 128-column segment of X, which holds y 2^-e (y = X 2^e is normalised).
 hipError_t launch_rowscale(int x_dtype, int y_dtype, const void* X, int64_t ldx,
                            int64_t n_rows, int64_t D, const float* m, int unit,
-                           const float* row_ss, int64_t n_ss, void* Y, int64_t ldy,
-                           hipStream_t s);
+                           const float* row_ss, const int8_t* seg_e, int64_t n_ss, void* Y,
+                           int64_t ldy, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // diagonal accumulate
@@ -112,7 +115,7 @@ struct SyrkPlan {
   int64_t C;       // rows per chunk (J * Cs)
   size_t part_bytes, h64_bytes;
 };
-SyrkPlan plan_syrk(int64_t n_rows, int64_t D);
+// plan_syrk(n_rows, D, ldx) is in syrk_plan.h (host only).
 hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, int64_t D, float* H,
                        const SyrkPlan& P, void* part, void* h64, hipStream_t s);
 

@@ -94,10 +94,13 @@ __device__ inline float row_scale(float ss, int unit) {
 
 // CH > 0: up to CH chunks of 8 elements per thread stay in registers.
 // CH == 0: any width, two passes over the row (second pass hits cache).
+// seg_e (with row_ss): X holds y 2^-e per 128-column segment, e = seg_e[r * n_ss
+// + segment]; the scale of such a segment is 2^e / ||y||.
 template <typename TX, typename TY, int CH>
 __global__ __launch_bounds__(256) void rowscale_kernel(const TX* __restrict__ X, int64_t ldx,
                                                        int64_t D, const float* __restrict__ m,
                                                        int unit, const float* __restrict__ row_ss,
+                                                       const int8_t* __restrict__ seg_e,
                                                        int64_t n_ss, TY* Y, int64_t ldy) {
   __shared__ float sh[4];
   const int64_t r = blockIdx.x;
@@ -133,8 +136,9 @@ __global__ __launch_bounds__(256) void rowscale_kernel(const TX* __restrict__ X,
     for (int j = 0; j < (CH > 0 ? CH : 1); ++j) {
       const int ch = threadIdx.x + j * 256;
       if (ch < n8) {
+        const float scj = seg_e ? ldexpf(sc, (int)seg_e[r * n_ss + (ch >> 4)]) : sc;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[j][e] *= sc;
+        for (int e = 0; e < 8; ++e) v[j][e] *= scj;
         store8<TY>(y + (int64_t)ch * 8, v[j]);
       }
     }
@@ -166,8 +170,9 @@ __global__ __launch_bounds__(256) void rowscale_kernel(const TX* __restrict__ X,
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] *= mm[e];
       }
+      const float scj = seg_e ? ldexpf(sc, (int)seg_e[r * n_ss + (ch >> 4)]) : sc;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] *= sc;
+      for (int e = 0; e < 8; ++e) v[e] *= scj;
       store8<TY>(y + (int64_t)ch * 8, v);
     }
   }
@@ -252,15 +257,16 @@ __global__ __launch_bounds__(256) void rowscale2_kernel(const TX* __restrict__ X
 
 template <typename TX, typename TY>
 hipError_t launch_rowscale_t(const void* X, int64_t ldx, int64_t n_rows, int64_t D,
-                             const float* m, int unit, const float* row_ss, int64_t n_ss,
-                             void* Y, int64_t ldy, hipStream_t s) {
+                             const float* m, int unit, const float* row_ss, const int8_t* seg_e,
+                             int64_t n_ss, void* Y, int64_t ldy, hipStream_t s) {
   dim3 grid((unsigned)n_rows), block(256);
   const int64_t n8 = D / 8;
   const TX* x = (const TX*)X;
   TY* y = (TY*)Y;
 #define ATTR_RS(CH) \
-  hipLaunchKernelGGL((rowscale_kernel<TX, TY, CH>), grid, block, 0, s, x, ldx, D, m, unit, row_ss, n_ss, y, ldy)
-  if (m && n8 <= 1024 && n_rows >= 2) {  // the scale is read once per two rows
+  hipLaunchKernelGGL((rowscale_kernel<TX, TY, CH>), grid, block, 0, s, x, ldx, D, m, unit, row_ss, \
+                     seg_e, n_ss, y, ldy)
+  if (m && !seg_e && n8 <= 1024 && n_rows >= 2) {  // the scale is read once per two rows
     dim3 g2((unsigned)((n_rows + 1) / 2));
 #define ATTR_R2(CH)                                                                        \
   hipLaunchKernelGGL((rowscale2_kernel<TX, TY, CH>), g2, block, 0, s, x, ldx, n_rows, D, m, \
@@ -356,15 +362,18 @@ __global__ __launch_bounds__(256) void colsumsq_final_kernel(const double* __res
 
 hipError_t launch_rowscale(int x_dtype, int y_dtype, const void* X, int64_t ldx,
                            int64_t n_rows, int64_t D, const float* m, int unit,
-                           const float* row_ss, int64_t n_ss, void* Y, int64_t ldy,
-                           hipStream_t s) {
+                           const float* row_ss, const int8_t* seg_e, int64_t n_ss, void* Y,
+                           int64_t ldy, hipStream_t s) {
   if (x_dtype == 0 && y_dtype == 0)
-    return launch_rowscale_t<float, float>(X, ldx, n_rows, D, m, unit, row_ss, n_ss, Y, ldy, s);
+    return launch_rowscale_t<float, float>(X, ldx, n_rows, D, m, unit, row_ss, seg_e, n_ss, Y, ldy, s);
   if (x_dtype == 0 && y_dtype == 2)
-    return launch_rowscale_t<float, _Float16>(X, ldx, n_rows, D, m, unit, row_ss, n_ss, Y, ldy, s);
+    return launch_rowscale_t<float, _Float16>(X, ldx, n_rows, D, m, unit, row_ss, seg_e, n_ss, Y, ldy,
+                                              s);
   if (x_dtype == 2 && y_dtype == 0)
-    return launch_rowscale_t<_Float16, float>(X, ldx, n_rows, D, m, unit, row_ss, n_ss, Y, ldy, s);
-  return launch_rowscale_t<_Float16, _Float16>(X, ldx, n_rows, D, m, unit, row_ss, n_ss, Y, ldy, s);
+    return launch_rowscale_t<_Float16, float>(X, ldx, n_rows, D, m, unit, row_ss, seg_e, n_ss, Y, ldy,
+                                              s);
+  return launch_rowscale_t<_Float16, _Float16>(X, ldx, n_rows, D, m, unit, row_ss, seg_e, n_ss, Y,
+                                               ldy, s);
 }
 
 int colsumsq_panels(int64_t n_rows, int64_t D) {

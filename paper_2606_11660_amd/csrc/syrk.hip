@@ -24,15 +24,12 @@
 #include "common.h"
 #include "gemm.h"
 #include "kernels.h"
+#include "syrk_plan.h"
 
 namespace attr {
 namespace {
 
-#ifndef ATTR_SYRK_CHUNK
-#define ATTR_SYRK_CHUNK 524288  // rows per SYRK launch (16 K-slices: whole rounds of 256 CUs)
-#endif
-constexpr int SYRK_CHUNK = ATTR_SYRK_CHUNK;
-constexpr int SYRK_SLICES = 16;  // K-slices per full chunk
+static_assert(kSyrkTile == GT, "the plan's tile is the GEMM core's");
 constexpr int TILE_E = GT * GT;  // elements per tile
 
 // Upper-triangle tile u -> (tp, tq), tp <= tq, row-major over tp.
@@ -222,35 +219,6 @@ __global__ __launch_bounds__(256) void syrk_reduce_store_kernel(const float* __r
 }
 
 }  // namespace
-
-SyrkPlan plan_syrk(int64_t n_rows, int64_t D) {
-  SyrkPlan P{};
-  P.nt = (int)((D + GT - 1) / GT);
-  P.n_up = P.nt * (P.nt + 1) / 2;
-  // equal chunks of at most SYRK_CHUNK rows (10^6 rows: two of 500000, each
-  // 16 slices of 31296, rather than one full chunk and a ragged one)
-  const int64_t n_chunks = n_rows > SYRK_CHUNK ? (n_rows + SYRK_CHUNK - 1) / SYRK_CHUNK : 1;
-  int64_t c = (n_rows + n_chunks - 1) / n_chunks;
-  c = (c + 63) / 64 * 64;
-  if (c < 64) c = 64;
-  // 16 K-slices, fewer for short chunks (slices of >= 8192 rows: each slice
-  // adds a partial tile to write and reduce), but enough for two workgroups
-  // per CU when the matrix has few tiles (D = 2048: 36 tiles), with slices
-  // of >= 1024 rows
-  int J = (int)(c / 8192);
-  const int fill = (512 + P.n_up - 1) / P.n_up;
-  const int Jmax_short = (int)(c / 1024);
-  if (J < fill) J = fill < Jmax_short ? fill : Jmax_short;
-  J = J < 1 ? 1 : (J > SYRK_SLICES ? SYRK_SLICES : J);
-  int64_t cs = (c + J - 1) / J;
-  cs = (cs + 63) / 64 * 64;
-  P.J = J;
-  P.Cs = cs;
-  P.C = cs * J;
-  P.part_bytes = (size_t)J * (size_t)P.n_up * TILE_E * 4;
-  P.h64_bytes = (size_t)P.n_up * TILE_E * 8;
-  return P;
-}
 
 hipError_t launch_syrk(bool bf16, const void* X, int64_t ldx, int64_t n_rows, int64_t D, float* H,
                        const SyrkPlan& P, void* part, void* h64, hipStream_t s) {

@@ -1,0 +1,45 @@
+// CPU check of the SYRK planner's arithmetic (host-only header): for row
+// strides up to the accepted maximum, every K-slice spans at most 2^31 bytes
+// (the GEMM core's past-the-end loads rely on it), the chunks cover the rows,
+// and the workspace query (no stride limit) is large enough for every
+// stride's plan.  Prints "ok" or the first violation and exits non-zero.
+#include <cstdio>
+#include <cstdlib>
+
+#include "syrk_plan.h"
+
+int main() {
+  const long long rows[] = {1, 63, 64, 1000, 8191, 8192, 16383, 16384, 24575, 100000, 262144,
+                            262145, 500000, 523264, 524288, 524289, 1000000, 1048576, 4000000,
+                            10000000};
+  const long long Ds[] = {64, 320, 2048, 8192, 32768};
+  const long long lds[] = {0, 64, 8192, 16384, 32768, 32832, 40000, 65536};
+  long long checked = 0;
+  for (long long n : rows)
+    for (long long D : Ds)
+      for (long long ldx : lds) {
+        if (ldx && ldx < D) continue;
+        const attr::SyrkPlan P = attr::plan_syrk(n, D, ldx);
+        const attr::SyrkPlan Q = attr::plan_syrk(n, D, 0);
+        const long long ld = ldx ? ldx : D;
+        const long long n_chunks = (n + P.C - 1) / P.C;
+        bool ok = P.J >= 1 && P.J <= attr::kSyrkSlices && P.Cs % 64 == 0 && P.Cs >= 64 &&
+                  P.C == P.Cs * P.J && n_chunks * P.C >= n && P.part_bytes <= Q.part_bytes &&
+                  P.h64_bytes == Q.h64_bytes;
+        if (ldx) ok = ok && P.Cs * ld * 2 <= (1ll << 31);
+        if (!ok) {
+          std::printf("violation: n=%lld D=%lld ldx=%lld -> J=%d Cs=%lld C=%lld part=%zu (query %zu)\n",
+                      n, D, ldx, P.J, (long long)P.Cs, (long long)P.C, P.part_bytes, Q.part_bytes);
+          return 1;
+        }
+        ++checked;
+      }
+  // the case that used to wrap: a full 524288-row chunk at the largest stride
+  const attr::SyrkPlan W = attr::plan_syrk(524288, 8192, 65536);
+  if (W.Cs * 65536ll * 2 > (1ll << 31)) {
+    std::printf("violation: 524288 rows at ldx 65536 give %lld-row slices\n", (long long)W.Cs);
+    return 1;
+  }
+  std::printf("ok %lld plans\n", checked);
+  return 0;
+}

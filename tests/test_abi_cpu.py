@@ -189,3 +189,24 @@ def test_build_flags_unprotected_lds_dma_loads():
     assert len(lds_dma_hazards(bad)) == 1
     assert lds_dma_hazards(good) == []
     assert lds_dma_hazards(other) == []
+
+
+def test_syrk_plan_slices_fit_their_buffer_range(tmp_path):
+    """Compile the host-only SYRK planner with g++ and check its arithmetic
+    over row counts, widths and strides up to the accepted maximum (65536):
+    no K-slice spans more than 2^31 bytes, chunks cover the rows, and the
+    workspace query covers every stride's plan."""
+    import shutil
+    import subprocess
+    gxx = shutil.which("g++")
+    if gxx is None:
+        pytest.skip("g++ not available")
+    exe = tmp_path / "syrk_plan_check"
+    src = os.path.join(ROOT, "tests", "native", "syrk_plan_check.cpp")
+    csrc = os.path.join(ROOT, "paper_2606_11660_amd", "csrc")
+    subprocess.run([gxx, "-std=c++17", "-O1", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                    f"-I{csrc}", f"-I{os.path.join(ROOT, 'include')}", src, "-o", str(exe)],
+                   check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert out.returncode == 0, out.stdout + out.stderr
+    assert out.stdout.startswith("ok")

@@ -6,6 +6,7 @@ import torch
 
 import oracle as O
 import paper_2606_11660_amd as P
+from paper_2606_11660_amd import finalize as fin
 import synth
 from tests._util import dev, host, row_rel_l2, say
 
@@ -133,7 +134,7 @@ def test_preconditioner_pipeline_lowrank():
     Xd, Qd = dev(X), dev(Qh)
     H = torch.zeros((D, D), dtype=torch.float32, device="cuda")
     P.attr_precond_accumulate(Xd, P.PRECOND_FULL, H)
-    M = P.finalize_full(H, N)
+    M = fin.finalize_full(H, N)
     Y = torch.empty((N, D), dtype=torch.float16, device="cuda")
     YQ = torch.empty((nq, D), dtype=torch.float16, device="cuda")
     P.attr_precond_apply(Xd, P.PRECOND_FULL, M, True, Y)
@@ -148,3 +149,38 @@ def test_preconditioner_pipeline_lowrank():
     say(f"store rows max rel-L2 {err.max():.2e}, queries {errq.max():.2e}, kappa {lam.max() / lam.min():.2e}")
     assert err.max() <= 2e-2 and errq.max() <= 2e-2
     assert np.abs(np.linalg.norm(host(Y)[sample].astype(np.float64), axis=1) - 1).max() <= 2e-3
+
+
+def test_full_apply_unit_rows_beyond_fp16_range():
+    """Rows whose whitened, un-normalised values exceed fp16's range (a large
+    component along the eigenvector of the smallest kept eigenvalue, which
+    H^{-1/2} amplifies most) and rows whose values sit far below fp16's
+    normal range: the unit rows written as fp16 are still finite and match
+    the oracle, on both the fp16 and the fp32 output paths."""
+    say("case: full apply, rows beyond fp16 range")
+    D, N = 512, 20000
+    F = synth.lowrank_factor(D, 64, seed=3)
+    X = synth.lowrank_rows(0, N, D=D, rank=64, chunk=8192, F=F)
+    M, lam = O.finalize_full(O.accumulate_full(X), N)
+    _, V = np.linalg.eigh(O.accumulate_full(X) / N)
+    v = V[:, 0] / np.abs(V[:, 0]).max()                 # smallest eigenvalue's direction
+    rng = np.random.default_rng(5)
+    rows = [30000.0 * v,                                 # |M x| ~ 3e5: past 65504
+            30000.0 * v + 100.0 * rng.standard_normal(D),
+            -20000.0 * v,
+            5e-7 * rng.standard_normal(D),               # |M x| < 6.1e-5: fp16 subnormals
+            X[7].astype(np.float64)]                     # an ordinary store row
+    Q = np.stack(rows).astype(np.float16)
+    Md = dev(M.astype(np.float32))
+    ref = O.precond_apply(Q, "full", M.astype(np.float32).astype(np.float64), unit_norm=True)
+    raw = O.precond_apply(Q, "full", M.astype(np.float32).astype(np.float64), unit_norm=False)
+    assert np.abs(raw[:3]).max(axis=1).min() > 65504 and np.abs(raw[3]).max() < 6.1e-5
+    for ydt in (torch.float16, torch.float32):
+        Y = torch.empty((Q.shape[0], D), dtype=ydt, device="cuda")
+        P.attr_precond_apply(dev(Q), P.PRECOND_FULL, Md, True, Y)
+        torch.cuda.synchronize()
+        got = host(Y).astype(np.float64)
+        assert np.isfinite(got).all(), f"{ydt}: non-finite unit rows"
+        err = row_rel_l2(got, ref)
+        say(f"y={ydt} max row rel-L2 {err.max():.2e}")
+        assert err.max() <= 2e-3

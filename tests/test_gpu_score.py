@@ -333,6 +333,54 @@ def test_streaming_plan_with_bound(nq, k, D, dt):
     check_topk(host(ts), host(ti), O.scores(Q, G), k, index_base=3)
 
 
+@pytest.mark.parametrize("nq,ng,D,k,n_pinf,dt", [
+    (8, 200, 256, 10, 3, np.float16),        # split-K, one selection wave per query
+    (40, 3001, 1024, 50, 3, np.float16),     # split-K, several parts + merge
+    (100, 9000, 256, 100, 3, np.float16),    # streaming
+    (20, 9000, 128, 10, 3, np.float32),      # streaming, fp32
+    (64, 300001, 64, 100, 3, np.float16),    # streaming with the prefix bound
+    (120, 300001, 64, 9, 12, np.float16),    # bound itself +inf: only +inf rows enter
+    (130, 5000, 256, 10, 3, np.float16),     # GEMM plan
+    (200, 300000, 64, 2, 3, np.float16),     # GEMM plan, running bound +inf after chunk 0
+])
+def test_infinite_and_nan_store_rows(nq, ng, D, k, n_pinf, dt):
+    """Store rows scoring +inf rank first, by index; rows scoring -inf or
+    NaN are never selected (the oracle's selection rule), on every plan."""
+    say(f"case: +-inf / NaN rows nq={nq} ng={ng} D={D} k={k} n_pinf={n_pinf} {dt.__name__}")
+    Q = synth.unit_rows(nq, D, seed=71, dtype=dt)
+    Q[:, 0] = np.abs(Q[:, 0]) + dt(0.05)         # every query positive on column 0
+    G = synth.unit_rows(ng, D, seed=72, dtype=dt)
+    rng = np.random.default_rng(73)
+    # +inf rows in distinct 64-row segments of the first 16384 rows (and one
+    # late row), -inf and NaN rows spread over the store
+    pinf = sorted(set((rng.choice(min(ng, 16384) // 64, n_pinf - 1, replace=False) * 64 + 7).tolist())
+                  | {ng - 3})
+    rest = np.setdiff1d(np.arange(ng), pinf)
+    ninf = rng.choice(rest, 4, replace=False)
+    nan = rng.choice(np.setdiff1d(rest, ninf), 3, replace=False)
+    G[pinf, 0] = np.inf
+    G[ninf, 0] = -np.inf
+    G[nan, 1] = np.nan
+    ts, ti = _topk(dev(Q), dev(G), k, index_base=5)
+    got_s, got_i = host(ts), host(ti)
+    finite = np.ones(ng, dtype=bool)
+    finite[pinf] = finite[ninf] = finite[nan] = False
+    Gf = G.copy()
+    Gf[~finite] = 0
+    sc = O.scores(Q, Gf)
+    sc[:, ~finite] = -1e30                       # never among a finite top-k
+    ref_s, ref_i = O.score_topk(Q, G, k, index_base=5)
+    npos = min(k, len(pinf))
+    # the +inf rows: exact scores and index order
+    np.testing.assert_array_equal(got_i[:, :npos], ref_i[:, :npos])
+    assert np.isposinf(got_s[:, :npos]).all() and np.isposinf(ref_s[:, :npos]).all()
+    # the rest: the top (k - npos) of the finite rows, by the usual gap rule
+    if k > npos:
+        check_topk(got_s[:, npos:], got_i[:, npos:], sc, k - npos, index_base=5)
+    bad = set((np.concatenate([ninf, nan]) + 5).tolist())
+    assert not (set(got_i.ravel().tolist()) & bad)
+
+
 def test_merge_fallback_all_ties():
     """Every store row equal and the query equal to it: all scores tie, each
     partition list holds its first k rows, and nearly every list entry ranks

@@ -45,6 +45,23 @@ def test_projection_golden_hand_worked(golden_dir):
         np.testing.assert_array_equal(P[0], np.array(d["P_flat"], dtype=np.float64))
 
 
+def test_concat_golden_module_and_flatten_order(golden_dir):
+    # Two modules, two examples, ragged lengths: the store row is module A's
+    # k x k block then module B's, each flattened with R's index first.  A
+    # module-order, axis or flatten mistake in the concatenation fails here.
+    d = _load(golden_dir, "concat_two_modules.json")
+    blocks = []
+    for m in ("A", "B"):
+        a = np.array(d[m + "_a"], dtype=np.float32)
+        g = np.array(d[m + "_g"], dtype=np.float32)
+        R = np.array(d[m + "_R"], dtype=np.float32)
+        S = np.array(d[m + "_S"], dtype=np.float32)
+        blocks.append(O.project(a, g, R, S, length=d[m + "_length"]))
+    rows = O.project_concat(blocks)
+    assert rows.shape == (2, 8)
+    np.testing.assert_array_equal(rows, np.array(d["rows"], dtype=np.float64))
+
+
 def _brute_gradient(a, g, L):
     """Per-example weight gradient summed over tokens by explicit loops over
     tokens and matrix entries (no matrix product)."""
@@ -467,3 +484,18 @@ def test_fewer_candidates_than_k_and_nan():
     s, i = O.score_topk(Q, G, 4)
     assert list(i[0]) == [1, -1, -1, -1]
     assert s[0, 0] == 2.0 and np.isneginf(s[0, 1:]).all()
+
+
+def test_infinite_scores_selection_rule():
+    # +inf ranks first (ties by index); -inf and NaN are never selected and
+    # leave (-inf, -1) padding, so a selected entry is always finite or +inf.
+    Q = np.array([[1.0, 1.0]])
+    G = np.array([[np.inf, 0.0], [1.0, 0.0], [-np.inf, 0.0], [np.nan, 0.0],
+                  [np.inf, 1.0], [-np.inf, 5.0], [0.5, 0.0]])
+    s, i = O.score_topk(Q, G, 6)
+    assert list(i[0]) == [0, 4, 1, 6, -1, -1]
+    assert list(s[0][:4]) == [np.inf, np.inf, 1.0, 0.5]
+    assert np.isneginf(s[0, 4:]).all()
+    # merging keeps the rule: a list holding only -inf candidates adds nothing
+    s2, i2 = O.merge_topk(s, i, np.array([[-np.inf, 2.0]]), np.array([[9, 10]]), 6)
+    assert list(i2[0]) == [0, 4, 10, 1, 6, -1]
