@@ -24,7 +24,8 @@
  * - The caller owns every buffer, including the workspace `ws` whose
  *   minimum size the matching *_workspace_size() function returns (0 means
  *   no workspace is needed; `ws` may then be NULL).  The library keeps no
- *   per-call state between calls and never allocates device memory.
+ *   per-call state between calls and never allocates device memory; the one
+ *   exception is the static per-GPU scratch array of attr_project_noalloc.
  * - Errors: arguments are validated on the host before anything is
  *   enqueued.  On any error the call enqueues nothing, leaves every output
  *   untouched and returns a non-zero attr_status; attr_last_error() then
@@ -46,7 +47,7 @@
 extern "C" {
 #endif
 
-#define ATTR_ABI_VERSION 2
+#define ATTR_ABI_VERSION 3
 
 typedef enum {
   ATTR_OK = 0,
@@ -147,6 +148,25 @@ attr_status attr_project_tokens(const attr_module* mods, int32_t n_mods, attr_dt
                                 const int64_t* row_offset, const int32_t* length, float* out,
                                 int64_t ldo, int64_t n_rows, void* ws, size_t ws_bytes,
                                 void* stream);
+
+/* attr_project without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops
+ * and harnesses that forbid allocation.  It computes exactly what
+ * attr_project computes (same kernels, same bits) and makes no allocating
+ * call: its scratch is a static device array of ATTR_PROJECT_NOALLOC_SCRATCH
+ * bytes, one per GPU, created when the library's code first runs on that
+ * GPU and held until the process ends.  Every call on a GPU shares that
+ * GPU's array, so calls that overlap on one GPU (different streams or host
+ * threads without ordering) race and give undefined results; order them.
+ * A call whose workspace would exceed the array (attr_project_workspace_size
+ * above ATTR_PROJECT_NOALLOC_SCRATCH) returns ATTR_ERR_WORKSPACE and
+ * enqueues nothing.  Arguments and other errors as attr_project.
+ */
+#define ATTR_PROJECT_NOALLOC_SCRATCH (64ull << 20)
+attr_status attr_project_noalloc(const attr_module* mods, int32_t n_mods, attr_dtype in_dtype,
+                                 int32_t k, int64_t n_examples, int64_t T,
+                                 const int64_t* row_offset, const int32_t* length, float* out,
+                                 int64_t ldo, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* (2a) attr_precond_accumulate: second-moment statistics of store rows.    */

@@ -23,7 +23,8 @@ import torch
 
 __all__ = [
     "AttrError", "ATTR_F32", "ATTR_BF16", "ATTR_F16", "PRECOND_NONE", "PRECOND_DIAG",
-    "PRECOND_FULL", "Module", "lib", "lib_path", "attr_project", "attr_project_tokens",
+    "PRECOND_FULL", "Module", "lib", "lib_path", "attr_project", "attr_project_noalloc",
+    "attr_project_tokens",
     "attr_precond_accumulate",
     "attr_precond_apply", "attr_score_topk", "attr_project_workspace_size",
     "attr_precond_accumulate_workspace_size", "attr_precond_apply_workspace_size",
@@ -82,6 +83,9 @@ def lib() -> ctypes.CDLL:
     L.attr_project_tokens.restype = ctypes.c_int
     L.attr_project_tokens.argtypes = [ctypes.POINTER(_CModule), i32, ctypes.c_int, i32, i64, i64, vp,
                                       vp, vp, i64, i64, vp, sz, vp]
+    L.attr_project_noalloc.restype = ctypes.c_int
+    L.attr_project_noalloc.argtypes = [ctypes.POINTER(_CModule), i32, ctypes.c_int, i32, i64, i64,
+                                       vp, vp, vp, i64, vp]
     L.attr_precond_accumulate_workspace_size.restype = sz
     L.attr_precond_accumulate_workspace_size.argtypes = [i64, i64, ctypes.c_int, ctypes.c_int]
     L.attr_precond_accumulate.restype = ctypes.c_int
@@ -296,6 +300,20 @@ def attr_project(mods: Sequence[Module], k: int, n_examples: int, T: int,
     wsp, wsn = _ws(ws, out.device, stream).get(need, stream)
     _check(L.attr_project(cm, len(mods), in_dtype, k, n_examples, T, _ptr(row_offset), _ptr(length),
                           out.data_ptr(), out.stride(0), wsp, wsn, _stream(stream)))
+    return out
+
+
+def attr_project_noalloc(mods: Sequence[Module], k: int, n_examples: int, T: int,
+                         out: torch.Tensor, row_offset: Optional[torch.Tensor] = None,
+                         length: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """attr_project without a workspace: the library's static per-GPU scratch
+    (ATTR_PROJECT_NOALLOC_SCRATCH bytes) serves as workspace, so this call
+    allocates nothing (usable under graph capture).  Calls that overlap on one
+    GPU share that scratch and must be ordered by the caller."""
+    in_dtype = _check_modules(mods, k, n_examples, T, row_offset, length, out, n_examples)
+    _check(lib().attr_project_noalloc(_cmods(mods), len(mods), in_dtype, k, n_examples, T,
+                                      _ptr(row_offset), _ptr(length), out.data_ptr(),
+                                      out.stride(0), _stream(stream)))
     return out
 
 

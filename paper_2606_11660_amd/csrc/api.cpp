@@ -307,6 +307,32 @@ attr_status attr_project_tokens(const attr_module* mods, int32_t n_mods, attr_dt
                       ws_bytes, stream, true, n_rows);
 }
 
+attr_status attr_project_noalloc(const attr_module* mods, int32_t n_mods, attr_dtype in_dtype,
+                                 int32_t k, int64_t n_examples, int64_t T,
+                                 const int64_t* row_offset, const int32_t* length, float* out,
+                                 int64_t ldo, void* stream) {
+  try {
+    g_err.clear();
+    attr_status st = project_validate(mods, n_mods, in_dtype, k, n_examples, T, out, ldo);
+    if (st != ATTR_OK) return st;
+    if (n_examples == 0) return ATTR_OK;
+    // the size check comes first: a call that cannot fit touches no device state
+    const size_t need = project_layout(mods, n_mods, dtype_bytes(in_dtype), n_examples, T, k).total;
+    if (need > attr::kProjectScratchBytes)
+      return fail(ATTR_ERR_WORKSPACE,
+                  "attr_project_noalloc: the call needs %zu bytes of scratch, the static buffer "
+                  "holds %zu; split the batch or call attr_project with a workspace",
+                  need, attr::kProjectScratchBytes);
+    void* scratch = nullptr;
+    const hipError_t e = attr::project_scratch(&scratch);
+    if (e != hipSuccess) return device_fail(e, "attr_project_noalloc: static scratch address");
+    return project_impl(mods, n_mods, in_dtype, k, n_examples, T, row_offset, length, out, ldo,
+                        scratch, attr::kProjectScratchBytes, stream, false, 0);
+  } catch (...) {
+    return fail(ATTR_ERR_INVALID_ARG, "attr_project_noalloc: host exception");
+  }
+}
+
 // ---------------------------------------------------------------------------
 size_t attr_precond_accumulate_workspace_size(int64_t n_rows, int64_t D, attr_dtype x_dtype,
                                               attr_precond mode) {

@@ -45,6 +45,11 @@ int project_chunk_tokens(int nk);
 // Bytes of packed S and R for one module.
 size_t project_packed_bytes(int64_t d_in, int64_t d_out, int k, int elem_bytes);
 
+// Static device scratch of attr_project_noalloc (per GPU, 256-byte aligned):
+// its device address on the current device, resolved once per device.
+constexpr size_t kProjectScratchBytes = (size_t)64 << 20;
+hipError_t project_scratch(void** ptr);
+
 hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab* tab,
                                char* pk_base, hipStream_t s);
 // Modules sharing their input rows (same a, lda, d_in) are projected in

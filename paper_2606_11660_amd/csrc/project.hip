@@ -22,11 +22,23 @@
 //    as one fp32 k x k partial per item; a second kernel sums the chunks of
 //    each (module, example) in chunk order into the output row
 //    (deterministic, no atomics).
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace attr {
 namespace {
+
+// Scratch of the allocation-free projection entry point: one copy per GPU,
+// held from the library's first use on that GPU until the process ends.  In
+// host code `scratch` names a host-side stand-in, never the device memory:
+// its device address comes from hipGetSymbolAddress, per device.
+static __device__ __align__(256) char scratch[kProjectScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
 
 template <bool BF16>
 struct ElemT;
@@ -444,6 +456,24 @@ __global__ __launch_bounds__(256) void project_reduce_kernel(
 }
 
 }  // namespace
+
+hipError_t project_scratch(void** ptr) {
+  *ptr = nullptr;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));  // the current device's copy
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 int project_chunk_tokens(int nk) {
   return 64 * (nk == 1 ? ATTR_PROJ_TT1 : (nk == 2 ? 2 : 1));

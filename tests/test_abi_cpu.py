@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.attr_abi_version() == 2
+    assert L.attr_abi_version() == 3
     assert L.attr_status_string(0) == b"ATTR_OK"
     assert L.attr_status_string(4) == b"ATTR_ERR_WORKSPACE"
     assert L.attr_last_error() == b""
@@ -210,3 +210,21 @@ def test_syrk_plan_slices_fit_their_buffer_range(tmp_path):
     out = subprocess.run([str(exe)], capture_output=True, text=True)
     assert out.returncode == 0, out.stdout + out.stderr
     assert out.stdout.startswith("ok")
+
+
+def test_project_noalloc_validation_and_scratch_limit(L):
+    """The allocation-free projection validates like attr_project, and a call
+    whose workspace would exceed the static scratch (64 MiB) is rejected with
+    ATTR_ERR_WORKSPACE before any device call."""
+    def call(mods, n=4, T=32, k=16, dtype=P.ATTR_BF16, ldo=256):
+        arr = (P._CModule * len(mods))(*mods)
+        return L.attr_project_noalloc(arr, len(mods), dtype, k, n, T, None, None, FAKE, ldo, None)
+    assert call([_mod()], k=24) == UNSUPPORTED
+    assert call([_mod(d_in=96)]) == ALIGN
+    assert call([_mod(out_col=1)]) == INVALID
+    assert call([_mod()], n=0) == OK                                    # nothing to do
+    # one 64x64 module at k = 64: 16 KiB of partials per example; 5000 examples need 78 MiB
+    need = L.attr_project_workspace_size((P._CModule * 1)(_mod()), 1, P.ATTR_BF16, 5000, 32, 64)
+    assert need > (64 << 20)
+    assert call([_mod()], n=5000, k=64, ldo=4096) == WORKSPACE
+    assert b"static buffer" in L.attr_last_error()
