@@ -266,6 +266,22 @@ attr_status attr_score_topk(const void* Q, int64_t n_q, int64_t ldq, const void*
                             void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Calibration (not part of the method): the rates this GPU sustains, used  */
+/* as measured peaks beside the nominal ones.                               */
+/* ------------------------------------------------------------------------ */
+
+/* Streams `bytes` (a multiple of 16, x 16-byte aligned) from device memory
+ * once with non-temporal 16-byte loads and no write stream (the result is
+ * folded into registers; `sink`, a device word, is written only on an
+ * improbable value).  Time it to get the achievable HBM read bandwidth. */
+attr_status attr_probe_read(const void* x, size_t bytes, void* sink, void* stream);
+/* Runs n_mfma (a multiple of 8, > 0) fp16 16x16x32 MFMAs per wave on 512
+ * workgroups of four waves (two waves per SIMD on 256 CUs), operands in
+ * registers: 2 * 16 * 16 * 32 * n_mfma * 2048 flops.  Time it to get the
+ * achievable dense fp16 matrix-core rate.  `sink`: a device float. */
+attr_status attr_probe_mfma(int64_t n_mfma, void* sink, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Diagnostics.                                                             */
 /* ------------------------------------------------------------------------ */
 

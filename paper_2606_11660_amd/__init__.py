@@ -28,7 +28,7 @@ __all__ = [
     "attr_precond_accumulate",
     "attr_precond_apply", "attr_score_topk", "attr_project_workspace_size",
     "attr_precond_accumulate_workspace_size", "attr_precond_apply_workspace_size",
-    "attr_score_topk_workspace_size", "Workspace",
+    "attr_score_topk_workspace_size", "Workspace", "attr_probe_read", "attr_probe_mfma",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -95,6 +95,10 @@ def lib() -> ctypes.CDLL:
     L.attr_precond_apply.restype = ctypes.c_int
     L.attr_precond_apply.argtypes = [vp, ctypes.c_int, i64, i64, i64, ctypes.c_int, vp, i32, vp,
                                      ctypes.c_int, i64, vp, sz, vp]
+    L.attr_probe_read.restype = ctypes.c_int
+    L.attr_probe_read.argtypes = [vp, sz, vp, vp]
+    L.attr_probe_mfma.restype = ctypes.c_int
+    L.attr_probe_mfma.argtypes = [i64, vp, vp]
     L.attr_score_topk_workspace_size.restype = sz
     L.attr_score_topk_workspace_size.argtypes = [i64, i64, i64, i32]
     L.attr_score_topk.restype = ctypes.c_int
@@ -424,3 +428,22 @@ def attr_score_topk(Q: torch.Tensor, G: torch.Tensor, k: int, top_score: torch.T
                              index_base, 1 if merge else 0, top_score.data_ptr(),
                              top_index.data_ptr(), wsp, wsn, _stream(stream)))
     return top_score, top_index
+
+
+# ----------------------------------------------------------------------------
+# calibration (measured peaks; not part of the method)
+# ----------------------------------------------------------------------------
+def attr_probe_read(x: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """One streaming read of every byte of x (HBM read-bandwidth probe)."""
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    _same_gpu(x, sink)
+    _check(lib().attr_probe_read(x.data_ptr(), x.numel() * x.element_size(), sink.data_ptr(),
+                                 _stream(stream)))
+
+
+def attr_probe_mfma(n_mfma: int, sink: torch.Tensor, stream=None) -> int:
+    """n_mfma fp16 16x16x32 MFMAs per wave on 2048 waves; returns the flops."""
+    _same_gpu(sink)
+    _check(lib().attr_probe_mfma(n_mfma, sink.data_ptr(), _stream(stream)))
+    return 2 * 16 * 16 * 32 * n_mfma * 2048

@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libattr.so")
 ARCH = "gfx950"
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
-HIP_SOURCES = ["project.hip", "rowwise.hip", "syrk.hip", "apply_full.hip", "score.hip"]
+HIP_SOURCES = ["project.hip", "rowwise.hip", "syrk.hip", "apply_full.hip", "score.hip", "probe.hip"]
 CXX_SOURCES = ["api.cpp"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall",

@@ -58,14 +58,13 @@ bool overlap(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
 // ---------------------------------------------------------------------------
 // projection
 // ---------------------------------------------------------------------------
-struct ProjRun {
-  int ms, slot0, n_groups;  // groups of ms modules sharing a, from slot0
-};
 struct ProjLayout {
-  size_t off_tab, off_pk, off_part, total;
+  size_t off_tab, off_gtab, off_wl, off_pk, off_part, total;
   std::vector<int> order;       // slot -> module index
   std::vector<size_t> pk_off;   // per slot, relative to off_pk
-  std::vector<ProjRun> runs;    // one main launch each
+  std::vector<int> slot_grp;    // slot -> group
+  std::vector<int> lead_ms;     // slot -> group size if the group's first slot, else 0
+  int n_groups;
   int n_chunks;
 };
 
@@ -75,9 +74,10 @@ ProjLayout project_layout(const attr_module* mods, int32_t n_mods, int eb, int64
   const int nk = k / 16;
   // Modules that read the same input rows (same a, lda and d_in: q/k/v or
   // gate/up of a transformer layer) form groups of up to kProjGroupMax,
-  // projected together so that a is read once.  Slots: groups by size
-  // (largest first), within a size largest work first, so the dispatcher
-  // starts the longest items first; a group's members take consecutive slots.
+  // projected together so that a is read once.  Groups are ordered by their
+  // work per token (the row elements they read), largest first, so that the
+  // one main launch starts the longest items first and ends on the
+  // shortest; a group's members take consecutive slots.
   // (three members at k = 64 would need more than 256 VGPRs: two waves per
   // SIMD no longer fit, so groups stop at two there)
   // (per-token blocks keep one module per item: their row-writing code would
@@ -102,19 +102,28 @@ ProjLayout project_layout(const attr_module* mods, int32_t n_mods, int eb, int64
   };
   std::stable_sort(groups.begin(), groups.end(),
                    [&](const std::vector<int>& x, const std::vector<int>& y) {
-                     if (x.size() != y.size()) return x.size() > y.size();
                      return cost(x) > cost(y);
                    });
-  for (const auto& gm : groups) {
-    const int ms = (int)gm.size();
-    if (L.runs.empty() || L.runs.back().ms != ms) L.runs.push_back({ms, (int)L.order.size(), 0});
-    ++L.runs.back().n_groups;
-    for (int x : gm) L.order.push_back(x);
+  L.n_groups = (int)groups.size();
+  for (int gi = 0; gi < L.n_groups; ++gi) {
+    const auto& gm = groups[gi];
+    for (size_t u = 0; u < gm.size(); ++u) {
+      L.order.push_back(gm[u]);
+      L.slot_grp.push_back(gi);
+      L.lead_ms.push_back(u == 0 ? (int)gm.size() : 0);
+    }
   }
   const int CT = attr::project_chunk_tokens(nk);
   L.n_chunks = (int)((T + CT - 1) / CT);
   L.off_tab = 0;
   size_t off = align_up(sizeof(attr::ProjTab) * (size_t)n_mods);
+  L.off_gtab = off;
+  off += align_up(sizeof(attr::ProjGroup) * (size_t)L.n_groups);
+  // work list (examples by chunk count, chunk-row offsets), whether or not
+  // the call passes lengths: the query has no lengths to look at
+  L.off_wl = off;
+  if (n_ex <= attr::kWorklistMaxExamples && L.n_chunks <= attr::kWorklistMaxChunks)
+    off += align_up(4 * (size_t)n_ex) + align_up(4 * ((size_t)L.n_chunks + 1));
   L.off_pk = off;
   size_t pk = 0;
   L.pk_off.resize(n_mods);
@@ -243,6 +252,7 @@ static attr_status project_impl(const attr_module* mods, int32_t n_mods, attr_dt
     hipStream_t s = static_cast<hipStream_t>(stream);
     char* base = static_cast<char*>(ws);
     attr::ProjTab* tab = reinterpret_cast<attr::ProjTab*>(base + L.off_tab);
+    attr::ProjGroup* gtab = reinterpret_cast<attr::ProjGroup*>(base + L.off_gtab);
     char* pk = base + L.off_pk;
     float* part = reinterpret_cast<float*>(base + L.off_part);
     const bool bf16 = in_dtype == ATTR_BF16;
@@ -267,17 +277,22 @@ static attr_status project_impl(const attr_module* mods, int32_t n_mods, attr_dt
         e.d_out = (int32_t)m.d_out;
         e.v_out = m.v_out;
         e.v_in = m.v_in;
+        e.grp = L.slot_grp[s0 + j];
+        e.lead_ms = L.lead_ms[s0 + j];
       }
-      hipError_t e = attr::launch_project_pack(bf16, nk, pa, tab, pk, s);
+      hipError_t e = attr::launch_project_pack(bf16, nk, pa, tab, gtab, pk, s);
       if (e != hipSuccess) return device_fail(e, "attr_project pack launch");
     }
-    hipError_t e = hipSuccess;
-    for (const ProjRun& r : L.runs) {
-      e = attr::launch_project_main(bf16, nk, r.ms, tab, r.slot0, r.n_groups, L.n_chunks,
-                                    n_examples, T, row_offset, length, tok ? out : part, s, tok,
-                                    ldo, n_rows);
-      if (e != hipSuccess) return device_fail(e, "attr_project main launch");
+    int32_t* wl_perm = nullptr;
+    int32_t* wl_off = nullptr;
+    if (attr::project_uses_worklist(length, n_examples, L.n_chunks)) {
+      wl_perm = reinterpret_cast<int32_t*>(base + L.off_wl);
+      wl_off = reinterpret_cast<int32_t*>(base + L.off_wl + align_up(4 * (size_t)n_examples));
     }
+    hipError_t e = attr::launch_project_main(bf16, nk, tab, gtab, L.n_groups, L.n_chunks,
+                                             n_examples, T, row_offset, length, wl_perm, wl_off,
+                                             tok ? out : part, s, tok, ldo, n_rows);
+    if (e != hipSuccess) return device_fail(e, "attr_project main launch");
     if (tok) return ATTR_OK;
     e = attr::launch_project_reduce(nk, tab, n_mods, L.n_chunks, n_examples, T, length, part, out,
                                     ldo, s);
@@ -541,6 +556,24 @@ attr_status attr_score_topk(const void* Q, int64_t n_q, int64_t ldq, const void*
   } catch (...) {
     return fail(ATTR_ERR_INVALID_ARG, "attr_score_topk: host exception");
   }
+}
+
+// ---------------------------------------------------------------------------
+attr_status attr_probe_read(const void* x, size_t bytes, void* sink, void* stream) {
+  g_err.clear();
+  if (bytes == 0) return ATTR_OK;
+  if (!x || !sink) return fail(ATTR_ERR_INVALID_ARG, "attr_probe_read: NULL pointer");
+  if (!aligned16(x) || bytes % 16) return fail(ATTR_ERR_ALIGNMENT, "attr_probe_read: x and bytes must be 16-byte multiples");
+  const hipError_t e = attr::launch_probe_read(x, bytes, sink, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ATTR_OK : device_fail(e, "attr_probe_read launch");
+}
+
+attr_status attr_probe_mfma(int64_t n_mfma, void* sink, void* stream) {
+  g_err.clear();
+  if (n_mfma <= 0 || n_mfma % 8) return fail(ATTR_ERR_INVALID_ARG, "attr_probe_mfma: n_mfma must be a positive multiple of 8");
+  if (!sink) return fail(ATTR_ERR_INVALID_ARG, "attr_probe_mfma: NULL sink");
+  const hipError_t e = attr::launch_probe_mfma(n_mfma, sink, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ATTR_OK : device_fail(e, "attr_probe_mfma launch");
 }
 
 }  // extern "C"

@@ -21,6 +21,12 @@ struct ProjTab {
   int32_t d_in, d_out;
 };
 
+// One work group of the projection: ms consecutive slots from slot0 whose
+// modules share their input rows (ms = 1 for a module on its own).
+struct ProjGroup {
+  int32_t slot0, ms;
+};
+
 // Host -> device upload of module descriptors travels in kernel arguments.
 struct PackEntry {
   const void* a;
@@ -31,6 +37,8 @@ struct PackEntry {
   const float* v_in;
   int64_t lda, ldg, out_col, pk_off;
   int32_t d_in, d_out;
+  int32_t grp;      // group of this slot
+  int32_t lead_ms;  // group size if this slot is the group's first, else 0
 };
 constexpr int kPackMax = 24;
 struct PackArgs {
@@ -51,15 +59,28 @@ constexpr size_t kProjectScratchBytes = (size_t)64 << 20;
 hipError_t project_scratch(void** ptr);
 
 hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab* tab,
-                               char* pk_base, hipStream_t s);
+                               ProjGroup* gtab, char* pk_base, hipStream_t s);
 // Modules sharing their input rows (same a, lda, d_in) are projected in
-// groups of up to kProjGroupMax consecutive slots (one read of a per group);
-// one launch per group size ms covers n_groups groups from slot0.
+// groups of up to kProjGroupMax consecutive slots (one read of a per group).
+// One launch covers every (group, token chunk, example) item, groups in
+// table order (largest work first).
 constexpr int kProjGroupMax = 3;
+// Work list of a call with per-example lengths (device-built): examples
+// sorted by chunk count, longest first, and the item offset of each chunk
+// row.  Built when length is given, n_chunks <= kWorklistMaxChunks and
+// n_examples <= kWorklistMaxExamples; otherwise the main kernel decodes its
+// block index densely.
+constexpr int kWorklistMaxChunks = 2048;
+constexpr int64_t kWorklistMaxExamples = 1 << 20;
+inline bool project_uses_worklist(const int32_t* length, int64_t n_ex, int n_chunks) {
+  return length && n_chunks <= kWorklistMaxChunks && n_ex <= kWorklistMaxExamples;
+}
 // tok: per-token blocks written straight into `partial` = the output [n_rows, ldo]
-hipError_t launch_project_main(bool bf16, int nk, int ms, const ProjTab* tab, int slot0,
+// wl_perm / wl_off: the work list (both NULL for the dense decode).
+hipError_t launch_project_main(bool bf16, int nk, const ProjTab* tab, const ProjGroup* gtab,
                                int n_groups, int n_chunks, int64_t n_ex, int64_t T,
                                const int64_t* row_offset, const int32_t* length,
+                               int32_t* wl_perm, int32_t* wl_off,
                                float* partial, hipStream_t s, bool tok = false, int64_t ldo = 0,
                                int64_t n_rows = 0);
 hipError_t launch_project_reduce(int nk, const ProjTab* tab, int n_slots, int n_chunks,
@@ -129,5 +150,11 @@ size_t apply_full_workspace(int64_t n_rows, int64_t D, int unit);
 hipError_t launch_apply_full(const void* X, int64_t n_rows, int64_t ldx, int64_t D, const float* M,
                              int y_dtype, void* Y, int64_t ldy, int unit, void* ws,
                              hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// calibration
+// ---------------------------------------------------------------------------
+hipError_t launch_probe_read(const void* x, size_t bytes, void* sink, hipStream_t s);
+hipError_t launch_probe_mfma(int64_t n_mfma, void* sink, hipStream_t s);
 
 }  // namespace attr

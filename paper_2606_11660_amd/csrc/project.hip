@@ -5,10 +5,11 @@
 // per-example gradient.
 //
 // Design (HBM-bound: every a/g element is read once and used for 2k flops):
-//  * One workgroup (4 waves) owns one (module, token chunk, example) item;
-//    each wave owns 16*TT consecutive tokens.  Items are enumerated module
-//    slot major (largest modules first), then chunk, then example, so the
-//    dispatcher hands out the most expensive items first.
+//  * One workgroup (4 waves) owns one (module group, token chunk, example)
+//    item of 64*TT tokens, a quarter of the chunk's valid tokens per wave.
+//    One launch covers every item: module groups (modules that share their
+//    input rows) by decreasing work per token, then chunk, then example, so
+//    the dispatcher hands out the most expensive items first.
 //  * Stage 1 runs on the matrix cores: A_tile (16 tokens x K) times the
 //    packed S fragment gives 16 tokens x 16 projected columns.  Every lane
 //    loads 16 contiguous bytes of one token row per step through a
@@ -84,7 +85,7 @@ __device__ inline uint16_t bf16_rne(float x) {
 // ---------------------------------------------------------------------------
 template <bool BF16, int NK>
 __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTab* tab,
-                                                           char* pk_base) {
+                                                           ProjGroup* gtab, char* pk_base) {
   using E_t = ElemT<BF16>;
   constexpr int E = 16 / E_t::bytes;
   constexpr int KS = 4 * E;
@@ -107,6 +108,7 @@ __global__ __launch_bounds__(256) void project_pack_kernel(PackArgs args, ProjTa
     t.d_in = pe.d_in;
     t.d_out = pe.d_out;
     tab[args.slot0 + j] = t;
+    if (pe.lead_ms > 0) gtab[pe.grp] = ProjGroup{args.slot0 + j, pe.lead_ms};
   }
   // Optimizer-state normalisation (factored second moment v = v_out v_in^T
   // / sum(v_out)): G / sqrt(v) = D_out G D_in with D_out = diag(sqrt(sum /
@@ -271,20 +273,21 @@ __device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int
   }
 }
 
-// One workgroup per (group, token chunk, example) item.  A group is MS
-// modules (consecutive slots from slot0 + MS * group) that share their
-// input rows a: the a tiles are read once and projected through each
-// member's S; each member's own g rows follow, and each member's k x k
-// partial goes to its slot's item.
+// One (group, token chunk, example) item, run by one workgroup.  A group
+// is MS modules (consecutive slots from s0) that share their input rows a:
+// the a tiles are read once and projected through each member's S; each
+// member's own g rows follow, and each member's k x k partial goes to its
+// slot's item.
 // TOK: per-token blocks instead of the token sum: token t's (R^T g_t)(S^T
 // a_t)^T is written to row (first row of the example) + t of `partial`
 // (then the caller's output, row stride ldo, n_rows rows), at the module's
 // out_col; no partials, no reduction.
 template <bool BF16, int NK, int MS, bool TOK>
-__global__ __launch_bounds__(256) void project_main_kernel(
-    const ProjTab* __restrict__ tab, int slot0, int n_chunks, int64_t n_ex, int64_t T,
-    const int64_t* __restrict__ row_offset, const int32_t* __restrict__ length,
-    float* __restrict__ partial, int64_t ldo, int64_t n_rows) {
+__device__ inline void project_item(const ProjTab* __restrict__ tab, int s0, uint32_t i, int c,
+                                    int n_chunks, int64_t n_ex, int64_t T, int64_t len,
+                                    const int64_t* __restrict__ row_offset,
+                                    float* __restrict__ partial, int64_t ldo, int64_t n_rows,
+                                    i32x4* __restrict__ xpose, float* __restrict__ red) {
   using E_t = ElemT<BF16>;
   using Tag = typename E_t::tag;
   constexpr int EB = E_t::bytes;
@@ -294,32 +297,23 @@ __global__ __launch_bounds__(256) void project_main_kernel(
   constexpr int TPW = 16 * TT;  // tokens per wave
   constexpr int CT = 4 * TPW;   // tokens per workgroup
   constexpr int KK = 256 * NK * NK;
-
-  // Work-item decode in 32-bit scalar arithmetic (the host keeps the grid
-  // below 2^24 items and n_examples below 2^31).
-  const uint32_t blk = blockIdx.x;
-  const uint32_t nex = (uint32_t)n_ex;
-  const uint32_t i = blk % nex;
-  const uint32_t rest = blk / nex;
-  const int c = (int)(rest % (uint32_t)n_chunks);
-  const int s0 = slot0 + MS * (int)(rest / (uint32_t)n_chunks);
-
-  int64_t len = length ? (int64_t)length[i] : T;
-  len = len < 0 ? 0 : (len > T ? T : len);
   const int64_t t0 = (int64_t)c * CT;
-  if (t0 >= len) return;  // uniform over the workgroup
 
-  __shared__ i32x4 xpose[4][TT * 128];
-  __shared__ float red[3][KK];
   // The wave index is uniform per wave; readfirstlane lets the compiler keep
   // everything derived from it (token range, buffer resources) in SGPRs.
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63;
-  const int64_t wt0 = t0 + (int64_t)wave * TPW;
-  int64_t ntok = len - wt0;
-  ntok = ntok < 0 ? 0 : (ntok > TPW ? TPW : ntok);
+  // The chunk's valid tokens are spread evenly over the four waves (TPW each
+  // in a full chunk), so the last, partial chunk of an example keeps every
+  // wave busy for a quarter of it instead of leaving trailing waves idle
+  // while the workgroup holds its slot.
+  const int64_t nv = len - t0 < CT ? len - t0 : CT;  // > 0
+  const int64_t q = (nv + 3) / 4;                     // <= TPW
+  const int64_t wt0 = t0 + (int64_t)wave * q;
+  int64_t ntok = nv - (int64_t)wave * q;
+  ntok = ntok < 0 ? 0 : (ntok > q ? q : ntok);
   const int64_t row0 = ntok > 0 ? (row_offset ? row_offset[i] : (int64_t)i * T) + wt0 : 0;
-  i32x4* xp = &xpose[wave][0];
+  i32x4* xp = xpose + wave * (TT * 128);
 
   f32x4 At[MS][TT][NK];
 #pragma unroll
@@ -402,7 +396,7 @@ __global__ __launch_bounds__(256) void project_main_kernel(
 #pragma unroll
         for (int ct = 0; ct < NK; ++ct)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) red[wave - 1][((rt * NK + ct) * 4 + q) * kWave + lane] = P[rt][ct][q];
+          for (int q = 0; q < 4; ++q) red[(wave - 1) * KK + ((rt * NK + ct) * 4 + q) * kWave + lane] = P[rt][ct][q];
     }
     __syncthreads();
     if (wave == 0) {
@@ -415,13 +409,129 @@ __global__ __launch_bounds__(256) void project_main_kernel(
           for (int q = 0; q < 4; ++q) {
             const int e = ((rt * NK + ct) * 4 + q) * kWave + lane;
             float v = P[rt][ct][q];
-            v += red[0][e];
-            v += red[1][e];
-            v += red[2][e];
+            v += red[e];
+            v += red[KK + e];
+            v += red[2 * KK + e];
             dst[e] = v;
           }
     }
   }
+}
+
+
+// Work list of a call with per-example lengths (one workgroup): example i
+// has n_i = ceil(len_i / CT) chunks.  perm lists the examples by decreasing
+// n_i (the order within equal n_i is whatever the scatter gives: it only
+// decides which workgroup takes an item, never a result), so the examples
+// that have a chunk c are exactly perm[0 .. cnt_c), cnt_c = #{i : n_i > c};
+// off[c] = cnt_0 + ... + cnt_{c-1} is the first item of chunk row c within a
+// group and off[n_chunks] the items per group.
+__global__ __launch_bounds__(1024) void project_worklist_kernel(const int32_t* __restrict__ length,
+                                                                int64_t n_ex, int64_t T, int CT,
+                                                                int n_chunks,
+                                                                int32_t* __restrict__ perm,
+                                                                int32_t* __restrict__ off) {
+  __shared__ int hist[kWorklistMaxChunks + 1];
+  __shared__ int cur[kWorklistMaxChunks + 1];
+  for (int j = threadIdx.x; j <= n_chunks; j += 1024) hist[j] = 0;
+  __syncthreads();
+  auto chunks_of = [&](int64_t i) {
+    int64_t len = length[i];
+    len = len < 0 ? 0 : (len > T ? T : len);
+    return (int)((len + CT - 1) / CT);
+  };
+  for (int64_t i = threadIdx.x; i < n_ex; i += 1024) atomicAdd(&hist[chunks_of(i)], 1);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;  // examples with more chunks than n come first
+    for (int n = n_chunks; n >= 0; --n) {
+      cur[n] = run;
+      run += hist[n];
+    }
+    int acc = 0;  // cnt_c = cur[c]: examples in buckets above c
+    for (int c = 0; c < n_chunks; ++c) {
+      off[c] = acc;
+      acc += cur[c];
+    }
+    off[n_chunks] = acc;
+  }
+  __syncthreads();
+  for (int64_t i = threadIdx.x; i < n_ex; i += 1024) perm[atomicAdd(&cur[chunks_of(i)], 1)] = (int32_t)i;
+}
+
+// One workgroup per (group, token chunk, example) item of the whole call:
+// items are enumerated group major (groups in table order, largest work
+// first), then chunk, then example, so the dispatcher hands out the most
+// expensive items first and the cheapest fill the tail of the one launch.
+// The group size is read from the group table and dispatched at run time
+// (uniform per workgroup); every size fits two waves per SIMD.
+template <bool BF16, int NK, bool TOK>
+__global__ __launch_bounds__(256, 2) void project_main_kernel(
+    const ProjTab* __restrict__ tab, const ProjGroup* __restrict__ gtab, int n_groups,
+    int n_chunks, int64_t n_ex, int64_t T, const int64_t* __restrict__ row_offset,
+    const int32_t* __restrict__ length, const int32_t* __restrict__ wl_perm,
+    const int32_t* __restrict__ wl_off, float* __restrict__ partial, int64_t ldo,
+    int64_t n_rows) {
+  constexpr int TT = Tiles<NK>::TT;
+  constexpr int CT = 4 * 16 * TT;  // tokens per workgroup
+  constexpr int KK = 256 * NK * NK;
+  // Work-item decode in 32-bit scalar arithmetic (the host keeps the grid
+  // below 2^24 items and n_examples below 2^31).  Workgroups go to the 8
+  // XCDs round robin (block % 8), so the decode must not tie an example to
+  // an XCD: with the example index varying fastest, example i would run on
+  // XCD i % 8 for the whole call and each XCD would carry the summed length
+  // of its own examples (ragged batches left XCDs idle while others worked).
+  const uint32_t blk = blockIdx.x;
+  uint32_t i;
+  int c;
+  ProjGroup gr;
+  if (wl_perm) {
+    // work list: block b takes the b-th valid item (group major, then chunk
+    // row, then examples longest first); the blocks past the last item exit
+    const uint32_t per = (uint32_t)wl_off[n_chunks];
+    if (per == 0) return;
+    const uint32_t g = blk / per;
+    if (g >= (uint32_t)n_groups) return;  // uniform over the workgroup
+    const uint32_t r = blk - g * per;
+    int lo = 0, hi = n_chunks - 1;  // largest c with off[c] <= r
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if ((uint32_t)wl_off[mid] <= r) lo = mid;
+      else hi = mid - 1;
+    }
+    c = lo;
+    i = (uint32_t)wl_perm[r - (uint32_t)wl_off[c]];
+    gr = gtab[g];
+  } else {
+    // dense decode: the example index is rotated per (group, chunk) row so
+    // that every XCD takes every example equally often
+    const uint32_t nex = (uint32_t)n_ex;
+    const uint32_t rest = blk / nex;
+    const uint32_t rot = rest + rest / (uint32_t)n_chunks;
+    i = (blk % nex + rot % nex) % nex;
+    c = (int)(rest % (uint32_t)n_chunks);
+    gr = gtab[rest / (uint32_t)n_chunks];
+  }
+
+  int64_t len = length ? (int64_t)length[i] : T;
+  len = len < 0 ? 0 : (len > T ? T : len);
+  if ((int64_t)c * CT >= len) return;  // uniform over the workgroup
+
+  __shared__ i32x4 xpose[4 * TT * 128];
+  __shared__ float red[3 * KK];
+  // groups of three at k = 64 and grouped per-token blocks would pass 256
+  // VGPRs; the host never forms them
+  constexpr bool m2 = !TOK;
+  constexpr bool m3 = !TOK && NK < 4;
+  if (m3 && gr.ms == 3)
+    project_item<BF16, NK, (m3 ? 3 : 1), TOK>(tab, gr.slot0, i, c, n_chunks, n_ex, T, len,
+                                               row_offset, partial, ldo, n_rows, xpose, red);
+  else if (m2 && gr.ms == 2)
+    project_item<BF16, NK, (m2 ? 2 : 1), TOK>(tab, gr.slot0, i, c, n_chunks, n_ex, T, len,
+                                               row_offset, partial, ldo, n_rows, xpose, red);
+  else
+    project_item<BF16, NK, 1, TOK>(tab, gr.slot0, i, c, n_chunks, n_ex, T, len, row_offset,
+                                   partial, ldo, n_rows, xpose, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -484,10 +594,10 @@ size_t project_packed_bytes(int64_t d_in, int64_t d_out, int k, int elem_bytes) 
 }
 
 hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab* tab,
-                               char* pk_base, hipStream_t s) {
+                               ProjGroup* gtab, char* pk_base, hipStream_t s) {
   dim3 grid(args.n, 8), block(256);
 #define ATTR_PACK(B, N) \
-  hipLaunchKernelGGL((project_pack_kernel<B, N>), grid, block, 0, s, args, tab, pk_base)
+  hipLaunchKernelGGL((project_pack_kernel<B, N>), grid, block, 0, s, args, tab, gtab, pk_base)
   if (bf16) {
     if (nk == 1) ATTR_PACK(true, 1);
     else if (nk == 2) ATTR_PACK(true, 2);
@@ -501,38 +611,38 @@ hipError_t launch_project_pack(bool bf16, int nk, const PackArgs& args, ProjTab*
   return hipGetLastError();
 }
 
-hipError_t launch_project_main(bool bf16, int nk, int ms, const ProjTab* tab, int slot0,
+hipError_t launch_project_main(bool bf16, int nk, const ProjTab* tab, const ProjGroup* gtab,
                                int n_groups, int n_chunks, int64_t n_ex, int64_t T,
                                const int64_t* row_offset, const int32_t* length,
+                               int32_t* wl_perm, int32_t* wl_off,
                                float* partial, hipStream_t s, bool tok, int64_t ldo,
                                int64_t n_rows) {
   const int64_t nblk = (int64_t)n_groups * n_chunks * n_ex;
   if (nblk == 0) return hipSuccess;
+  if (wl_perm) {
+    hipLaunchKernelGGL(project_worklist_kernel, dim3(1), dim3(1024), 0, s, length, n_ex, T,
+                       project_chunk_tokens(nk), n_chunks, wl_perm, wl_off);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   dim3 grid((unsigned)nblk), block(256);
-#define ATTR_MAIN(B, N, M, TK)                                                                    \
-  hipLaunchKernelGGL((project_main_kernel<B, N, M, TK>), grid, block, 0, s, tab, slot0, n_chunks,  \
-                     n_ex, T, row_offset, length, partial, ldo, n_rows)
-#define ATTR_MAIN_MS(B, N)                                                   \
-  if (tok) {                                                                 \
-    if (ms == 1) ATTR_MAIN(B, N, 1, true);                                   \
-    else if (ms == 2) ATTR_MAIN(B, N, 2, true);                              \
-    else ATTR_MAIN(B, N, 3, true);                                           \
-  } else {                                                                   \
-    if (ms == 1) ATTR_MAIN(B, N, 1, false);                                  \
-    else if (ms == 2) ATTR_MAIN(B, N, 2, false);                             \
-    else ATTR_MAIN(B, N, 3, false);                                          \
-  }
-  if (ms < 1 || ms > kProjGroupMax) return hipErrorInvalidValue;
+#define ATTR_MAIN(B, N, TK)                                                                   \
+  hipLaunchKernelGGL((project_main_kernel<B, N, TK>), grid, block, 0, s, tab, gtab, n_groups, \
+                     n_chunks, n_ex, T, row_offset, length, (const int32_t*)wl_perm,          \
+                     (const int32_t*)wl_off, partial, ldo, n_rows)
+#define ATTR_MAIN_TK(B, N) \
+  if (tok) ATTR_MAIN(B, N, true); \
+  else ATTR_MAIN(B, N, false);
   if (bf16) {
-    if (nk == 1) { ATTR_MAIN_MS(true, 1) }
-    else if (nk == 2) { ATTR_MAIN_MS(true, 2) }
-    else { ATTR_MAIN_MS(true, 4) }
+    if (nk == 1) { ATTR_MAIN_TK(true, 1) }
+    else if (nk == 2) { ATTR_MAIN_TK(true, 2) }
+    else { ATTR_MAIN_TK(true, 4) }
   } else {
-    if (nk == 1) { ATTR_MAIN_MS(false, 1) }
-    else if (nk == 2) { ATTR_MAIN_MS(false, 2) }
-    else { ATTR_MAIN_MS(false, 4) }
+    if (nk == 1) { ATTR_MAIN_TK(false, 1) }
+    else if (nk == 2) { ATTR_MAIN_TK(false, 2) }
+    else { ATTR_MAIN_TK(false, 4) }
   }
-#undef ATTR_MAIN_MS
+#undef ATTR_MAIN_TK
 #undef ATTR_MAIN
   return hipGetLastError();
 }

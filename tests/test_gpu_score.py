@@ -540,14 +540,16 @@ def test_gemm_plan_running_bound(order):
         assert (host(ti)[sample][:, 1:] < chunk).all()
 
 
-def test_bench_two_stream_step_matches_one_stream():
+@pytest.mark.parametrize("ragged", [False, True])
+def test_bench_two_stream_step_matches_one_stream(ragged):
     """The bench step pipelines over two streams (projection of batch i + 1
     while batch i is normalised and scored; two fp32 row buffers ordered by
     events).  Every call is deterministic, so the store rows and the running
     top-k after 5 pipelined steps equal, bitwise, the same calls issued one
-    after another on one stream."""
+    after another on one stream.  ragged: the steps cycle over two packed
+    batches of ragged lengths (row_offset / length), as the headline does."""
     import bench
-    say("case: two-stream bench step vs one stream, 5 steps")
+    say(f"case: two-stream bench step vs one stream, 5 steps, ragged={ragged}")
     rng = np.random.default_rng(91)
     k, B, T, steps, topk = 16, 8, 96, 5, 7
     shapes = [(64, 192), (128, 64), (64, 128)]
@@ -560,6 +562,13 @@ def test_bench_two_stream_step_matches_one_stream():
         S = torch.from_numpy(synth.to_bf16_bits(rng.standard_normal((d_in, k)) / 4).view(np.int16)).view(torch.bfloat16).cuda()
         mods.append(P.Module(a, g, R, S, m * k * k))
     Qrows = torch.from_numpy(rng.standard_normal((6, D)).astype(np.float16)).cuda()
+    batches = None
+    if ragged:
+        batches = []
+        for lens in ([96, 0, 17, 64, 95, 1, 33, 80], [5, 96, 96, 96, 2, 60, 0, 70]):
+            offs = np.concatenate([[0], np.cumsum(lens)[:-1]])
+            batches.append((torch.from_numpy(offs.astype(np.int64)).cuda(),
+                            torch.from_numpy(np.asarray(lens, dtype=np.int32)).cuda()))
     results = []
     for two in (True, False):
         s1 = torch.cuda.Stream()
@@ -571,12 +580,14 @@ def test_bench_two_stream_step_matches_one_stream():
         ws = [P.Workspace("cuda") for _ in range(3)]
         pd, nd = bench._pipeline_events(s2)
         bench.run_pipeline(mods, k, B, T, rows, store, Qrows, topk, top_s, top_i, 0, steps, s1, s2,
-                           ws[0], ws[1], ws[2], pd, nd)
+                           ws[0], ws[1], ws[2], pd, nd, batches=batches)
         s1.synchronize()
         s2.synchronize()
         results.append((host(store), host(top_s), host(top_i)))
     (st2, ts2, ti2), (st1, ts1, ti1) = results
     assert np.isfinite(st2).all()
+    if ragged:   # a zero-length example stores a zero row, never NaN
+        assert (st2[1] == 0).all() and (st2[B + 6] == 0).all()
     assert np.array_equal(st2.view(np.uint16), st1.view(np.uint16))
     assert np.array_equal(ts2, ts1) and np.array_equal(ti2, ti1)
     assert (ti2 >= 0).all() and (ti2 < steps * B).all()
