@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256, 2) void probe_mfma_kernel(int64_t n_mfma, floa
 
 hipError_t launch_probe_read(const void* x, size_t bytes, void* sink, hipStream_t s) {
   const int64_t n16 = (int64_t)(bytes / 16);
-  hipLaunchKernelGGL(probe_read_kernel, dim3(2048), dim3(256), 0, s, (const i32x4*)x, n16,
+  hipLaunchKernelGGL(probe_read_kernel, dim3(8192), dim3(256), 0, s, (const i32x4*)x, n16,
                      (uint32_t*)sink);
   return hipGetLastError();
 }
