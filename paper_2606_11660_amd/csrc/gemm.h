@@ -230,6 +230,14 @@ struct GemmCore {
 // consecutive K-rows; two such reads give the 8 K-values of an MFMA operand.
 // It issues twice as many LDS reads as the row-major core (512 instead of
 // 1024 bytes each) and needs no transposed copy of the operands.
+//
+// NEG: the sign bit of every 16-bit value of the B fragments is flipped (XOR
+// 0x80008000) between the loop that reads a K-half and the loop that uses
+// it, so the core accumulates -A B^T.  The second-moment accumulation alternates the sign of
+// its row slices this way to cancel the matrix core's rounding bias (see
+// syrk.hip).  It is a compile-time choice: the non-negated core is the
+// plain loop, and a run-time mask or branch inside the loop raised the
+// scalar-register pressure or the instruction count of every slice.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 __device__ inline i32x2 lds_read_tr16(uint32_t byte_addr) {
   const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -238,7 +246,7 @@ __device__ inline i32x2 lds_read_tr16(uint32_t byte_addr) {
 }
 __device__ inline int kmajor_swz(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
 
-template <typename Tag>
+template <typename Tag, bool NEG = false>
 struct GemmCoreT {
   f32x4 acc[8][8];
 
@@ -253,6 +261,7 @@ struct GemmCoreT {
   // Byte offsets within a descriptor must fit 31 bits.
   __device__ inline void run(GemmSmem& sm, const i32x4& da, int64_t lda, const i32x4& db,
                              int64_t ldb, int n_st) {
+    constexpr int32_t neg_mask = NEG ? (int32_t)0x80008000 : 0;
     if (n_st <= 0) return;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = threadIdx.x & 63;
@@ -325,6 +334,15 @@ struct GemmCoreT {
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[i][j] = mma16(Tag{}, fa[i], fb[j], acc[i][j]);
     };
+    // NEG: the B fragments of a K-half are flipped in place once their reads
+    // have landed, between the loop that read them and the loop that uses
+    // them
+    auto negate_b = [&](i32x4 (&fb)[8]) {
+      if (NEG) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) fb[j] ^= neg_mask;
+      }
+    };
     i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
 
     // same pipeline as GemmCore::run
@@ -337,6 +355,7 @@ struct GemmCoreT {
       h0a[i] = frag(sa0, wm, i, 0);
       h0b[i] = frag(sb0, wn, i, 0);
     }
+    negate_b(h0b);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       read_pair(i, sa0, sb0, 1, h1a, h1b);
@@ -344,6 +363,7 @@ struct GemmCoreT {
       mma_row(i, h0a, h0b);
       __builtin_amdgcn_sched_barrier(0);
     }
+    negate_b(h1b);
     for (int st = 1; st < n_st; ++st) {
       gemm_wait_vm<0>();
       wait_lgkm0();
@@ -373,6 +393,7 @@ struct GemmCoreT {
         for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
+      negate_b(h0b);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         read_pair(i, pa, pb, 1, h1a, h1b);
@@ -380,6 +401,7 @@ struct GemmCoreT {
         mma_row(i, h0a, h0b);
         __builtin_amdgcn_sched_barrier(0);
       }
+      negate_b(h1b);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);

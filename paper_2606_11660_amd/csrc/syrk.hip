@@ -102,16 +102,31 @@ __global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ X, int6
   const int64_t ca = (int64_t)tp * GT, cb = (int64_t)tq * GT;
   const i32x4 da = make_desc(X + rs * ldx + ca, range(ca));
   const i32x4 db = make_desc(X + rs * ldx + cb, range(cb));
-  GemmCoreT<Tag> core;
-  core.zero();
-  core.run(sm, da, ldx, db, ldx, (int)((nr + GKS - 1) / GKS));  // stages holding rows
+  // odd slices accumulate -X^T X (A fragments negated) and store the negated
+  // sum: the matrix core's accumulation rounds toward -infinity on average,
+  // so the odd slices' sums come out high by about as much as the even
+  // slices' come out low, and the fp64 sum over slices cancels the bias
+  const int n_st = (int)((nr + GKS - 1) / GKS);  // stages holding rows
   float* dst = part + ((int64_t)j * n_up + u) * TILE_E;
+  auto store = [&](const f32x4 (&acc)[8][8], float sgn) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj)
+      for (int jj = 0; jj < 8; ++jj)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) dst[((i * 8 + jj) * 4 + r) * 256 + threadIdx.x] = core.acc[i][jj][r];
+        for (int r = 0; r < 4; ++r) dst[((i * 8 + jj) * 4 + r) * 256 + threadIdx.x] = sgn * acc[i][jj][r];
+  };
+  if (j & 1) {
+    GemmCoreT<Tag, true> core;
+    core.zero();
+    core.run(sm, da, ldx, db, ldx, n_st);
+    store(core.acc, -1.f);
+  } else {
+    GemmCoreT<Tag, false> core;
+    core.zero();
+    core.run(sm, da, ldx, db, ldx, n_st);
+    store(core.acc, 1.f);
+  }
 }
 
 // h64[u][e] += sum_j part[j][u][e], slices in order (fragment-order layout).

@@ -10,9 +10,13 @@
 
 namespace attr {
 
+#ifndef ATTR_SYRK_SLICE_ROWS
+#define ATTR_SYRK_SLICE_ROWS 32768
+#endif
 constexpr int kSyrkTile = 256;          // block tile of the GEMM core (both sides)
-constexpr int kSyrkChunkRows = 524288;  // rows per launch (16 K-slices: whole rounds of 256 CUs)
-constexpr int kSyrkSlices = 16;         // K-slices per full chunk
+constexpr int kSyrkSlices = 16;         // K-slices per full chunk (whole rounds of 256 CUs)
+constexpr int kSyrkSliceRows = ATTR_SYRK_SLICE_ROWS;        // longest fp32 accumulation
+constexpr int kSyrkChunkRows = kSyrkSlices * kSyrkSliceRows;  // rows per launch
 
 // Rows of one K-slice must span at most 2^31 bytes: the GEMM core marks its
 // loads past the last stage by adding 2^31 to their offset, which lands out

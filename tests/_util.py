@@ -69,3 +69,32 @@ def check_topk(got_s, got_i, ref_scores, k, index_base=0, tol=1e-3):
             right = rs[r] - rs[r + 1] if r + 1 < ng else np.inf
             if left > tol and right > tol:
                 assert gi[r] == order[r], (q, r, gi[r], order[r])
+
+
+def check_topk_from_lists(got_s, got_i, ref_s, ref_i, returned_scores, k, tol=1e-3):
+    """The checks of check_topk from the oracle's top-(k + 1) list instead of
+    the full score matrix (for stores too large to score whole on the host).
+
+    ref_s / ref_i: [nq, k + 1] the oracle's best k + 1 (score desc, index
+    asc); returned_scores: [nq, k] the oracle's scores of the returned
+    indices.  (a) returned scores within tol of the oracle's score of the
+    returned index and of the oracle's score at that rank; (b) every oracle
+    item scoring above s_{k+1} + tol is returned; (c) indices equal the
+    oracle's wherever the oracle's scores are separated from both neighbours
+    by more than tol; (d) indices unique and valid, scores non-increasing."""
+    got_s = np.asarray(got_s, dtype=np.float64)
+    got_i = np.asarray(got_i, dtype=np.int64)
+    for q in range(got_s.shape[0]):
+        rs, ri = ref_s[q], ref_i[q]
+        gs, gi = got_s[q], got_i[q]
+        assert (gi >= 0).all() and len(set(gi.tolist())) == k, "invalid or duplicate indices"
+        assert (np.diff(gs) <= 0).all(), "scores not sorted"
+        assert np.abs(gs - returned_scores[q]).max() <= tol, (q, np.abs(gs - returned_scores[q]).max())
+        assert np.abs(gs - rs[:k]).max() <= tol, (q, np.abs(gs - rs[:k]).max())
+        must = ri[:k][rs[:k] > rs[k] + tol]
+        assert set(must.tolist()) <= set(gi.tolist()), (q, "missing a clear winner")
+        for r in range(k):
+            left = rs[r - 1] - rs[r] if r > 0 else np.inf
+            right = rs[r] - rs[r + 1]
+            if left > tol and right > tol:
+                assert gi[r] == ri[r], (q, r, gi[r], ri[r])
