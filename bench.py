@@ -413,7 +413,7 @@ def _row_precond(dev, stream):
     return out
 
 
-def _row_store_scan(dev, stream, qs=(16, 64, 128, 256, 1024)):
+def _row_store_scan(dev, stream, qs=(16, 64, 128, 200, 256, 1024)):
     """4M x 8192 fp16 unit store (65.5 GB), top-100, Q sweep; 16 planted
     near-duplicates (cosine 0.9) of known rows must rank first."""
     import torch
@@ -442,7 +442,9 @@ def _row_store_scan(dev, stream, qs=(16, 64, 128, 256, 1024)):
         ti = torch.empty((nq, 100), dtype=torch.int64, device=dev)
         ms = _median_ms(lambda: P.attr_score_topk(Q, G, 100, ts, ti, ws=ws, stream=stream), stream)
         ok = bool((ti[:16, 0] == targets).all().item())
-        out[str(nq)] = {"plan": "streaming" if nq < 128 else "gemm", "ms": ms,
+        plan = ("streaming" if nq < 128 else
+                "gemm 128x512" if 1 <= nq % 256 <= 128 and nq <= 384 else "gemm 256x256")
+        out[str(nq)] = {"plan": plan, "ms": ms,
                         "pairs_per_s": nq * NS / (ms * 1e-3), **_hbm(NS * D * 2, ms),
                         **_mfma(2.0 * nq * NS * D, ms), "planted_rank1": ok}
     del G, ws

@@ -215,7 +215,172 @@ struct GemmCore {
   __device__ static inline int col_of(int j) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     return 128 * (wave & 1) + 16 * j + (lane & 15);
+  }  __device__ static inline int col_base() { return 128 * (int)((threadIdx.x >> 6) & 1); }
+};
+
+// Query-narrow block tile: 128 rows of A (queries) against 512 rows of B
+// (store rows), for products whose A side is a single 128-row tile, where the
+// 256 x 256 tile would compute a zero half.  Wave w holds the 128 x 128
+// sub-tile of all A rows and B rows [128 w, 128 w + 128), as 8 x 8 MFMA
+// accumulators, so the MFMA work per stage and the fragment reads per MFMA
+// are those of GemmCore; only the operand mix changes: a stage brings 16 KB
+// of A (shared by the four waves) and 64 KB of B (each wave loads and reads
+// only its own 16 KB), two slots filling the 160 KB of LDS.  Each wave reads
+// B through its own descriptor (its first row, its row count), so offsets
+// span 128 rows.  A wave issues 4 loads of A and 16 of B per stage (M0 set
+// once per 4), spread over the first loop of the step: two at each of the
+// first four issue points, one at each of the other twelve.  The pipeline
+// is GemmCore's: wait for stage s, barrier, MFMAs of h1 of stage s - 1
+// while reading h0 of s and loading s + 1 into the freed slot, then MFMAs
+// of h0 of s while reading h1 of s.
+constexpr int GNQ = 128;                 // A rows per tile
+constexpr int GNR = 512;                 // B rows per tile (128 per wave)
+
+struct GemmSmemN {
+  i32x4 a[2][GNQ * 8];
+  i32x4 b[2][GNR * 8];
+};
+
+template <typename Tag>
+struct GemmCoreN {
+  f32x4 acc[8][8];
+
+  __device__ inline void zero() {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+
+  // n_st stages (K = 64 n_st): da covers the tile's A rows (stride lda), dbw
+  // this wave's B rows (stride ldb), both from their first row.  Rows outside
+  // a descriptor's range read as zeros; byte offsets fit 31 bits when 128
+  // rows of either operand span less than 1 GiB.
+  __device__ inline void run(GemmSmemN& sm, const i32x4& da, int64_t lda, const i32x4& dbw,
+                             int64_t ldb, int n_st) {
+    if (n_st <= 0) return;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
+    const int lr = lane >> 3;
+    const int lc = (lane & 7) ^ lr;
+    // A: rows 32 wave + 8 u + lane / 8 (u = 0..3); B: the wave's rows
+    // 32 g + 8 u + lane / 8 (g = 0..3)
+    const uint32_t a_off = (uint32_t)((int64_t)(32 * wave + lr) * lda * 2 + lc * 16);
+    const uint32_t b_off = (uint32_t)((int64_t)lr * ldb * 2 + lc * 16);
+    const uint32_t a8 = (uint32_t)(8 * lda * 2), b8 = (uint32_t)(8 * ldb * 2);
+    const uint32_t lds_a = (uint32_t)(uintptr_t)&sm.a[0][0] + (uint32_t)(32 * wave) * 128u;
+    const uint32_t lds_b = (uint32_t)(uintptr_t)&sm.b[0][0] + (uint32_t)(128 * wave) * 128u;
+    constexpr uint32_t SLOT_A = GNQ * 128, SLOT_B = GNR * 128;
+    // load n (0..19) of stage st: group n / 4 (0: A, 1-4: B), member n % 4
+    auto issue = [&](int st, int n) {
+      const int g = n >> 2, u = n & 3;
+      const uint32_t ko = (uint32_t)st * 128u + (st < n_st ? 0u : 0x80000000u);
+      if (u == 0)
+        set_m0(g == 0 ? lds_a + (uint32_t)(st & 1) * SLOT_A
+                      : lds_b + (uint32_t)(st & 1) * SLOT_B + (uint32_t)(g - 1) * 4096u);
+      const uint32_t voff = g == 0 ? a_off + (uint32_t)u * a8 + ko
+                                   : b_off + (uint32_t)(4 * (g - 1) + u) * b8 + ko;
+      const i32x4& d = g == 0 ? da : dbw;
+      switch (u) {
+        case 0: lds_dma16_m0<0>(d, voff); break;
+        case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
+        case 2: lds_dma16_m0<2048>(d, voff - 2048u); break;
+        default: lds_dma16_m0<3072>(d, voff - 3072u); break;
+      }
+    };
+    // issue point p (0..15) of a step takes loads [first(p), first(p + 1))
+    auto first = [](int p) { return p < 4 ? 2 * p : p + 4; };
+    auto issue_point = [&](int st, int p) {
+#pragma unroll
+      for (int n = first(p); n < first(p + 1); ++n) issue(st, n);
+    };
+    const int ri = lane & 15, rg = lane >> 4;
+    const int fa0 = ri * 8, fb0 = (128 * wave + ri) * 8;
+    const int fs0 = rg ^ (ri & 7), fs1 = (4 + rg) ^ (ri & 7);
+    auto read_pair = [&](int i, const i32x4* pa, const i32x4* pb, int fs, i32x4 (&fa)[8],
+                         i32x4 (&fb)[8]) {
+      if (i < 4) {
+        fb[2 * i] = pb[fb0 + 128 * (2 * i) + fs];
+        fb[2 * i + 1] = pb[fb0 + 128 * (2 * i + 1) + fs];
+      } else {
+        fa[2 * i - 8] = pa[fa0 + 128 * (2 * i - 8) + fs];
+        fa[2 * i - 7] = pa[fa0 + 128 * (2 * i - 7) + fs];
+      }
+    };
+    auto mma_row = [&](int i, const i32x4 (&fa)[8], const i32x4 (&fb)[8]) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = mma16(Tag{}, fa[i], fb[j], acc[i][j]);
+    };
+    i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
+
+    // prologue: stage 0 in, stage 1 on its way, h0 of stage 0 in registers
+#pragma unroll
+    for (int n = 0; n < 20; ++n) issue(0, n);
+    gemm_wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+#pragma unroll
+    for (int n = 0; n < 20; ++n) issue(1, n);
+    {
+      const i32x4* pa = sm.a[0];
+      const i32x4* pb = sm.b[0];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        h0a[i] = pa[fa0 + 128 * i + fs0];
+        h0b[i] = pb[fb0 + 128 * i + fs0];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, pa, pb, fs1, h1a, h1b);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_row(i, h0a, h0b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    for (int st = 1; st < n_st; ++st) {
+      gemm_wait_vm<0>();
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+      const i32x4* pa = sm.a[st & 1];
+      const i32x4* pb = sm.b[st & 1];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, pa, pb, fs0, h0a, h0b);
+        issue_point(st + 1, 2 * i);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
+        issue_point(st + 1, 2 * i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, pa, pb, fs1, h1a, h1b);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_row(i, h0a, h0b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);
+    gemm_wait_vm<0>();
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+  }
+
+  // Row (A) / column (B) of accumulator element (i, j, r) for this lane.
+  __device__ static inline int row_of(int i, int r) {
+    const int lane = threadIdx.x & 63;
+    return 16 * i + 4 * (lane >> 4) + r;
+  }
+  __device__ static inline int col_of(int j) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    return 128 * wave + 16 * j + (lane & 15);
+  }
+  __device__ static inline int col_base() { return 128 * (int)(threadIdx.x >> 6); }
 };
 
 // The same block tile for K-major operands: C[m][n] += sum_k AT[k][m] BT[k][n]

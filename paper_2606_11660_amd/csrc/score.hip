@@ -530,6 +530,57 @@ __device__ inline float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), C, 0xf, 0xf, false));
 }
 
+// Epilogue of a score tile.  A wave's 128 columns are two 64-row segments of
+// the chunk (accumulator columns j < 4 and j >= 4); the 16 lanes that share
+// a query row reduce each segment's maximum, which is stored for the
+// selection.  With a bound from earlier chunks (running k-th best score of
+// the query), a segment whose maximum is below it cannot contribute and is
+// not written.  bound(row) gives the bound of the tile's query row.
+template <typename Core, typename Bound>
+__device__ inline void score_tile_store(const Core& core, int64_t q0, int64_t nq, int64_t c0,
+                                        int64_t nr, float* __restrict__ S, int64_t lds,
+                                        float* __restrict__ segmax, int64_t n_seg, Bound bound) {
+  const int lane = threadIdx.x & 63;
+  const int64_t seg0 = c0 / RS_SEG + Core::col_base() / RS_SEG;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = Core::row_of(i, r);
+      float m[2];
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        float v = -__builtin_inff();
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          if (Core::col_of(4 * g + jj) < nr) v = fmaxf(v, core.acc[i][4 * g + jj][r]);
+        // rotations within each row of 16 lanes (DPP row_ror 8, 4, 2, 1)
+        v = fmaxf(v, dpp_f<0x128>(v));
+        v = fmaxf(v, dpp_f<0x124>(v));
+        v = fmaxf(v, dpp_f<0x122>(v));
+        v = fmaxf(v, dpp_f<0x121>(v));
+        m[g] = v;
+      }
+      if (row < nq) {
+        const float b = bound(row);
+        if ((lane & 15) == 0) {
+          segmax[(q0 + row) * n_seg + seg0] = m[0];
+          segmax[(q0 + row) * n_seg + seg0 + 1] = m[1];
+        }
+        float* dst = S + (q0 + row) * lds + c0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int col = Core::col_of(j);
+          if (col < nr && !(m[j >> 2] < b)) dst[col] = core.acc[i][j][r];
+        }
+      }
+    }
+}
+
+// Scores of one chunk of store rows: items are (query tile, row tile) pairs.
+// XCD x (workgroup b goes to XCD b % 8) takes a contiguous range of items,
+// query tile fastest: the query tiles of one row tile read the same store
+// rows through the same L2.
 template <typename Tag>
 __global__ __launch_bounds__(256) void score_gemm_kernel(
     const _Float16* __restrict__ Q, int64_t n_q, int64_t ldq, const _Float16* __restrict__ G,
@@ -537,9 +588,6 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(
     float* __restrict__ S, int64_t lds, float* __restrict__ segmax, int64_t n_seg,
     const float* __restrict__ thr, int use_bound) {
   __shared__ GemmSmem sm;
-  // XCD x (workgroup b goes to XCD b % 8) takes a contiguous range of
-  // (query tile fastest, row tile) items: the query tiles of one row tile
-  // read the same store rows through the same L2
   const int item = (int)(blockIdx.x & 7u) * per_xcd + (int)(blockIdx.x >> 3);
   if (item >= n_items) return;  // uniform
   const int qt = item % n_qt, rt = item / n_qt;
@@ -555,46 +603,37 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(
   GemmCore<Tag> core;
   core.zero();
   core.run(sm, dq, ldq, dg, dg, ldg, n_st, n_st);
-  // Epilogue.  A wave's 128 columns are two 64-row segments of the chunk
-  // (accumulator columns j < 4 and j >= 4); the 16 lanes that share a query
-  // row reduce each segment's maximum, which is stored for the selection.
-  // With a bound from earlier chunks (running k-th best score of the query),
-  // a segment whose maximum is below it cannot contribute and is not written.
-  const int lane = threadIdx.x & 63;
-  const int64_t seg0 = c0 / RS_SEG + 2 * ((threadIdx.x >> 6) & 1);
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = GemmCore<Tag>::row_of(i, r);
-      float m[2];
-#pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        float v = -__builtin_inff();
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj)
-          if (GemmCore<Tag>::col_of(4 * g + jj) < nr) v = fmaxf(v, core.acc[i][4 * g + jj][r]);
-        // rotations within each row of 16 lanes (DPP row_ror 8, 4, 2, 1)
-        v = fmaxf(v, dpp_f<0x128>(v));
-        v = fmaxf(v, dpp_f<0x124>(v));
-        v = fmaxf(v, dpp_f<0x122>(v));
-        v = fmaxf(v, dpp_f<0x121>(v));
-        m[g] = v;
-      }
-      if (row < nq) {
-        const float b = tb[row];
-        if ((lane & 15) == 0) {
-          segmax[(q0 + row) * n_seg + seg0] = m[0];
-          segmax[(q0 + row) * n_seg + seg0 + 1] = m[1];
-        }
-        float* dst = S + (q0 + row) * lds + c0;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int col = GemmCore<Tag>::col_of(j);
-          if (col < nr && !(m[j >> 2] < b)) dst[col] = core.acc[i][j][r];
-        }
-      }
-    }
+  score_tile_store(core, q0, nq, c0, nr, S, lds, segmax, n_seg, [&](int row) { return tb[row]; });
+}
+
+// The same with 128-query x 512-row tiles (GemmCoreN): for query counts whose
+// last 256-query tile would be at most half used.
+template <typename Tag>
+__global__ __launch_bounds__(256) void score_gemm_n_kernel(
+    const _Float16* __restrict__ Q, int64_t n_q, int64_t ldq, const _Float16* __restrict__ G,
+    int64_t nc, int64_t ldg, int n_qt, int n_items, int per_xcd, int n_st,
+    float* __restrict__ S, int64_t lds, float* __restrict__ segmax, int64_t n_seg,
+    const float* __restrict__ thr, int use_bound) {
+  __shared__ GemmSmemN sm;
+  const int item = (int)(blockIdx.x & 7u) * per_xcd + (int)(blockIdx.x >> 3);
+  if (item >= n_items) return;  // uniform
+  const int qt = item % n_qt, rt = item / n_qt;
+  const int64_t q0 = (int64_t)qt * GNQ, c0 = (int64_t)rt * GNR;
+  int64_t nq = n_q - q0, nr = nc - c0;
+  nq = nq > GNQ ? GNQ : nq;
+  nr = nr > GNR ? GNR : nr;
+  // this wave's 128 store rows
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  int64_t nw = nr - 128 * wave;
+  nw = nw < 0 ? 0 : (nw > 128 ? 128 : nw);
+  const i32x4 dq = make_desc(Q + q0 * ldq, (uint32_t)(nq * ldq * 2));
+  const i32x4 dg = make_desc(G + (c0 + 128 * wave) * ldg, (uint32_t)(nw * ldg * 2));
+  GemmCoreN<Tag> core;
+  core.zero();
+  core.run(sm, dq, ldq, dg, ldg, n_st);
+  // (the two LDS slots fill the 160 KB: bounds come from memory)
+  score_tile_store(core, q0, nq, c0, nr, S, lds, segmax, n_seg,
+                   [&](int row) { return use_bound ? thr[q0 + row] : -__builtin_inff(); });
 }
 
 // Order-preserving key of a float (larger float, larger key).  Selectable
@@ -1304,15 +1343,22 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     // GEMM plan: score chunks of at most ~256 MB (MALL-resident between the
     // GEMM and the selection) and 128K rows, at most 255 chunks (the merge
     // takes 256 sources)
+    // Tiles: 256 x 256, or 128 queries x 512 rows where the last 256-query
+    // tile would be at most half used (n_q % 256 in [1, 128]) and the query
+    // count is small enough that store rows, not queries, set the work (the
+    // narrow tile reads each store row once per 128 queries).
+    const int64_t rem = n_q % 256;
+    const bool narrow = rem >= 1 && rem <= 128 && n_q <= 384;
+    const int64_t rt = narrow ? GNR : GT;
     int64_t chunk = ((int64_t)256 << 20) / (n_q * 4);
     chunk = chunk > 131072 ? 131072 : chunk;  // <= 32 rows per threshold sample
     const int64_t min_chunk = (n_g + 254) / 255;
     chunk = chunk < min_chunk ? min_chunk : chunk;
     chunk = chunk < 4096 ? 4096 : chunk;
-    chunk = (chunk + GT - 1) / GT * GT;
-    const int64_t all = (n_g + GT - 1) / GT * GT;
+    chunk = (chunk + rt - 1) / rt * rt;
+    const int64_t all = (n_g + rt - 1) / rt * rt;
     chunk = chunk > all ? all : chunk;
-    P.gemm = 1;
+    P.gemm = narrow ? 2 : 1;
     P.chunk = chunk;
     P.n_parts = (int)((n_g + chunk - 1) / chunk);
     P.rows_per_part = chunk;
@@ -1391,7 +1437,8 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
                              float* part_s, int64_t* part_i, float* spart, hipStream_t s) {
   const int n_parts = n_g > 0 ? plan.n_parts : 0;
   if (n_g > 0 && plan.gemm) {
-    const int n_qt = (int)((n_q + GT - 1) / GT);
+    const int tq = plan.gemm == 2 ? GNQ : GT, tr = plan.gemm == 2 ? GNR : GT;
+    const int n_qt = (int)((n_q + tq - 1) / tq);
     const int n_st = plan.n_grp;  // 64-element fp16 stages (128 bytes)
     const int64_t n_seg = plan.chunk / RS_SEG;
     float* segmax = spart + n_q * plan.chunk;
@@ -1399,12 +1446,12 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
     for (int c = 0; c < plan.n_parts; ++c) {
       const int64_t r0 = (int64_t)c * plan.chunk;
       const int64_t nc = n_g - r0 < plan.chunk ? n_g - r0 : plan.chunk;
-      const int n_items = n_qt * (int)((nc + GT - 1) / GT);
+      const int n_items = n_qt * (int)((nc + tr - 1) / tr);
       const int per_xcd = (n_items + 7) / 8;
-      hipLaunchKernelGGL(score_gemm_kernel<F16Tag>, dim3((unsigned)(8 * per_xcd)), dim3(256), 0, s,
-                         (const _Float16*)Q, n_q, ldq, (const _Float16*)G + r0 * ldg, nc, ldg, n_qt,
-                         n_items, per_xcd, n_st, spart, plan.chunk, segmax, n_seg,
-                         (const float*)thr, c > 0 ? 1 : 0);
+      hipLaunchKernelGGL(plan.gemm == 2 ? score_gemm_n_kernel<F16Tag> : score_gemm_kernel<F16Tag>,
+                         dim3((unsigned)(8 * per_xcd)), dim3(256), 0, s, (const _Float16*)Q, n_q,
+                         ldq, (const _Float16*)G + r0 * ldg, nc, ldg, n_qt, n_items, per_xcd, n_st,
+                         spart, plan.chunk, segmax, n_seg, (const float*)thr, c > 0 ? 1 : 0);
       hipLaunchKernelGGL(score_rselect_kernel, dim3((unsigned)n_q), dim3(256), 0, s,
                          (const float*)spart, plan.chunk, (const float*)segmax, n_seg, thr, nc, k, c,
                          plan.n_parts, index_base + r0, part_s, part_i);

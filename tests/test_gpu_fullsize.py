@@ -9,7 +9,8 @@ times.
   under the same M; whitening the store without normalisation and
   accumulating again gives N I.
 * Store scan, 4M x 8192 unit store, top-100, on every plan the bench runs
-  (Q = 16 and 64 streaming with the prefix bound, Q = 1024 GEMM): for 8
+  (Q = 16 and 64 streaming with the prefix bound; Q = 128 GEMM with
+  128-query tiles, Q = 200 and 1024 GEMM with 256-query tiles): for 8
   queries per plan, planted near-duplicates and random queries, the oracle's
   complete answer over all 4M rows (scores of every row, read back in
   65,536-row chunks) against the returned lists, with the gap rule.
@@ -157,8 +158,9 @@ def test_preconditioner_full_config_end_to_end():
 
 
 def test_store_scan_full_config():
-    """4M x 8192 unit fp16 store (65.5 GB), top-100, three plans on one
-    store: Q = 16 and Q = 64 (streaming, prefix bound), Q = 1024 (GEMM).
+    """4M x 8192 unit fp16 store (65.5 GB), top-100, five query counts on
+    one store: Q = 16 and Q = 64 (streaming, prefix bound), Q = 128 (GEMM,
+    128 x 512 tiles), Q = 200 and Q = 1024 (GEMM, 256 x 256 tiles).
     The first min(16, Q / 2) queries are planted near-duplicates (cosine 0.9)
     of known rows and must rank them first; for 8 queries per plan (planted
     and random) the returned lists are checked against the oracle's scores
@@ -169,7 +171,7 @@ def test_store_scan_full_config():
     gen = torch.Generator(device="cuda")
     gen.manual_seed(22)
     got, Qs, picks = {}, {}, {}
-    for nq in (16, 64, 1024):
+    for nq in (16, 64, 128, 200, 1024):
         n_pl = min(16, nq // 2)
         targets = np.random.default_rng(4).choice(n, n_pl, replace=False)
         q = torch.randn((nq, D), generator=gen, device="cuda")
@@ -194,7 +196,7 @@ def test_store_scan_full_config():
     # the oracle's lookup over every row, chunk by chunk (exact fp64 values
     # of the fp16 rows, top-(k + 1) per chunk merged across chunks), and its
     # scores of the returned rows
-    Qall = np.concatenate([Qs[nq] for nq in (16, 64, 1024)])
+    Qall = np.concatenate([Qs[nq] for nq in (16, 64, 128, 200, 1024)])
     ref_s = np.full((Qall.shape[0], k + 1), -np.inf)
     ref_i = np.full((Qall.shape[0], k + 1), -1, dtype=np.int64)
     for lo in range(0, n, 65536):
@@ -203,7 +205,7 @@ def test_store_scan_full_config():
         cs, ci = O.score_topk(Qall, Gc, k + 1, index_base=lo)
         ref_s, ref_i = O.merge_topk(ref_s, ref_i, cs, ci, k + 1)
     at = 0
-    for nq in (16, 64, 1024):
+    for nq in (16, 64, 128, 200, 1024):
         m = len(picks[nq])
         gs, gi = got[nq]
         say(f"  oracle check nq={nq}: queries {picks[nq].tolist()}")
