@@ -32,7 +32,9 @@ __all__ = [
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_PKG, "libattr.so")
+# ATTR_LIBRARY selects another build of the same library (the host-sanitizer
+# build of the CPU tests); by default the in-tree libattr.so.
+_LIB_PATH = os.environ.get("ATTR_LIBRARY") or os.path.join(_PKG, "libattr.so")
 
 ATTR_F32, ATTR_BF16, ATTR_F16 = 0, 1, 2
 PRECOND_NONE, PRECOND_DIAG, PRECOND_FULL = 0, 1, 2

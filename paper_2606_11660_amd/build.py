@@ -55,35 +55,88 @@ def _sgprs(tok: str) -> set:
     return {int(m.group(1))} if m else set()
 
 
+# VALU instructions whose second operand is an SGPR destination (VOP3b
+# carry-out / condition outputs); the first operand of any VALU instruction
+# is its destination.
+_VOP3B_SDST = re.compile(r"^v_(?:add_co|sub_co|subrev_co|addc_co|subb_co|subbrev_co)_u32"
+                         r"|^v_div_scale_f(?:32|64)|^v_mad_(?:u64_u32|i64_i32)")
+_BRANCH = re.compile(r"^s_(?:cbranch_\w+|branch)\s+(\S+)")
+_NO_FALLTHROUGH = ("s_branch", "s_endpgm", "s_setpc_b64")
+
+
+def _operands(line: str) -> list:
+    parts = line.split(None, 1)
+    return [t.strip() for t in parts[1].split(",")] if len(parts) > 1 else []
+
+
+def _valu_sgpr_dests(line: str) -> set:
+    op = line.split()[0]
+    ops = _operands(line)
+    out = _sgprs(ops[0]) if ops else set()
+    if _VOP3B_SDST.match(op) and len(ops) > 1:
+        out |= _sgprs(ops[1])
+    return out
+
+
 def lds_dma_hazards(asm: str) -> list:
     """Direct-to-LDS buffer loads come from inline asm, which the compiler's
-    hazard recognizer does not look into: a VALU instruction that writes one of
-    the load's descriptor SGPRs needs five wait states before the load reads
-    it.  Returns a description of every load in `asm` (device assembly)
-    without them."""
+    hazard recognizer does not look into.  Two hazards are checked:
+    * a VALU instruction that writes one of the load's descriptor SGPRs (as
+      its destination, or as the carry / condition output of a VOP3b form)
+      needs five wait states before the load reads it;
+    * an instruction that writes M0 needs one wait state before the load.
+    Wait states are counted backwards along every path into the load: through
+    a label into each branch that targets it (loop back-edges included) and
+    into the fall-through predecessor, with one wait state per instruction
+    and N + 1 per s_nop N.  Returns a description of every violation found
+    in `asm` (device assembly)."""
     lines = [l.strip() for l in asm.splitlines()]
+    preds = {}
+    for i, l in enumerate(lines):
+        m = _BRANCH.match(l)
+        if m:
+            preds.setdefault(m.group(1), []).append(i)
     found, kernel = [], "?"
     for idx, line in enumerate(lines):
         if re.match(r"^_Z\S+:", line):
             kernel = line[:-1]
         if "buffer_load_dword" not in line or " lds" not in line:
             continue
-        desc = _sgprs(line.split(",")[1].strip())
-        ws, j = 0, idx - 1
-        while j >= 0 and ws < 5:
-            prev = lines[j]
-            j -= 1
-            if not prev or prev.startswith((";", ".")) or prev.endswith(":"):
-                continue
-            op = prev.split()[0]
-            if op == "s_nop":
-                ws += int(prev.split()[1], 0) + 1
-                continue
-            if op.startswith("v_") and _sgprs(prev.split()[1].rstrip(",")) & desc:
-                found.append(f"{kernel}: '{prev}' {ws} wait states before '{line}'")
-                break
-            ws += 1
-    return found
+        desc = _sgprs(_operands(line)[1])
+        # (line index, wait states so far, reached by a jump from that line)
+        stack, seen = [(idx - 1, 0, False)], set()
+        while stack:
+            j, ws, jumped = stack.pop()
+            while j >= 0 and ws < 5:
+                if (j, ws, jumped) in seen:
+                    break
+                seen.add((j, ws, jumped))
+                prev = lines[j]
+                if prev.endswith(":"):
+                    if not prev.startswith("."):
+                        break  # function entry: no predecessor
+                    stack.extend((b, ws, True) for b in preds.get(prev[:-1], []))
+                    j -= 1
+                    continue
+                if not prev or prev.startswith((";", ".")):
+                    j -= 1
+                    continue
+                op = prev.split()[0]
+                if op in _NO_FALLTHROUGH and not jumped:
+                    break  # control does not fall through into the code below
+                jumped = False
+                if op == "s_nop":
+                    ws += int(prev.split()[1], 0) + 1
+                    j -= 1
+                    continue
+                ops = _operands(prev)
+                if ws < 1 and ops and ops[0] == "m0":
+                    found.append(f"{kernel}: '{prev}' writes M0 {ws} wait states before '{line}'")
+                if op.startswith("v_") and _valu_sgpr_dests(prev) & desc:
+                    found.append(f"{kernel}: '{prev}' {ws} wait states before '{line}'")
+                ws += 1
+                j -= 1
+    return sorted(set(found))
 
 
 def build(verbose: bool = False) -> str:
@@ -122,6 +175,31 @@ def build(verbose: bool = False) -> str:
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)
     return LIB
+
+
+def build_host_sanitized(out: str | None = None) -> str:
+    """libattr with its C-ABI layer (api.cpp) compiled by g++ under
+    AddressSanitizer and UndefinedBehaviorSanitizer, linked with the device
+    objects of the last build().  Only the host argument checks, planning and
+    layout arithmetic are instrumented (kernels are not).  Load it with g++'s
+    libasan preloaded and the library path in ATTR_LIBRARY."""
+    gxx = shutil.which("g++")
+    if gxx is None:
+        raise RuntimeError("g++ not found")
+    out = out or os.path.join(BUILD, "libattr_hostsan.so")
+    dev_objs = [os.path.join(BUILD, s + ".o") for s in HIP_SOURCES]
+    missing = [o for o in dev_objs if not os.path.exists(o)]
+    if missing:
+        raise RuntimeError(f"device objects missing (run build() first): {missing}")
+    san = ["-fsanitize=address", "-fsanitize=undefined", "-fno-sanitize-recover=undefined",
+           "-fno-omit-frame-pointer"]
+    obj = out + ".api.o"
+    _run([gxx, "-O1", "-g", "-fPIC", "-std=c++17", *san, "-D__HIP_PLATFORM_AMD__",
+          f"-I{ROCM}/include", f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, "api.cpp"),
+          "-o", obj])
+    _run([gxx, "-shared", *san, obj, *dev_objs, f"-L{ROCM}/lib", "-lamdhip64",
+          f"-Wl,-rpath,{ROCM}/lib", "-o", out])
+    return out
 
 
 if __name__ == "__main__":
