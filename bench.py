@@ -443,7 +443,7 @@ def _row_store_scan(dev, stream, qs=(16, 64, 128, 200, 256, 1024)):
         ms = _median_ms(lambda: P.attr_score_topk(Q, G, 100, ts, ti, ws=ws, stream=stream), stream)
         ok = bool((ti[:16, 0] == targets).all().item())
         plan = ("streaming" if nq < 128 else
-                "gemm 128x512" if 1 <= nq % 256 <= 128 and nq <= 384 else "gemm 256x256")
+                "gemm 128x256 ring" if 1 <= nq % 256 <= 128 and nq <= 384 else "gemm 256x256")
         out[str(nq)] = {"plan": plan, "ms": ms,
                         "pairs_per_s": nq * NS / (ms * 1e-3), **_hbm(NS * D * 2, ms),
                         **_mfma(2.0 * nq * NS * D, ms), "planted_rank1": ok}

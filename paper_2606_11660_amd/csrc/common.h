@@ -89,6 +89,15 @@ __device__ inline void lds_dma16_m0(const i32x4& desc, uint32_t voff) {
                : "v"(voff), "s"(uniform_desc(desc)), "n"(OFF)
                : "memory");
 }
+// The same with the non-temporal cache policy (data read once).
+template <int OFF>
+__device__ inline void lds_dma16_m0_nt(const i32x4& desc, uint32_t voff) {
+  static_assert(OFF >= 0 && OFF < 4096, "12-bit instruction offset");
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen offset:%2 nt lds"
+               :
+               : "v"(voff), "s"(uniform_desc(desc)), "n"(OFF)
+               : "memory");
+}
 
 // s_waitcnt lgkmcnt(0) through the builtin, so that the compiler's own wait
 // insertion knows every LDS read before it has completed (an inline-asm wait

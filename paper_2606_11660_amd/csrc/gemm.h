@@ -25,7 +25,9 @@
 // step), the 32 fragment reads over all 128 (two per 8): issued in bursts
 // they fill the address and LDS command queues and stall the wave, and with
 // it the matrix core.  Rows outside the operand's
-// range read as zeros through the buffer descriptors' range check.
+// range read as zeros through the buffer descriptors' range check.  NT loads
+// B with the non-temporal cache policy, for a B that is read once (a stream
+// of store rows against a single tile of queries).
 #pragma once
 
 #include <type_traits>
@@ -48,7 +50,7 @@ __device__ inline void gemm_wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <typename Tag>
+template <typename Tag, bool NT = false>
 struct GemmCore {
   f32x4 acc[8][8];
 
@@ -96,6 +98,8 @@ struct GemmCore {
       const int h = 4 * (g & 1) + u;
       if (g < 2) {
         lds_dma16_m0<1024 * u>(da, a_off + h * a8 + ko - 1024u * u);
+      } else if (NT) {
+        lds_dma16_m0_nt<1024 * u>(sw ? db2 : db, b_off + h * b8 + ko - 1024u * u);
       } else {
         lds_dma16_m0<1024 * u>(sw ? db2 : db, b_off + h * b8 + ko - 1024u * u);
       }
@@ -215,48 +219,55 @@ struct GemmCore {
   __device__ static inline int col_of(int j) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     return 128 * (wave & 1) + 16 * j + (lane & 15);
-  }  __device__ static inline int col_base() { return 128 * (int)((threadIdx.x >> 6) & 1); }
+  }
+  static constexpr int NJ = 8;  // 16-column accumulator blocks per wave
+  __device__ static inline int col_base() { return 128 * (int)((threadIdx.x >> 6) & 1); }
 };
 
-// Query-narrow block tile: 128 rows of A (queries) against 512 rows of B
-// (store rows), for products whose A side is a single 128-row tile, where the
-// 256 x 256 tile would compute a zero half.  Wave w holds the 128 x 128
-// sub-tile of all A rows and B rows [128 w, 128 w + 128), as 8 x 8 MFMA
-// accumulators, so the MFMA work per stage and the fragment reads per MFMA
-// are those of GemmCore; only the operand mix changes: a stage brings 16 KB
-// of A (shared by the four waves) and 64 KB of B (each wave loads and reads
-// only its own 16 KB), two slots filling the 160 KB of LDS.  Each wave reads
-// B through its own descriptor (its first row, its row count), so offsets
-// span 128 rows.  A wave issues 4 loads of A and 16 of B per stage (M0 set
-// once per 4), spread over the first loop of the step: two at each of the
-// first four issue points, one at each of the other twelve.  The pipeline
-// is GemmCore's: wait for stage s, barrier, MFMAs of h1 of stage s - 1
-// while reading h0 of s and loading s + 1 into the freed slot, then MFMAs
-// of h0 of s while reading h1 of s.
-constexpr int GNQ = 128;                 // A rows per tile
-constexpr int GNR = 512;                 // B rows per tile (128 per wave)
+// Query-narrow ring tile: 128 rows of A (queries) against 256 rows of B
+// (store rows) with a three-slot LDS ring, for streaming a large B past a
+// small A.  Wave w holds all 128 A rows against B rows [64 w, 64 w + 64) as
+// 8 x 4 MFMA accumulators.  A slot holds one stage (K = 64): 16 KB of A and
+// 32 KB of B (144 KB for the ring).  The step of stage s waits only for
+// stage s (the loads of stage s + 1 stay in flight), crosses the barrier
+// (stage s visible; the slot of stage s - 1 free) and refills that slot with
+// stage s + 2 while the MFMAs run, so two stages are always on their way
+// from memory and the issue never drains: at one workgroup per CU a ring of
+// 256-row x 128-byte stages streams at ~7.1 TB/s, where waiting for every
+// load before issuing the next stage (the two-slot schedule) holds a read
+// stream to ~5 TB/s.  Each wave loads 4 KB of A and its own 8 KB of B per
+// stage (12 direct-to-LDS loads, M0 set once per 4), one load per issue
+// point over the first 12 of the 16 points of a step, and reads B through
+// its own descriptor.  Fragment reads, the two K-halves and their register
+// sets are GemmCore's.  NT loads B with the non-temporal cache policy (B
+// read once): at 2M x 8192 store rows and 128 queries that took the whole
+// scan from 6.42 to 5.64 ms (the data stream no longer competes with the
+// queries, which every workgroup re-reads, for cache).
+constexpr int GRQ = 128;                 // A rows per tile
+constexpr int GRR = 256;                 // B rows per tile (64 per wave)
+constexpr int GR_SLOTS = 3;
 
-struct GemmSmemN {
-  i32x4 a[2][GNQ * 8];
-  i32x4 b[2][GNR * 8];
+struct GemmSmemR {
+  i32x4 a[GR_SLOTS][GRQ * 8];
+  i32x4 b[GR_SLOTS][GRR * 8];
 };
 
-template <typename Tag>
-struct GemmCoreN {
-  f32x4 acc[8][8];
+template <typename Tag, bool NT = false>
+struct GemmCoreR {
+  f32x4 acc[8][4];
 
   __device__ inline void zero() {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
   // n_st stages (K = 64 n_st): da covers the tile's A rows (stride lda), dbw
-  // this wave's B rows (stride ldb), both from their first row.  Rows outside
-  // a descriptor's range read as zeros; byte offsets fit 31 bits when 128
-  // rows of either operand span less than 1 GiB.
-  __device__ inline void run(GemmSmemN& sm, const i32x4& da, int64_t lda, const i32x4& dbw,
+  // this wave's 64 B rows (stride ldb), both from their first row.  Rows
+  // outside a descriptor's range read as zeros; byte offsets fit 31 bits
+  // when 128 rows of either operand span less than 1 GiB.
+  __device__ inline void run(GemmSmemR& sm, const i32x4& da, int64_t lda, const i32x4& dbw,
                              int64_t ldb, int n_st) {
     if (n_st <= 0) return;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -264,123 +275,140 @@ struct GemmCoreN {
     const int lr = lane >> 3;
     const int lc = (lane & 7) ^ lr;
     // A: rows 32 wave + 8 u + lane / 8 (u = 0..3); B: the wave's rows
-    // 32 g + 8 u + lane / 8 (g = 0..3)
+    // 8 (4 g + u) + lane / 8 (g = 0, 1; u = 0..3)
     const uint32_t a_off = (uint32_t)((int64_t)(32 * wave + lr) * lda * 2 + lc * 16);
     const uint32_t b_off = (uint32_t)((int64_t)lr * ldb * 2 + lc * 16);
     const uint32_t a8 = (uint32_t)(8 * lda * 2), b8 = (uint32_t)(8 * ldb * 2);
     const uint32_t lds_a = (uint32_t)(uintptr_t)&sm.a[0][0] + (uint32_t)(32 * wave) * 128u;
-    const uint32_t lds_b = (uint32_t)(uintptr_t)&sm.b[0][0] + (uint32_t)(128 * wave) * 128u;
-    constexpr uint32_t SLOT_A = GNQ * 128, SLOT_B = GNR * 128;
-    // load n (0..19) of stage st: group n / 4 (0: A, 1-4: B), member n % 4
-    auto issue = [&](int st, int n) {
+    const uint32_t lds_b = (uint32_t)(uintptr_t)&sm.b[0][0] + (uint32_t)(64 * wave) * 128u;
+    constexpr uint32_t SLOT_A = GRQ * 128, SLOT_B = GRR * 128;
+    // load n (0..11) of stage st into slot sl: group n / 4 (0: A, 1-2: B),
+    // member n % 4; a stage past the end fetches nothing and zero-fills a
+    // slot that is not read again
+    auto issue = [&](int st, int sl, int n) {
       const int g = n >> 2, u = n & 3;
       const uint32_t ko = (uint32_t)st * 128u + (st < n_st ? 0u : 0x80000000u);
       if (u == 0)
-        set_m0(g == 0 ? lds_a + (uint32_t)(st & 1) * SLOT_A
-                      : lds_b + (uint32_t)(st & 1) * SLOT_B + (uint32_t)(g - 1) * 4096u);
+        set_m0(g == 0 ? lds_a + (uint32_t)sl * SLOT_A
+                      : lds_b + (uint32_t)sl * SLOT_B + (uint32_t)(g - 1) * 4096u);
       const uint32_t voff = g == 0 ? a_off + (uint32_t)u * a8 + ko
                                    : b_off + (uint32_t)(4 * (g - 1) + u) * b8 + ko;
-      const i32x4& d = g == 0 ? da : dbw;
-      switch (u) {
-        case 0: lds_dma16_m0<0>(d, voff); break;
-        case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
-        case 2: lds_dma16_m0<2048>(d, voff - 2048u); break;
-        default: lds_dma16_m0<3072>(d, voff - 3072u); break;
+      if (g == 0 || !NT) {
+        const i32x4& d = g == 0 ? da : dbw;
+        switch (u) {
+          case 0: lds_dma16_m0<0>(d, voff); break;
+          case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
+          case 2: lds_dma16_m0<2048>(d, voff - 2048u); break;
+          default: lds_dma16_m0<3072>(d, voff - 3072u); break;
+        }
+      } else {
+        switch (u) {
+          case 0: lds_dma16_m0_nt<0>(dbw, voff); break;
+          case 1: lds_dma16_m0_nt<1024>(dbw, voff - 1024u); break;
+          case 2: lds_dma16_m0_nt<2048>(dbw, voff - 2048u); break;
+          default: lds_dma16_m0_nt<3072>(dbw, voff - 3072u); break;
+        }
       }
-    };
-    // issue point p (0..15) of a step takes loads [first(p), first(p + 1))
-    auto first = [](int p) { return p < 4 ? 2 * p : p + 4; };
-    auto issue_point = [&](int st, int p) {
-#pragma unroll
-      for (int n = first(p); n < first(p + 1); ++n) issue(st, n);
     };
     const int ri = lane & 15, rg = lane >> 4;
-    const int fa0 = ri * 8, fb0 = (128 * wave + ri) * 8;
+    const int fa0 = ri * 8, fb0 = (64 * wave + ri) * 8;
     const int fs0 = rg ^ (ri & 7), fs1 = (4 + rg) ^ (ri & 7);
-    auto read_pair = [&](int i, const i32x4* pa, const i32x4* pb, int fs, i32x4 (&fa)[8],
-                         i32x4 (&fb)[8]) {
-      if (i < 4) {
+    // the 12 fragments of a half: B (4) in calls 0-1, A (8) in calls 2-5
+    auto read_set = [&](int i, const i32x4* pa, const i32x4* pb, int fs, i32x4 (&fa)[8],
+                        i32x4 (&fb)[4]) {
+      if (i < 2) {
         fb[2 * i] = pb[fb0 + 128 * (2 * i) + fs];
         fb[2 * i + 1] = pb[fb0 + 128 * (2 * i + 1) + fs];
-      } else {
-        fa[2 * i - 8] = pa[fa0 + 128 * (2 * i - 8) + fs];
-        fa[2 * i - 7] = pa[fa0 + 128 * (2 * i - 7) + fs];
+      } else if (i < 6) {
+        fa[2 * i - 4] = pa[fa0 + 128 * (2 * i - 4) + fs];
+        fa[2 * i - 3] = pa[fa0 + 128 * (2 * i - 3) + fs];
       }
     };
-    auto mma_row = [&](int i, const i32x4 (&fa)[8], const i32x4 (&fb)[8]) {
+    auto mma_row = [&](int i, const i32x4 (&fa)[8], const i32x4 (&fb)[4]) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[i][j] = mma16(Tag{}, fa[i], fb[j], acc[i][j]);
+      for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, fa[i], fb[j], acc[i][j]);
     };
-    i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
+    i32x4 h0a[8], h0b[4], h1a[8], h1b[4];
 
-    // prologue: stage 0 in, stage 1 on its way, h0 of stage 0 in registers
+    // prologue: stages 0 and 1 on their way, stage 0 landed, stage 2 issued
+    // into the third slot, h0 of stage 0 in registers
 #pragma unroll
-    for (int n = 0; n < 20; ++n) issue(0, n);
-    gemm_wait_vm<0>();
+    for (int n = 0; n < 12; ++n) issue(0, 0, n);
+#pragma unroll
+    for (int n = 0; n < 12; ++n) issue(1, 1, n);
+    gemm_wait_vm<12>();
     __builtin_amdgcn_s_barrier();
 #pragma unroll
-    for (int n = 0; n < 20; ++n) issue(1, n);
+    for (int n = 0; n < 12; ++n) issue(2, 2, n);
     {
       const i32x4* pa = sm.a[0];
       const i32x4* pb = sm.b[0];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        h0a[i] = pa[fa0 + 128 * i + fs0];
-        h0b[i] = pb[fb0 + 128 * i + fs0];
-      }
+      for (int i = 0; i < 8; ++i) h0a[i] = pa[fa0 + 128 * i + fs0];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) h0b[j] = pb[fb0 + 128 * j + fs0];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        read_pair(i, pa, pb, fs1, h1a, h1b);
+        read_set(i, pa, pb, fs1, h1a, h1b);
         __builtin_amdgcn_sched_barrier(0);
         mma_row(i, h0a, h0b);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    int sl = 1;  // slot of stage st
     for (int st = 1; st < n_st; ++st) {
-      gemm_wait_vm<0>();
+      // stage st landed (stage st + 1's loads may still be in flight); this
+      // wave's reads of stage st - 1 are complete
+      gemm_wait_vm<12>();
       wait_lgkm0();
       __builtin_amdgcn_s_barrier();
-      const i32x4* pa = sm.a[st & 1];
-      const i32x4* pb = sm.b[st & 1];
+      const int sl2 = sl == 0 ? 2 : sl - 1;  // slot of stage st - 1 = slot of st + 2
+      const i32x4* pa = sm.a[sl];
+      const i32x4* pb = sm.b[sl];
+      // h1 of stage st - 1, reading h0 of stage st, loading stage st + 2
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        read_pair(i, pa, pb, fs0, h0a, h0b);
-        issue_point(st + 1, 2 * i);
+        read_set(i, pa, pb, fs0, h0a, h0b);
+        if (2 * i < 12) issue(st + 2, sl2, 2 * i);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        for (int j = 0; j < 2; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
-        issue_point(st + 1, 2 * i + 1);
+        if (2 * i + 1 < 12) issue(st + 2, sl2, 2 * i + 1);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        for (int j = 2; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
+      // h0 of stage st, reading h1 of stage st
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        read_pair(i, pa, pb, fs1, h1a, h1b);
+        read_set(i, pa, pb, fs1, h1a, h1b);
         __builtin_amdgcn_sched_barrier(0);
         mma_row(i, h0a, h0b);
         __builtin_amdgcn_sched_barrier(0);
       }
+      sl = sl == 2 ? 0 : sl + 1;
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);
+    // the zero-filling loads past the end have landed and every wave's LDS
+    // reads are complete before the workgroup moves on
     gemm_wait_vm<0>();
     wait_lgkm0();
     __builtin_amdgcn_s_barrier();
   }
 
-  // Row (A) / column (B) of accumulator element (i, j, r) for this lane.
+  static constexpr int NJ = 4;  // 16-column accumulator blocks per wave
   __device__ static inline int row_of(int i, int r) {
     const int lane = threadIdx.x & 63;
     return 16 * i + 4 * (lane >> 4) + r;
   }
   __device__ static inline int col_of(int j) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    return 128 * wave + 16 * j + (lane & 15);
+    return 64 * wave + 16 * j + (lane & 15);
   }
-  __device__ static inline int col_base() { return 128 * (int)(threadIdx.x >> 6); }
+  __device__ static inline int col_base() { return 64 * (int)(threadIdx.x >> 6); }
 };
 
 // The same block tile for K-major operands: C[m][n] += sum_k AT[k][m] BT[k][n]

@@ -119,7 +119,7 @@ struct ScorePlan {
   int64_t rows_per_part;
   size_t spart_bytes;    // split-K partial scores / GEMM-plan score chunk
   size_t list_entries;   // n_q * n_parts * k
-  int gemm;              // GEMM plan (1: 256 x 256 tiles, 2: 128 x 512): row chunks of `chunk` rows, one list per chunk
+  int gemm;              // GEMM plan (1: 256 x 256 tiles, 2: 128 x 256 ring): row chunks of `chunk` rows, one list per chunk
   int64_t chunk;
   int64_t D;
   int64_t bound_rows;    // streaming plan: rows of the prefix scan that bounds the k-th best (0: none)

@@ -530,16 +530,18 @@ __device__ inline float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), C, 0xf, 0xf, false));
 }
 
-// Epilogue of a score tile.  A wave's 128 columns are two 64-row segments of
-// the chunk (accumulator columns j < 4 and j >= 4); the 16 lanes that share
-// a query row reduce each segment's maximum, which is stored for the
-// selection.  With a bound from earlier chunks (running k-th best score of
-// the query), a segment whose maximum is below it cannot contribute and is
-// not written.  bound(row) gives the bound of the tile's query row.
+// Epilogue of a score tile.  A wave's columns are 64-row segments of the
+// chunk (accumulator column blocks 4 g .. 4 g + 3 form segment g); the 16
+// lanes that share a query row reduce each segment's maximum, which is
+// stored for the selection.  With a bound from earlier chunks (running k-th
+// best score of the query), a segment whose maximum is below it cannot
+// contribute and is not written.  bound(row) gives the bound of the tile's
+// query row.
 template <typename Core, typename Bound>
 __device__ inline void score_tile_store(const Core& core, int64_t q0, int64_t nq, int64_t c0,
                                         int64_t nr, float* __restrict__ S, int64_t lds,
                                         float* __restrict__ segmax, int64_t n_seg, Bound bound) {
+  constexpr int NJ = Core::NJ, NG = NJ / 4;
   const int lane = threadIdx.x & 63;
   const int64_t seg0 = c0 / RS_SEG + Core::col_base() / RS_SEG;
 #pragma unroll
@@ -547,9 +549,9 @@ __device__ inline void score_tile_store(const Core& core, int64_t q0, int64_t nq
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = Core::row_of(i, r);
-      float m[2];
+      float m[NG];
 #pragma unroll
-      for (int g = 0; g < 2; ++g) {
+      for (int g = 0; g < NG; ++g) {
         float v = -__builtin_inff();
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj)
@@ -564,12 +566,12 @@ __device__ inline void score_tile_store(const Core& core, int64_t q0, int64_t nq
       if (row < nq) {
         const float b = bound(row);
         if ((lane & 15) == 0) {
-          segmax[(q0 + row) * n_seg + seg0] = m[0];
-          segmax[(q0 + row) * n_seg + seg0 + 1] = m[1];
+#pragma unroll
+          for (int g = 0; g < NG; ++g) segmax[(q0 + row) * n_seg + seg0 + g] = m[g];
         }
         float* dst = S + (q0 + row) * lds + c0;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < NJ; ++j) {
           const int col = Core::col_of(j);
           if (col < nr && !(m[j >> 2] < b)) dst[col] = core.acc[i][j][r];
         }
@@ -580,8 +582,9 @@ __device__ inline void score_tile_store(const Core& core, int64_t q0, int64_t nq
 // Scores of one chunk of store rows: items are (query tile, row tile) pairs.
 // XCD x (workgroup b goes to XCD b % 8) takes a contiguous range of items,
 // query tile fastest: the query tiles of one row tile read the same store
-// rows through the same L2.
-template <typename Tag>
+// rows through the same L2.  NT (a single query tile): every store row is
+// read once, with the non-temporal cache policy.
+template <typename Tag, bool NT>
 __global__ __launch_bounds__(256) void score_gemm_kernel(
     const _Float16* __restrict__ Q, int64_t n_q, int64_t ldq, const _Float16* __restrict__ G,
     int64_t nc, int64_t ldg, int n_qt, int n_items, int per_xcd, int n_st,
@@ -600,40 +603,43 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(
   // the tile's query bounds, staged in LDS (the main loop's barriers publish them)
   __shared__ float tb[GT];
   tb[threadIdx.x] = use_bound && q0 + threadIdx.x < n_q ? thr[q0 + threadIdx.x] : -__builtin_inff();
-  GemmCore<Tag> core;
+  GemmCore<Tag, NT> core;
   core.zero();
   core.run(sm, dq, ldq, dg, dg, ldg, n_st, n_st);
   score_tile_store(core, q0, nq, c0, nr, S, lds, segmax, n_seg, [&](int row) { return tb[row]; });
 }
 
-// The same with 128-query x 512-row tiles (GemmCoreN): for query counts whose
-// last 256-query tile would be at most half used.
-template <typename Tag>
-__global__ __launch_bounds__(256) void score_gemm_n_kernel(
+// The same with 128-query x 256-row tiles on the three-slot ring
+// (GemmCoreR): for query counts whose last 256-query tile would be at most
+// half used.
+template <typename Tag, bool NT>
+__global__ __launch_bounds__(256) void score_gemm_r_kernel(
     const _Float16* __restrict__ Q, int64_t n_q, int64_t ldq, const _Float16* __restrict__ G,
     int64_t nc, int64_t ldg, int n_qt, int n_items, int per_xcd, int n_st,
     float* __restrict__ S, int64_t lds, float* __restrict__ segmax, int64_t n_seg,
     const float* __restrict__ thr, int use_bound) {
-  __shared__ GemmSmemN sm;
+  __shared__ GemmSmemR sm;
   const int item = (int)(blockIdx.x & 7u) * per_xcd + (int)(blockIdx.x >> 3);
   if (item >= n_items) return;  // uniform
   const int qt = item % n_qt, rt = item / n_qt;
-  const int64_t q0 = (int64_t)qt * GNQ, c0 = (int64_t)rt * GNR;
+  const int64_t q0 = (int64_t)qt * GRQ, c0 = (int64_t)rt * GRR;
   int64_t nq = n_q - q0, nr = nc - c0;
-  nq = nq > GNQ ? GNQ : nq;
-  nr = nr > GNR ? GNR : nr;
-  // this wave's 128 store rows
+  nq = nq > GRQ ? GRQ : nq;
+  nr = nr > GRR ? GRR : nr;
+  // this wave's 64 store rows
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  int64_t nw = nr - 128 * wave;
-  nw = nw < 0 ? 0 : (nw > 128 ? 128 : nw);
+  int64_t nw = nr - 64 * wave;
+  nw = nw < 0 ? 0 : (nw > 64 ? 64 : nw);
   const i32x4 dq = make_desc(Q + q0 * ldq, (uint32_t)(nq * ldq * 2));
-  const i32x4 dg = make_desc(G + (c0 + 128 * wave) * ldg, (uint32_t)(nw * ldg * 2));
-  GemmCoreN<Tag> core;
+  const i32x4 dg = make_desc(G + (c0 + 64 * wave) * ldg, (uint32_t)(nw * ldg * 2));
+  // the tile's query bounds, staged in LDS (the ring's barriers publish them)
+  __shared__ float tb[GRQ];
+  if (threadIdx.x < GRQ)
+    tb[threadIdx.x] = use_bound && q0 + threadIdx.x < n_q ? thr[q0 + threadIdx.x] : -__builtin_inff();
+  GemmCoreR<Tag, NT> core;
   core.zero();
   core.run(sm, dq, ldq, dg, ldg, n_st);
-  // (the two LDS slots fill the 160 KB: bounds come from memory)
-  score_tile_store(core, q0, nq, c0, nr, S, lds, segmax, n_seg,
-                   [&](int row) { return use_bound ? thr[q0 + row] : -__builtin_inff(); });
+  score_tile_store(core, q0, nq, c0, nr, S, lds, segmax, n_seg, [&](int row) { return tb[row]; });
 }
 
 // Order-preserving key of a float (larger float, larger key).  Selectable
@@ -1343,13 +1349,13 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     // GEMM plan: score chunks of at most ~256 MB (MALL-resident between the
     // GEMM and the selection) and 128K rows, at most 255 chunks (the merge
     // takes 256 sources)
-    // Tiles: 256 x 256, or 128 queries x 512 rows where the last 256-query
-    // tile would be at most half used (n_q % 256 in [1, 128]) and the query
-    // count is small enough that store rows, not queries, set the work (the
-    // narrow tile reads each store row once per 128 queries).
+    // Tiles: 256 x 256, or 128 queries x 256 rows (the ring core) where the
+    // last 256-query tile would be at most half used (n_q % 256 in [1, 128])
+    // and the query count is small enough that store rows, not queries, set
+    // the work (the narrow tile reads each store row once per 128 queries).
     const int64_t rem = n_q % 256;
     const bool narrow = rem >= 1 && rem <= 128 && n_q <= 384;
-    const int64_t rt = narrow ? GNR : GT;
+    const int64_t rt = narrow ? GRR : GT;
     int64_t chunk = ((int64_t)256 << 20) / (n_q * 4);
     chunk = chunk > 131072 ? 131072 : chunk;  // <= 32 rows per threshold sample
     const int64_t min_chunk = (n_g + 254) / 255;
@@ -1437,7 +1443,7 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
                              float* part_s, int64_t* part_i, float* spart, hipStream_t s) {
   const int n_parts = n_g > 0 ? plan.n_parts : 0;
   if (n_g > 0 && plan.gemm) {
-    const int tq = plan.gemm == 2 ? GNQ : GT, tr = plan.gemm == 2 ? GNR : GT;
+    const int tq = plan.gemm == 2 ? GRQ : GT, tr = plan.gemm == 2 ? GRR : GT;
     const int n_qt = (int)((n_q + tq - 1) / tq);
     const int n_st = plan.n_grp;  // 64-element fp16 stages (128 bytes)
     const int64_t n_seg = plan.chunk / RS_SEG;
@@ -1448,7 +1454,11 @@ hipError_t launch_score_topk(bool f16, const ScorePlan& plan, const void* Q, int
       const int64_t nc = n_g - r0 < plan.chunk ? n_g - r0 : plan.chunk;
       const int n_items = n_qt * (int)((nc + tr - 1) / tr);
       const int per_xcd = (n_items + 7) / 8;
-      hipLaunchKernelGGL(plan.gemm == 2 ? score_gemm_n_kernel<F16Tag> : score_gemm_kernel<F16Tag>,
+      const bool nt = n_qt == 1;
+      hipLaunchKernelGGL(plan.gemm == 2 ? (nt ? score_gemm_r_kernel<F16Tag, true>
+                                              : score_gemm_r_kernel<F16Tag, false>)
+                                        : (nt ? score_gemm_kernel<F16Tag, true>
+                                              : score_gemm_kernel<F16Tag, false>),
                          dim3((unsigned)(8 * per_xcd)), dim3(256), 0, s, (const _Float16*)Q, n_q,
                          ldq, (const _Float16*)G + r0 * ldg, nc, ldg, n_qt, n_items, per_xcd, n_st,
                          spart, plan.chunk, segmax, n_seg, (const float*)thr, c > 0 ? 1 : 0);

@@ -10,7 +10,7 @@ times.
   accumulating again gives N I.
 * Store scan, 4M x 8192 unit store, top-100, on every plan the bench runs
   (Q = 16 and 64 streaming with the prefix bound; Q = 128 GEMM with
-  128-query tiles, Q = 200 and 1024 GEMM with 256-query tiles): for 8
+  128-query ring tiles, Q = 200 and 1024 GEMM with 256-query tiles): for 8
   queries per plan, planted near-duplicates and random queries, the oracle's
   complete answer over all 4M rows (scores of every row, read back in
   65,536-row chunks) against the returned lists, with the gap rule.
@@ -160,7 +160,7 @@ def test_preconditioner_full_config_end_to_end():
 def test_store_scan_full_config():
     """4M x 8192 unit fp16 store (65.5 GB), top-100, five query counts on
     one store: Q = 16 and Q = 64 (streaming, prefix bound), Q = 128 (GEMM,
-    128 x 512 tiles), Q = 200 and Q = 1024 (GEMM, 256 x 256 tiles).
+    128 x 256 ring tiles), Q = 200 and Q = 1024 (GEMM, 256 x 256 tiles).
     The first min(16, Q / 2) queries are planted near-duplicates (cosine 0.9)
     of known rows and must rank them first; for 8 queries per plan (planted
     and random) the returned lists are checked against the oracle's scores
