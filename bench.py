@@ -583,7 +583,7 @@ def _profile_row(row, dev):
     """One row of the path on its own, for rocprofv3 counter runs, each
     operation PROFILE_REPS times: `llama1b` the headline projection call
     (batch 0: 32 examples, 43190 tokens, separate inputs), `gpt2` the
-    64-example GPT-2-shaped call, `syrk` a 500000 x 8192 accumulate (one full
+    64-example GPT-2-shaped call, `gpt2_tok` its per-token variant, `syrk` a 500000 x 8192 accumulate (one full
     launch), `full_apply` 131072 rows, `scan16` / `scan128` / `scan1024` a
     1M x 8192 store with top-100, `diag_acc` / `diag_apply` 10^6 x 8192."""
     import torch
@@ -598,12 +598,17 @@ def _profile_row(row, dev):
         for _ in range(PROFILE_REPS):
             P.attr_project(mods, wl.k, BATCH, wl.T, rows, row_offset=batches[0][0],
                            length=batches[0][1])
-    elif row == "gpt2":
+    elif row in ("gpt2", "gpt2_tok"):
         wl = synth.GPT2
         mods = _gpt2_modules(dev, 64)
-        rows = torch.empty((64, wl.D), dtype=torch.float32, device=dev)
-        for _ in range(PROFILE_REPS):
-            P.attr_project(mods, wl.k, 64, wl.T, rows)
+        if row == "gpt2":
+            rows = torch.empty((64, wl.D), dtype=torch.float32, device=dev)
+            for _ in range(PROFILE_REPS):
+                P.attr_project(mods, wl.k, 64, wl.T, rows)
+        else:
+            rows = torch.empty((64 * wl.T, wl.D), dtype=torch.float32, device=dev)
+            for _ in range(PROFILE_REPS):
+                P.attr_project_tokens(mods, wl.k, 64, wl.T, rows)
     elif row in ("diag_acc", "diag_apply"):
         X = _unit_store(dev, 1_000_000, 8192, seed=3)
         if row == "diag_acc":
@@ -686,7 +691,7 @@ def main():
     ap.add_argument("--quick", action="store_true", help="headline only (no other rows, no peaks)")
     ap.add_argument("--copy-reference", action="store_true",
                     help="only run the 1 GiB copy used to calibrate traffic counters")
-    ap.add_argument("--profile-row", choices=["llama1b", "gpt2", "syrk", "full_apply", "scan16",
+    ap.add_argument("--profile-row", choices=["llama1b", "gpt2", "gpt2_tok", "syrk", "full_apply", "scan16",
                                               "scan128", "scan1024", "diag_acc", "diag_apply",
                                               "kfac"],
                     help="only run one row of the path, for counter runs")

@@ -24,6 +24,7 @@
 //    each (module, example) in chunk order into the output row
 //    (deterministic, no atomics).
 #include <mutex>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -273,6 +274,24 @@ __device__ inline void project_side(__amdgpu_buffer_rsrc_t rsrc, int64_t ld, int
   }
 }
 
+// f(integral_constant<int, I>) for I = B .. E - 1, in order.
+template <int B, int E>
+struct StaticFor {
+  template <typename F>
+  __device__ static inline void run(F&& f) {
+    if constexpr (B < E) {
+      f(std::integral_constant<int, B>{});
+      StaticFor<B + 1, E>::run(f);
+    }
+  }
+};
+
+// v of lane N of this lane's row of 16 (DPP row_newbcast:N).
+template <int N>
+__device__ inline float row_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + N, 0xf, 0xf, false));
+}
+
 // One (group, token chunk, example) item, run by one workgroup.  A group
 // is MS modules (consecutive slots from s0) that share their input rows a:
 // the a tiles are read once and projected through each member's S; each
@@ -353,21 +372,24 @@ __device__ inline void project_item(const ProjTab* __restrict__ tab, int s0, uin
 
       if constexpr (TOK) {
         // register q of the stage-1 tiles holds token 16 tt + 4 (lane / 16) +
-        // q of the wave, column lane % 16: g~[t][r] comes from lane r % 16 of
-        // the same 16-lane group (every lane shuffles, only valid tokens store)
+        // q of the wave, column lane % 16: each 16-lane row writes its own
+        // token's block, taking g~[t][r] from lane r % 16 of the row by a DPP
+        // row broadcast (a VALU move: a shuffle through the LDS crossbar put
+        // its latency between every product and its store)
 #pragma unroll
         for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int tw = 16 * tt + 4 * (lane >> 4) + q;
-            const bool ok = tw < ntok && row0 + tw < n_rows;
-            float* orow = partial + (row0 + (ok ? tw : 0)) * ldo + md.out_col + (lane & 15);
+            if (tw < ntok && row0 + tw < n_rows) {  // whole 16-lane rows
+              float* orow = partial + (row0 + tw) * ldo + md.out_col + (lane & 15);
+              StaticFor<0, 16 * NK>::run([&](auto rc) {
+                constexpr int r = decltype(rc)::value;
+                const float gr = row_bcast<(r & 15)>(Gt[0][tt][r >> 4][q]);
 #pragma unroll
-            for (int r = 0; r < 16 * NK; ++r) {
-              const float gr = __shfl(Gt[0][tt][r >> 4][q], r & 15, 16);
-#pragma unroll
-              for (int ct = 0; ct < NK; ++ct)
-                if (ok) orow[r * 16 * NK + 16 * ct] = gr * At[m][tt][ct][q];
+                for (int ct = 0; ct < NK; ++ct)
+                  __builtin_nontemporal_store(gr * At[m][tt][ct][q], orow + r * 16 * NK + 16 * ct);
+              });
             }
           }
       } else {
