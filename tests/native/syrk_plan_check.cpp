@@ -9,11 +9,11 @@
 #include "syrk_plan.h"
 
 int main() {
-  const long long rows[] = {1, 63, 64, 1000, 8191, 8192, 16383, 16384, 24575, 100000, 262144,
-                            262145, 500000, 523264, 524288, 524289, 1000000, 1048576, 4000000,
-                            10000000};
-  const long long Ds[] = {64, 320, 2048, 8192, 32768};
-  const long long lds[] = {0, 64, 8192, 16384, 32768, 32832, 40000, 65536};
+  const long long rows[] = {1, 63, 64, 1000, 8191, 8192, 16383, 16384, 21900, 24575, 65536,
+                            100000, 131072, 200000, 262144, 262145, 300000, 500000, 523264,
+                            524288, 524289, 600000, 1000000, 1048576, 4000000, 10000000};
+  const long long Ds[] = {64, 320, 2048, 4096, 8192, 32768};
+  const long long lds[] = {0, 64, 8192, 16384, 20000, 32768, 32832, 40000, 50000, 65536};
   long long checked = 0;
   for (long long n : rows)
     for (long long D : Ds)
@@ -23,7 +23,8 @@ int main() {
         const attr::SyrkPlan Q = attr::plan_syrk(n, D, 0);
         const long long ld = ldx ? ldx : D;
         const long long n_chunks = (n + P.C - 1) / P.C;
-        bool ok = P.J >= 1 && P.J <= attr::kSyrkSlices && P.Cs % 64 == 0 && P.Cs >= 64 &&
+        bool ok = P.J >= 1 && P.J <= attr::kSyrkSlices && (P.J == 1 || P.J % 2 == 0) &&
+                  P.Cs % 64 == 0 && P.Cs >= 64 &&
                   P.C == P.Cs * P.J && n_chunks * P.C >= n && P.part_bytes <= Q.part_bytes &&
                   P.h64_bytes == Q.h64_bytes;
         if (ldx) ok = ok && P.Cs * ld * 2 <= (1ll << 31);
@@ -38,6 +39,16 @@ int main() {
   const attr::SyrkPlan W = attr::plan_syrk(524288, 8192, 65536);
   if (W.Cs * 65536ll * 2 > (1ll << 31)) {
     std::printf("violation: 524288 rows at ldx 65536 give %lld-row slices\n", (long long)W.Cs);
+    return 1;
+  }
+  // the cost model's choices on the workloads it was tuned for: 10^6 x 8192
+  // (two chunks of 16 slices of 31296 rows), K-FAC factors over 21900 rows
+  const attr::SyrkPlan A = attr::plan_syrk(1000000, 8192, 8192);
+  const attr::SyrkPlan B = attr::plan_syrk(21900, 2048, 2048);
+  const attr::SyrkPlan C = attr::plan_syrk(21900, 8192, 8192);
+  if (A.J != 16 || A.Cs != 31296 || B.J != 6 || C.J != 4) {
+    std::printf("unexpected plans: 10^6x8192 J=%d Cs=%lld, 21900x2048 J=%d, 21900x8192 J=%d\n", A.J,
+                (long long)A.Cs, B.J, C.J);
     return 1;
   }
   std::printf("ok %lld plans\n", checked);
