@@ -9,7 +9,8 @@
 // A_hi + A_lo equals A to about 22 significant bits: the preconditioner is
 // badly conditioned and an fp16 (or bf16) M alone perturbs the whitened
 // rows by percents.  Y = 2^-s X (A_hi + A_lo)^T is then one MFMA GEMM whose
-// K loop runs over A_hi and then over A_lo into the same fp32 accumulators;
+// K loop takes each 64-wide block of X against A_hi and then A_lo into the
+// same fp32 accumulators (X is read once);
 // the epilogue applies 2^-s, writes Y and per-row partial sums of squares
 // (from the fp32 values), which the row-scale kernel turns into the
 // unit-norm scale in a second pass.  With unit normalisation into an fp16
@@ -91,10 +92,9 @@ __global__ __launch_bounds__(256) void apply_full_kernel(
   const i32x4 dx = make_desc(X + r0 * ldx, (uint32_t)(nr * ldx * 2));
   const i32x4 dlo = make_desc(Mlo + c0 * D, (uint32_t)(nc * D * 2));
   const i32x4 dhi = make_desc(Mhi + c0 * D, (uint32_t)(nc * D * 2));
-  GemmCore<F16Tag> core;
+  GemmCoreHL<F16Tag> core;
   core.zero();
-  const int n_st = (int)(D / GKS);
-  core.run(sm, dx, ldx, dhi, dlo, D, n_st, 2 * n_st);
+  core.run(sm, dx, ldx, dhi, dlo, D, (int)(D / GKS));
   const float unscale = ldexpf(1.f, -split_exponent(*maxbits));
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -102,7 +102,7 @@ __global__ __launch_bounds__(256) void apply_full_kernel(
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = GemmCore<F16Tag>::row_of(i, r);
+      const int row = GemmCore<F16Tag>::row_of(i, r);  // same layout as GemmCoreHL
       float v[8];
       float ss = 0.f, mx = 0.f;
 #pragma unroll

@@ -224,6 +224,195 @@ struct GemmCore {
   __device__ static inline int col_base() { return 128 * (int)((threadIdx.x >> 6) & 1); }
 };
 
+// The 256 x 256 tile of GemmCore for C = A (B1 + B2)^T with the two B
+// operands interleaved per K-block: step 2 s multiplies A block s by B1
+// block s, step 2 s + 1 the same A block by B2 block s (one accumulator).
+// A block s is loaded into LDS once for both steps, with two steps to land
+// (it is issued in step 2 s - 2, after that step's B load, into the A slot
+// the pair before freed), and the odd step reuses the even step's A
+// fragments from registers, so per pair of steps the core issues 24 loads
+// and 48 fragment reads per wave instead of 32 and 64, and reads A from
+// memory once instead of once per B operand.  Otherwise the pipeline is
+// GemmCore's: wait for step t, barrier, MFMAs of h1 of step t - 1 while
+// reading h0 of t, then MFMAs of h0 of t while reading h1 of t.
+template <typename Tag>
+struct GemmCoreHL {
+  f32x4 acc[8][8];
+
+  __device__ inline void zero() {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // n_k K-blocks of 64 (2 n_k steps): A rows through da (stride lda), B1 and
+  // B2 rows through db1, db2 (stride ldb), all from the tile's first row.
+  // Rows outside a descriptor's range read as zeros; byte offsets must fit
+  // 31 bits.
+  __device__ inline void run(GemmSmem& sm, const i32x4& da, int64_t lda, const i32x4& db1,
+                             const i32x4& db2, int64_t ldb, int n_k) {
+    if (n_k <= 0) return;
+    const int n_t = 2 * n_k;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lr = lane >> 3;
+    const int lc = (lane & 7) ^ lr;
+    const uint32_t a_off = (uint32_t)((int64_t)(64 * wave + lr) * lda * 2 + lc * 16);
+    const uint32_t b_off = (uint32_t)((int64_t)(64 * wave + lr) * ldb * 2 + lc * 16);
+    const uint32_t a8 = (uint32_t)(8 * lda * 2), b8 = (uint32_t)(8 * ldb * 2);
+    const uint32_t lds_a = (uint32_t)(uintptr_t)&sm.a[0][0] + (uint32_t)(64 * wave) * 128u;
+    const uint32_t lds_b = (uint32_t)(uintptr_t)&sm.b[0][0] + (uint32_t)(64 * wave) * 128u;
+    // load n (0..7) of A block s (slot s & 1) or of B step t (slot t & 1):
+    // group n / 4 covers rows 32 (n / 4) .. + 31 of the wave's 64, member
+    // n % 4 lands at M0 + 1024 (n % 4); past the end nothing is fetched.
+    // The first load of a group is guarded: this core's register pressure
+    // leads the compiler to keep the descriptors in VGPRs and move them into
+    // SGPRs right before it.
+    auto load_a = [&](int s, int n) {
+      const int g = n >> 2, u = n & 3;
+      const uint32_t ko = (uint32_t)s * 128u + (s < n_k ? 0u : 0x80000000u);
+      if (u == 0) set_m0(lds_a + (uint32_t)(s & 1) * G_SLOT + (uint32_t)g * 4096u);
+      const uint32_t voff = a_off + (uint32_t)(4 * g + u) * a8 + ko;
+      switch (u) {
+        case 0: lds_dma16_m0_guarded<0>(da, voff); break;
+        case 1: lds_dma16_m0<1024>(da, voff - 1024u); break;
+        case 2: lds_dma16_m0<2048>(da, voff - 2048u); break;
+        default: lds_dma16_m0<3072>(da, voff - 3072u); break;
+      }
+    };
+    // d: db1 for even t, db2 for odd t (the caller knows the parity at
+    // compile time: a run-time choice put a VALU write of the descriptor
+    // right before the load)
+    auto load_b = [&](int t, int n, const i32x4& d) {
+      const int g = n >> 2, u = n & 3;
+      const int s = t >> 1;
+      const uint32_t ko = (uint32_t)s * 128u + (t < n_t ? 0u : 0x80000000u);
+      if (u == 0) set_m0(lds_b + (uint32_t)(t & 1) * G_SLOT + (uint32_t)g * 4096u);
+      const uint32_t voff = b_off + (uint32_t)(4 * g + u) * b8 + ko;
+      switch (u) {
+        case 0: lds_dma16_m0_guarded<0>(d, voff); break;
+        case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
+        case 2: lds_dma16_m0<2048>(d, voff - 2048u); break;
+        default: lds_dma16_m0<3072>(d, voff - 3072u); break;
+      }
+    };
+    const int ri = lane & 15, rg = lane >> 4;
+    const int fa0 = (128 * wm + ri) * 8, fb0 = (128 * wn + ri) * 8;
+    const int fs0 = rg ^ (ri & 7), fs1 = (4 + rg) ^ (ri & 7);
+    // the fragments of a half, two per call (B first); RA: also A's
+    auto read_pair = [&](int i, bool ra, const i32x4* pa, const i32x4* pb, int fs, i32x4 (&fa)[8],
+                         i32x4 (&fb)[8]) {
+      if (i < 4) {
+        fb[2 * i] = pb[fb0 + 128 * (2 * i) + fs];
+        fb[2 * i + 1] = pb[fb0 + 128 * (2 * i + 1) + fs];
+      } else if (ra) {
+        fa[2 * i - 8] = pa[fa0 + 128 * (2 * i - 8) + fs];
+        fa[2 * i - 7] = pa[fa0 + 128 * (2 * i - 7) + fs];
+      }
+    };
+    auto mma_row = [&](int i, const i32x4 (&fa)[8], const i32x4 (&fb)[8]) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[i][j] = mma16(Tag{}, fa[i], fb[j], acc[i][j]);
+    };
+    i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
+
+    // prologue: A block 0 and B step 0 in; B step 1 and A block 1 on their
+    // way; h0 of step 0 in registers, then h1 of step 0 read under the MFMAs
+    // of its h0
+#pragma unroll
+    for (int n = 0; n < 8; ++n) load_a(0, n);
+#pragma unroll
+    for (int n = 0; n < 8; ++n) load_b(0, n, db1);
+    gemm_wait_vm<0>();
+    __builtin_amdgcn_s_barrier();
+#pragma unroll
+    for (int n = 0; n < 8; ++n) load_b(1, n, db2);
+#pragma unroll
+    for (int n = 0; n < 8; ++n) load_a(1, n);
+    {
+      const i32x4* pa = sm.a[0];
+      const i32x4* pb = sm.b[0];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        h0a[i] = pa[fa0 + 128 * i + fs0];
+        h0b[i] = pb[fb0 + 128 * i + fs0];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, true, pa, pb, fs1, h1a, h1b);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_row(i, h0a, h0b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // step t (t >= 1): ODD steps reuse the A fragments of step t - 1 and load
+    // only B; even steps (t = 2 s) also load A block s + 1
+    auto step = [&](int t, auto odd_c) {
+      constexpr bool ODD = decltype(odd_c)::value;
+      // odd: B of step t was issued before the A block that may still be in
+      // flight (8 loads); even: everything issued before step t - 1's B
+      if (ODD) {
+        gemm_wait_vm<8>();
+      } else {
+        gemm_wait_vm<0>();
+      }
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+      const i32x4* pa = sm.a[(t >> 1) & 1];
+      const i32x4* pb = sm.b[t & 1];
+      // h1 of step t - 1, reading h0 of step t, loading B of step t + 1 (odd:
+      // one load per row; even: all of B in rows 0-3, then A block t / 2 + 1
+      // in rows 4-7, so that every B load precedes every A load and the odd
+      // step's wait leaves exactly the 8 A loads in flight)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, !ODD, pa, pb, fs0, h0a, h0b);
+        if (ODD) {
+          load_b(t + 1, i, db1);
+        } else if (i < 4) {
+          load_b(t + 1, 2 * i, db2);
+        } else {
+          load_a((t >> 1) + 1, 2 * (i - 4));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (!ODD) {
+          if (i < 4) {
+            load_b(t + 1, 2 * i + 1, db2);
+          } else {
+            load_a((t >> 1) + 1, 2 * (i - 4) + 1);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // h0 of step t, reading h1 of step t
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        read_pair(i, !ODD, pa, pb, fs1, h1a, h1b);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_row(i, h0a, h0b);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    for (int t = 1; t < n_t; t += 2) {
+      step(t, std::integral_constant<bool, true>{});
+      if (t + 1 < n_t) step(t + 1, std::integral_constant<bool, false>{});
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);
+    gemm_wait_vm<0>();
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+  }
+};
+
 // Query-narrow ring tile: 128 rows of A (queries) against 256 rows of B
 // (store rows) with a three-slot LDS ring, for streaming a large B past a
 // small A.  Wave w holds all 128 A rows against B rows [64 w, 64 w + 64) as
