@@ -507,11 +507,11 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(
 // GEMM core computes the fp32 score matrix S[q][r] into the workspace (sized
 // to stay in the MALL), then one workgroup per query selects that chunk's
 // top k exactly:
-//  * a strided sample of 2048 scores is sorted; the sample at a rank chosen
-//    so that ~2k + 256 scores are expected above it is a threshold tau;
+//  * a strided sample of RS_SMP scores is sorted; the sample at a rank
+//    chosen so that ~2k + 256 scores are expected above it is a threshold tau;
 //  * one pass collects the scores >= tau into LDS (counting them all); if
 //    there are at least k of them the top k are all among them (the k-th
-//    best is >= tau), and if at most 4096 a bitonic sort orders them by
+//    best is >= tau), and if at most RS_CAP a bitonic sort orders them by
 //    (score desc, index asc) and the first k are the chunk's list;
 //  * otherwise tau moves by bisection over the sample ranks (more passes);
 //    if no rank works (a chunk of massive ties or one ordered against the
@@ -522,7 +522,8 @@ __global__ __launch_bounds__(256, 2) void score_stream_kernel(
 constexpr int RS_CAP = 2048;  // candidates sorted per (query, chunk)
 constexpr int RS_SMP = 1024;  // threshold samples
 constexpr int RS_SEG = 64;    // chunk rows per score segment (one maximum each)
-constexpr int RS_MAXSEG = 131072 / RS_SEG;  // segments of the largest chunk
+constexpr int64_t RS_MAXCHUNK = 262144;  // rows of the largest chunk (its segment tables sit in LDS)
+constexpr int RS_MAXSEG = (int)(RS_MAXCHUNK / RS_SEG);  // segments of the largest chunk
 
 // v of another lane of the same row of 16 (DPP control C, full masks)
 template <int C>
@@ -1345,10 +1346,14 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
   P.n_grp = (int)(D * elem_bytes / 128);
   if (n_q <= 0 || n_g <= 0) return P;
   // (the streaming plan at 128-384 queries measured 1.2-2.8x slower)
-  if (elem_bytes == 2 && D % GKS == 0 && n_q >= 128 && n_g >= 4096) {
-    // GEMM plan: score chunks of at most ~256 MB (MALL-resident between the
-    // GEMM and the selection) and 128K rows, at most 255 chunks (the merge
-    // takes 256 sources)
+  // GEMM plan: score chunks of at most ~256 MB (MALL-resident between the
+  // GEMM and the selection) and RS_MAXCHUNK rows, at most GEMM_MAX_PARTS
+  // chunks (the merge takes 1024 sources, one of them the previous list);
+  // a store too large for that takes the streaming plan, whose partitions
+  // grow with the store
+  constexpr int64_t GEMM_MAX_PARTS = 1023;
+  if (elem_bytes == 2 && D % GKS == 0 && n_q >= 128 && n_g >= 4096 &&
+      n_g <= RS_MAXCHUNK * GEMM_MAX_PARTS) {
     // Tiles: 256 x 256, or 128 queries x 256 rows (the ring core) where the
     // last 256-query tile would be at most half used (n_q % 256 in [1, 128])
     // and the query count is small enough that store rows, not queries, set
@@ -1357,8 +1362,8 @@ ScorePlan plan_score(int64_t n_q, int64_t n_g, int64_t D, int k, int elem_bytes)
     const bool narrow = rem >= 1 && rem <= 128 && n_q <= 384;
     const int64_t rt = narrow ? GRR : GT;
     int64_t chunk = ((int64_t)256 << 20) / (n_q * 4);
-    chunk = chunk > 131072 ? 131072 : chunk;  // <= 32 rows per threshold sample
-    const int64_t min_chunk = (n_g + 254) / 255;
+    chunk = chunk > RS_MAXCHUNK ? RS_MAXCHUNK : chunk;
+    const int64_t min_chunk = (n_g + GEMM_MAX_PARTS - 1) / GEMM_MAX_PARTS;  // <= RS_MAXCHUNK
     chunk = chunk < min_chunk ? min_chunk : chunk;
     chunk = chunk < 4096 ? 4096 : chunk;
     chunk = (chunk + rt - 1) / rt * rt;

@@ -215,3 +215,53 @@ def test_store_scan_full_config():
         at += m
     del G
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("nq", [128, 1024])
+def test_store_scan_many_chunks(nq):
+    """40M x 64 unit fp16 store (5.1 GB), top-100, GEMM plan with many
+    chunks: at Q = 128, 153 chunks of 262144 rows (the largest chunk the
+    selection's segment tables hold; the earlier rule of at most 255 chunks
+    would have asked for 156863-row chunks); at Q = 1024, 611 chunks of
+    65536 rows, merged in one pass from 612 sources.  Planted
+    near-duplicates rank first; 6 queries per case against the oracle's
+    complete lookup over all 40M rows."""
+    n, Dq, k = 40_000_000, 64, 100
+    say(f"case: store scan, many chunks n={n} D={Dq} nq={nq}")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(31)
+    G = torch.empty((n, Dq), dtype=torch.float16, device="cuda")
+    for lo in range(0, n, 1 << 22):
+        hi = min(n, lo + (1 << 22))
+        c = torch.randn((hi - lo, Dq), generator=gen, device="cuda")
+        G[lo:hi] = (c / c.norm(dim=1, keepdim=True)).half()
+    n_pl = 4
+    targets = np.random.default_rng(nq).choice(n, n_pl, replace=False)
+    q = torch.randn((nq, Dq), generator=gen, device="cuda")
+    q = q / q.norm(dim=1, keepdim=True)
+    g = G[torch.from_numpy(targets).cuda()].float()
+    g = g / g.norm(dim=1, keepdim=True)
+    u = q[:n_pl] - (q[:n_pl] * g).sum(1, keepdim=True) * g
+    u = u / u.norm(dim=1, keepdim=True)
+    q[:n_pl] = 0.98 * g + (1 - 0.98 ** 2) ** 0.5 * u
+    Q = q.half().contiguous()
+    ts = torch.empty((nq, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((nq, k), dtype=torch.int64, device="cuda")
+    P.attr_score_topk(Q, G, k, ts, ti)
+    torch.cuda.synchronize()
+    assert (host(ti)[:n_pl, 0] == targets).all()
+    pick = np.array([0, n_pl - 1, n_pl, nq // 2, nq - 2, nq - 1])
+    Qp = host(Q[torch.from_numpy(pick).cuda()])
+    ref_s = np.full((len(pick), k + 1), -np.inf)
+    ref_i = np.full((len(pick), k + 1), -1, dtype=np.int64)
+    for lo in range(0, n, 1 << 21):
+        hi = min(n, lo + (1 << 21))
+        Gc = G[lo:hi].cpu().to(torch.float64).numpy()
+        cs, ci = O.score_topk(Qp, Gc, k + 1, index_base=lo)
+        ref_s, ref_i = O.merge_topk(ref_s, ref_i, cs, ci, k + 1)
+    gs, gi = host(ts)[pick], host(ti)[pick]
+    ret = np.stack([O.scores(Qp[j:j + 1], host(G[torch.from_numpy(gi[j]).cuda()]))[0]
+                    for j in range(len(pick))])
+    check_topk_from_lists(gs, gi, ref_s, ref_i, ret, k)
+    del G
+    torch.cuda.empty_cache()
