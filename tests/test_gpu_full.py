@@ -104,10 +104,14 @@ def test_syrk_lowrank_small_eigenvalues():
     assert rel.max() <= 1e-2
 
 
-def test_full_apply_well_conditioned():
-    say("case: full apply, random SPD M")
+@pytest.mark.parametrize("n,D", [(1000, 512), (777, 320), (300, 64)])
+def test_full_apply_well_conditioned(n, D):
+    """Random SPD M; ragged row tiles (777 = 3 x 256 + 9, 300 = 256 + 44), a
+    ragged 64-column tile and an odd count of 64-wide K-blocks (D = 320:
+    the hi/lo-interleaved core's last pair of steps), a single K-block
+    (D = 64)."""
+    say(f"case: full apply, random SPD M n={n} D={D}")
     rng = np.random.default_rng(3)
-    n, D = 1000, 512
     X = (rng.standard_normal((n, D)) * 3).astype(np.float16)
     B = rng.standard_normal((D, D)) / np.sqrt(D)
     M = (B @ B.T + 0.5 * np.eye(D)).astype(np.float32)
