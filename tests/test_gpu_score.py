@@ -430,14 +430,14 @@ def test_streaming_bound_ties_at_the_bound():
 @pytest.mark.parametrize("nq,ng,D,k", [(130, 5000, 256, 10), (300, 9000, 256, 100),
                                        (257, 4100, 64, 128), (128, 5000, 256, 10),
                                        (128, 4097, 128, 5), (384, 6000, 192, 50),
-                                       (128, 270000, 64, 100)])
+                                       (128, 530000, 64, 100)])
 def test_gemm_plan(nq, ng, D, k):
     """256 x 256 tiles (130 queries) and 128-query x 256-row ring tiles (128,
     257, 300, 384 queries): ragged query tiles, ragged row tiles whose last
     workgroup has waves without rows (4097 = 16 x 256 + 1: one row in wave 0;
     5000 = 19 x 256 + 136: 8 rows in wave 2, none in wave 3), one and three
     stages (D = 64, 192: fewer stages than ring slots), three chunks of at
-    most 131072 rows with the running bound (270000 rows); a tie far apart, a
+    most 262144 rows with the running bound (530000 rows); a tie far apart, a
     NaN row that must never be selected."""
     say(f"case: gemm plan nq={nq} ng={ng} D={D} k={k}")
     Q = synth.unit_rows(nq, D, seed=41)
