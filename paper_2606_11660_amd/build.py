@@ -88,8 +88,11 @@ def lds_dma_hazards(asm: str) -> list:
     Wait states are counted backwards along every path into the load: through
     a label into each branch that targets it (loop back-edges included) and
     into the fall-through predecessor, with one wait state per instruction
-    and N + 1 per s_nop N.  Returns a description of every violation found
-    in `asm` (device assembly)."""
+    and N + 1 per s_nop N.  The loads take their LDS address from M0, which
+    the asm sets itself: in a function that holds such loads, an M0 write
+    by compiler-generated code (outside the asm blocks) is a violation too,
+    since it could fall between an M0 set-up and its loads.  Returns a
+    description of every violation found in `asm` (device assembly)."""
     lines = [l.strip() for l in asm.splitlines()]
     preds = {}
     for i, l in enumerate(lines):
@@ -97,6 +100,23 @@ def lds_dma_hazards(asm: str) -> list:
         if m:
             preds.setdefault(m.group(1), []).append(i)
     found, kernel = [], "?"
+    # compiler-generated M0 writes per function, and whether it has loads
+    in_asm, m0_writes, has_dma = False, {}, set()
+    for line in lines:
+        if re.match(r"^_Z\S+:", line):
+            kernel = line[:-1]
+        if line.startswith(";;#ASMSTART"):
+            in_asm = True
+        elif line.startswith(";;#ASMEND"):
+            in_asm = False
+        elif "buffer_load_dword" in line and " lds" in line:
+            has_dma.add(kernel)
+        elif not in_asm and line[:1].isalpha() and _operands(line)[:1] == ["m0"]:
+            m0_writes.setdefault(kernel, []).append(line)
+    for k in sorted(has_dma):
+        for w in m0_writes.get(k, []):
+            found.append(f"{k}: compiler-generated M0 write '{w}' in a function with direct-to-LDS loads")
+    kernel = "?"
     for idx, line in enumerate(lines):
         if re.match(r"^_Z\S+:", line):
             kernel = line[:-1]

@@ -31,7 +31,6 @@ namespace {
 constexpr int SQB = 64;       // queries per workgroup
 constexpr int STN = 128;      // store rows per tile (4 waves x 32 rows)
 constexpr int SPD = 3;        // 128-byte K-groups of store loads in flight (5 or 7: no faster)
-constexpr int SCP = STN + 4;  // padded score-tile row (bank spread)
 
 template <bool F16>
 struct STag;

@@ -241,8 +241,22 @@ def test_lds_dma_hazards_m0_write():
     """The load reads its LDS address from M0: an M0 write needs one wait
     state before it."""
     from paper_2606_11660_amd.build import lds_dma_hazards
-    assert len(lds_dma_hazards(_asm("\ts_mov_b32 m0, s8", LOAD))) == 1
-    assert lds_dma_hazards(_asm("\ts_mov_b32 m0, s8", "\ts_nop 0", LOAD)) == []
+    set_m0 = [";;#ASMSTART", "\ts_mov_b32 m0, s8"]
+    assert len(lds_dma_hazards(_asm(*set_m0, ";;#ASMEND", LOAD))) == 1
+    assert lds_dma_hazards(_asm(*set_m0, "\ts_nop 0", ";;#ASMEND", LOAD)) == []
+
+
+def test_lds_dma_hazards_compiler_m0_write():
+    """M0 belongs to the asm that sets it for the loads: a compiler-generated
+    M0 write (outside the asm blocks) in a function with direct-to-LDS loads
+    is refused; the same write in a function without them is not."""
+    from paper_2606_11660_amd.build import lds_dma_hazards
+    own = _asm(";;#ASMSTART", "\ts_mov_b32 m0, s8", "\ts_nop 0", ";;#ASMEND", "\ts_nop 7", LOAD)
+    assert lds_dma_hazards(own) == []
+    comp = _asm("\ts_movk_i32 m0, 0x100", "\ts_nop 7", "\ts_nop 7", LOAD)
+    assert len(lds_dma_hazards(comp)) == 1
+    other = "\n".join(["_Zother:", "\ts_mov_b32 m0, -1", "\ts_endpgm"]) + "\n" + _asm("\ts_nop 7", LOAD)
+    assert lds_dma_hazards(other) == []
 
 
 def test_built_device_code_passes_the_hazard_scan():
