@@ -63,12 +63,10 @@ struct GemmCore {
 
   // Accumulate n_st stages (K = 64 n_st) of the tile's rows: A rows through
   // descriptor da (row stride lda elements), B rows through db (stride ldb);
-  // both descriptors start at the tile's first row.  Stages [0, n_sw) take
-  // K = [0, 64 n_sw) of A and of db; stages [n_sw, n_st) take K restarting
-  // from 0 of A and of db2 (two products summed into one accumulator).  Byte
-  // offsets within a descriptor must fit 31 bits.
+  // both descriptors start at the tile's first row.  Byte offsets within a
+  // descriptor must fit 31 bits.
   __device__ inline void run(GemmSmem& sm, const i32x4& da, int64_t lda, const i32x4& db,
-                             const i32x4& db2, int64_t ldb, int n_sw, int n_st) {
+                             int64_t ldb, int n_st) {
     if (n_st <= 0) return;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = threadIdx.x & 63;
@@ -84,24 +82,25 @@ struct GemmCore {
     const uint32_t lds_b = (uint32_t)(uintptr_t)&sm.b[0][0] + (uint32_t)(64 * wave) * 128u;
     // loads of stage st come in 4 groups of 4 instructions (A rows 0-31 and
     // 32-63 of the wave, then B): group g sets M0 once, instruction u of it
-    // lands at M0 + 1024 u through the instruction offset.  A stage past the
-    // end is issued with every lane out of range: it fetches nothing and
-    // zero-fills a slot that is no longer read.
+    // lands at M0 + 1024 u through the instruction offset.  The stage's K
+    // offset moves the descriptors (desc_at), so the per-lane offsets are
+    // fixed.  A stage past the end is issued with every lane out of range:
+    // it fetches nothing and zero-fills a slot that is no longer read.
     auto issue_grp = [&](int st, int g) {
       const uint32_t sb = (uint32_t)(st & 1) * G_SLOT;
       set_m0((g < 2 ? lds_a : lds_b) + sb + (uint32_t)(g & 1) * 4096u);
     };
     auto issue_u = [&](int st, int g, auto uc) {
       constexpr int u = decltype(uc)::value;
-      const bool sw = st >= n_sw;
-      const uint32_t ko = (uint32_t)(sw ? st - n_sw : st) * 128u + (st < n_st ? 0u : 0x80000000u);
       const int h = 4 * (g & 1) + u;
+      const uint32_t ko = (uint32_t)st * 128u;
+      const bool live = st < n_st;
       if (g < 2) {
-        lds_dma16_m0<1024 * u>(da, a_off + h * a8 + ko - 1024u * u);
+        lds_dma16_m0<1024 * u>(desc_at(da, ko, live), a_off + h * a8 - 1024u * u);
       } else if (NT) {
-        lds_dma16_m0_nt<1024 * u>(sw ? db2 : db, b_off + h * b8 + ko - 1024u * u);
+        lds_dma16_m0_nt<1024 * u>(desc_at(db, ko, live), b_off + h * b8 - 1024u * u);
       } else {
-        lds_dma16_m0<1024 * u>(sw ? db2 : db, b_off + h * b8 + ko - 1024u * u);
+        lds_dma16_m0<1024 * u>(desc_at(db, ko, live), b_off + h * b8 - 1024u * u);
       }
     };
     auto issue_all = [&](int st) {
@@ -272,25 +271,24 @@ struct GemmCoreHL {
     // SGPRs right before it.
     auto load_a = [&](int s, int n) {
       const int g = n >> 2, u = n & 3;
-      const uint32_t ko = (uint32_t)s * 128u + (s < n_k ? 0u : 0x80000000u);
+      const i32x4 d = desc_at(da, (uint32_t)s * 128u, s < n_k);
       if (u == 0) set_m0(lds_a + (uint32_t)(s & 1) * G_SLOT + (uint32_t)g * 4096u);
-      const uint32_t voff = a_off + (uint32_t)(4 * g + u) * a8 + ko;
+      const uint32_t voff = a_off + (uint32_t)(4 * g + u) * a8;
       switch (u) {
-        case 0: lds_dma16_m0_guarded<0>(da, voff); break;
-        case 1: lds_dma16_m0<1024>(da, voff - 1024u); break;
-        case 2: lds_dma16_m0<2048>(da, voff - 2048u); break;
-        default: lds_dma16_m0<3072>(da, voff - 3072u); break;
+        case 0: lds_dma16_m0_guarded<0>(d, voff); break;
+        case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
+        case 2: lds_dma16_m0<2048>(d, voff - 2048u); break;
+        default: lds_dma16_m0<3072>(d, voff - 3072u); break;
       }
     };
     // d: db1 for even t, db2 for odd t (the caller knows the parity at
     // compile time: a run-time choice put a VALU write of the descriptor
     // right before the load)
-    auto load_b = [&](int t, int n, const i32x4& d) {
+    auto load_b = [&](int t, int n, const i32x4& db) {
       const int g = n >> 2, u = n & 3;
-      const int s = t >> 1;
-      const uint32_t ko = (uint32_t)s * 128u + (t < n_t ? 0u : 0x80000000u);
+      const i32x4 d = desc_at(db, (uint32_t)(t >> 1) * 128u, t < n_t);
       if (u == 0) set_m0(lds_b + (uint32_t)(t & 1) * G_SLOT + (uint32_t)g * 4096u);
-      const uint32_t voff = b_off + (uint32_t)(4 * g + u) * b8 + ko;
+      const uint32_t voff = b_off + (uint32_t)(4 * g + u) * b8;
       switch (u) {
         case 0: lds_dma16_m0_guarded<0>(d, voff); break;
         case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
@@ -476,14 +474,15 @@ struct GemmCoreR {
     // slot that is not read again
     auto issue = [&](int st, int sl, int n) {
       const int g = n >> 2, u = n & 3;
-      const uint32_t ko = (uint32_t)st * 128u + (st < n_st ? 0u : 0x80000000u);
+      const uint32_t ko = (uint32_t)st * 128u;
+      const bool live = st < n_st;
       if (u == 0)
         set_m0(g == 0 ? lds_a + (uint32_t)sl * SLOT_A
                       : lds_b + (uint32_t)sl * SLOT_B + (uint32_t)(g - 1) * 4096u);
-      const uint32_t voff = g == 0 ? a_off + (uint32_t)u * a8 + ko
-                                   : b_off + (uint32_t)(4 * (g - 1) + u) * b8 + ko;
+      const uint32_t voff = g == 0 ? a_off + (uint32_t)u * a8
+                                   : b_off + (uint32_t)(4 * (g - 1) + u) * b8;
       if (g == 0 || !NT) {
-        const i32x4& d = g == 0 ? da : dbw;
+        const i32x4 d = desc_at(g == 0 ? da : dbw, ko, live);
         switch (u) {
           case 0: lds_dma16_m0<0>(d, voff); break;
           case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
@@ -491,11 +490,12 @@ struct GemmCoreR {
           default: lds_dma16_m0<3072>(d, voff - 3072u); break;
         }
       } else {
+        const i32x4 d = desc_at(dbw, ko, live);
         switch (u) {
-          case 0: lds_dma16_m0_nt<0>(dbw, voff); break;
-          case 1: lds_dma16_m0_nt<1024>(dbw, voff - 1024u); break;
-          case 2: lds_dma16_m0_nt<2048>(dbw, voff - 2048u); break;
-          default: lds_dma16_m0_nt<3072>(dbw, voff - 3072u); break;
+          case 0: lds_dma16_m0_nt<0>(d, voff); break;
+          case 1: lds_dma16_m0_nt<1024>(d, voff - 1024u); break;
+          case 2: lds_dma16_m0_nt<2048>(d, voff - 2048u); break;
+          default: lds_dma16_m0_nt<3072>(d, voff - 3072u); break;
         }
       }
     };
@@ -671,12 +671,12 @@ struct GemmCoreT {
     };
     auto issue_u = [&](int st, int g, auto uc) {
       constexpr int u = decltype(uc)::value;
-      const uint32_t ko = st < n_st ? 0u : 0x80000000u;
+      const bool live = st < n_st;
       const int h = 4 * (g & 1) + u;
       if (g < 2) {
-        lds_dma16_m0<1024 * u>(da, oa[h] + (uint32_t)st * kst_a + ko);
+        lds_dma16_m0<1024 * u>(desc_at(da, (uint32_t)st * kst_a, live), oa[h]);
       } else {
-        lds_dma16_m0<1024 * u>(db, ob[h] + (uint32_t)st * kst_b + ko);
+        lds_dma16_m0<1024 * u>(desc_at(db, (uint32_t)st * kst_b, live), ob[h]);
       }
     };
     auto issue_all = [&](int st) {

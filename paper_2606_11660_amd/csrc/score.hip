@@ -605,7 +605,7 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(
   tb[threadIdx.x] = use_bound && q0 + threadIdx.x < n_q ? thr[q0 + threadIdx.x] : -__builtin_inff();
   GemmCore<Tag, NT> core;
   core.zero();
-  core.run(sm, dq, ldq, dg, dg, ldg, n_st, n_st);
+  core.run(sm, dq, ldq, dg, ldg, n_st);
   score_tile_store(core, q0, nq, c0, nr, S, lds, segmax, n_seg, [&](int row) { return tb[row]; });
 }
 
