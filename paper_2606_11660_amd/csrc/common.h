@@ -44,15 +44,18 @@ __device__ inline i32x4 make_desc(const void* base, uint32_t bytes) {
 }
 
 // The descriptor d moved on by off bytes: base + off and range - off, or
-// range 0 (every lane out of range) when off reaches the range or live is
-// false.  The GEMM cores advance their operand descriptors by one K-stage
-// this way, with scalar arithmetic once per stage, so that the per-lane
-// offsets of their loads stay fixed (no vector address arithmetic per load)
-// and the range check still ends at the operand's last row.
+// range 0 (every lane out of range) when live is false or the range is
+// empty.  The caller guarantees off < range when live and the range is not
+// empty (a live K-stage starts inside the operand's first row).  The GEMM
+// cores advance their operand descriptors by one K-stage this way, with
+// scalar arithmetic once per stage, so that the per-lane offsets of their
+// loads stay fixed (no vector address arithmetic per load) and the range
+// check still ends at the operand's last row.  (A clamped subtraction here
+// would be selected as a vector instruction.)
 __device__ inline i32x4 desc_at(const i32x4& d, uint32_t off, bool live) {
   const uint64_t b = (((uint64_t)(uint32_t)d.y << 32) | (uint32_t)d.x) + off;
   const uint32_t r = (uint32_t)d.z;
-  return i32x4{(int)(uint32_t)b, (int)(uint32_t)(b >> 32), (int)(live && off < r ? r - off : 0u), d.w};
+  return i32x4{(int)(uint32_t)b, (int)(uint32_t)(b >> 32), (int)(live && r != 0u ? r - off : 0u), d.w};
 }
 
 // Direct-to-LDS 16-byte buffer load: lane l's 16 bytes at voff land at LDS

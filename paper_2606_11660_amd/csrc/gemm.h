@@ -641,8 +641,8 @@ struct GemmCoreT {
 
   // n_st stages of 64 K-rows; K-rows past a descriptor's range read zeros.
   // Byte offsets within a descriptor must fit 31 bits.
-  __device__ inline void run(GemmSmem& sm, const i32x4& da, int64_t lda, const i32x4& db,
-                             int64_t ldb, int n_st) {
+  __device__ inline void run(GemmSmem& sm, const i32x4& da, const i32x4& db, int64_t ld,
+                             int n_st) {
     constexpr int32_t neg_mask = NEG ? (int32_t)0x80008000 : 0;
     if (n_st <= 0) return;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -653,15 +653,14 @@ struct GemmCoreT {
     // ((s / 2) ^ g(row)) * 2 + s % 2; offsets carry -1024 (h % 4) for the
     // instruction offset that places four loads behind one M0 write
     const int lr = lane >> 5, s = lane & 31;
-    uint32_t oa[8], ob[8];
+    uint32_t oa[8];
 #pragma unroll
     for (int h = 0; h < 8; ++h) {
       const int row = 16 * wave + 2 * h + lr;
       const int c = (((s >> 1) ^ kmajor_swz(row)) << 1) | (s & 1);
-      oa[h] = (uint32_t)((int64_t)row * lda * 2 + c * 16) - 1024u * (uint32_t)(h & 3);
-      ob[h] = (uint32_t)((int64_t)row * ldb * 2 + c * 16) - 1024u * (uint32_t)(h & 3);
+      oa[h] = (uint32_t)((int64_t)row * ld * 2 + c * 16) - 1024u * (uint32_t)(h & 3);
     }
-    const uint32_t kst_a = (uint32_t)(64 * lda * 2), kst_b = (uint32_t)(64 * ldb * 2);
+    const uint32_t kst = (uint32_t)(64 * ld * 2);
     const uint32_t sa0 = (uint32_t)(uintptr_t)&sm.a[0][0], sb0 = (uint32_t)(uintptr_t)&sm.b[0][0];
     const uint32_t lds_a = sa0 + (uint32_t)(16 * wave) * 512u;
     const uint32_t lds_b = sb0 + (uint32_t)(16 * wave) * 512u;
@@ -669,14 +668,19 @@ struct GemmCoreT {
       const uint32_t sb = (uint32_t)(st & 1) * G_SLOT;
       set_m0((g < 2 ? lds_a : lds_b) + sb + (uint32_t)(g & 1) * 4096u);
     };
+    // the same for a stage whose slot is known at compile time
+    auto issue_grp_s = [&](auto slot_c, int g) {
+      constexpr uint32_t sb = (uint32_t)decltype(slot_c)::value * G_SLOT;
+      set_m0((g < 2 ? lds_a : lds_b) + sb + (uint32_t)(g & 1) * 4096u);
+    };
     auto issue_u = [&](int st, int g, auto uc) {
       constexpr int u = decltype(uc)::value;
       const bool live = st < n_st;
       const int h = 4 * (g & 1) + u;
       if (g < 2) {
-        lds_dma16_m0<1024 * u>(desc_at(da, (uint32_t)st * kst_a, live), oa[h]);
+        lds_dma16_m0<1024 * u>(desc_at(da, (uint32_t)st * kst, live), oa[h]);
       } else {
-        lds_dma16_m0<1024 * u>(desc_at(db, (uint32_t)st * kst_b, live), ob[h]);
+        lds_dma16_m0<1024 * u>(desc_at(db, (uint32_t)st * kst, live), oa[h]);
       }
     };
     auto issue_all = [&](int st) {
@@ -691,25 +695,34 @@ struct GemmCoreT {
     };
     // fragment of 16-column block t (of the wave's 128) in K-half hk: lane
     // (rg, i) reads K-rows 32 hk + 8 rg + 4 h + i / 4 (h = 0, 1), columns
-    // 16 t + 4 (i % 4) .. + 3 of its operand half wx
+    // 16 t + 4 (i % 4) .. + 3 of its operand half wx.  The lane's address
+    // of block t in slot 0, K-half 0 is fixed (fpa, fpb); the slot and the
+    // K-half add a constant that the reads carry in their offset field (the
+    // stage loop runs in pairs, so every stage's slot is known at compile
+    // time), and no address arithmetic is left in the loop.
     const int rg = lane >> 4, i4 = lane & 15;
     const int gl = (i4 >> 2) | ((rg & 1) << 2);  // g() of every K-row this lane reads
     const uint32_t rowb = (uint32_t)(8 * rg + (i4 >> 2)) * 512u + 8u * (uint32_t)(i4 & 3);
-    auto frag = [&](uint32_t base, int wx, int t, int hk) -> i32x4 {
-      const uint32_t a0 =
-          base + (uint32_t)(32 * hk) * 512u + rowb + 32u * (uint32_t)((8 * wx + t) ^ gl);
-      const i32x2 lo = lds_read_tr16(a0);
-      const i32x2 hi = lds_read_tr16(a0 + 4u * 512u);
+    uint32_t fpa[8], fpb[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      fpa[t] = sa0 + rowb + 32u * (uint32_t)((8 * wm + t) ^ gl);
+      fpb[t] = sb0 + rowb + 32u * (uint32_t)((8 * wn + t) ^ gl);
+    }
+    auto frag = [&](uint32_t addr) -> i32x4 {
+      const i32x2 lo = lds_read_tr16(addr);
+      const i32x2 hi = lds_read_tr16(addr + 4u * 512u);
       return i32x4{lo.x, lo.y, hi.x, hi.y};
     };
-    // the 16 fragments of a half, two per call, B first (as in GemmCore)
-    auto read_pair = [&](int i, uint32_t pa, uint32_t pb, int hk, i32x4 (&fa)[8], i32x4 (&fb)[8]) {
+    // the 16 fragments of a half (slot and K-half in off), two per call, B
+    // first (as in GemmCore)
+    auto read_pair = [&](int i, uint32_t off, i32x4 (&fa)[8], i32x4 (&fb)[8]) {
       if (i < 4) {
-        fb[2 * i] = frag(pb, wn, 2 * i, hk);
-        fb[2 * i + 1] = frag(pb, wn, 2 * i + 1, hk);
+        fb[2 * i] = frag(fpb[2 * i] + off);
+        fb[2 * i + 1] = frag(fpb[2 * i + 1] + off);
       } else {
-        fa[2 * i - 8] = frag(pa, wm, 2 * i - 8, hk);
-        fa[2 * i - 7] = frag(pa, wm, 2 * i - 7, hk);
+        fa[2 * i - 8] = frag(fpa[2 * i - 8] + off);
+        fa[2 * i - 7] = frag(fpa[2 * i - 7] + off);
       }
     };
     auto mma_row = [&](int i, const i32x4 (&fa)[8], const i32x4 (&fb)[8]) {
@@ -728,35 +741,37 @@ struct GemmCoreT {
     i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
 
     // same pipeline as GemmCore::run
+    constexpr uint32_t HK1 = 32u * 512u;  // K-half 1 of a slot
     issue_all(0);
     gemm_wait_vm<0>();
     __builtin_amdgcn_s_barrier();
     issue_all(1);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      h0a[i] = frag(sa0, wm, i, 0);
-      h0b[i] = frag(sb0, wn, i, 0);
+      h0a[i] = frag(fpa[i]);
+      h0b[i] = frag(fpb[i]);
     }
     negate_b(h0b);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      read_pair(i, sa0, sb0, 1, h1a, h1b);
+      read_pair(i, HK1, h1a, h1b);
       __builtin_amdgcn_sched_barrier(0);
       mma_row(i, h0a, h0b);
       __builtin_amdgcn_sched_barrier(0);
     }
     negate_b(h1b);
-    for (int st = 1; st < n_st; ++st) {
+    // stage st in slot SLOT = st & 1 (a compile-time constant)
+    auto stage = [&](int st, auto slot_c) {
+      constexpr uint32_t SLOT = decltype(slot_c)::value;
+      constexpr uint32_t base = SLOT * G_SLOT;
       gemm_wait_vm<0>();
       wait_lgkm0();
       __builtin_amdgcn_s_barrier();
-      const uint32_t pa = sa0 + (uint32_t)(st & 1) * G_SLOT;
-      const uint32_t pb = sb0 + (uint32_t)(st & 1) * G_SLOT;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        read_pair(i, pa, pb, 0, h0a, h0b);
+        read_pair(i, base, h0a, h0b);
         if ((i & 1) == 0) {
-          issue_grp(st + 1, i >> 1);
+          issue_grp_s(std::integral_constant<uint32_t, 1u - SLOT>{}, i >> 1);
           issue_u(st + 1, i >> 1, std::integral_constant<int, 0>{});
         } else {
           issue_u(st + 1, i >> 1, std::integral_constant<int, 2>{});
@@ -778,12 +793,62 @@ struct GemmCoreT {
       negate_b(h0b);
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        read_pair(i, pa, pb, 1, h1a, h1b);
+        read_pair(i, base + HK1, h1a, h1b);
         __builtin_amdgcn_sched_barrier(0);
         mma_row(i, h0a, h0b);
         __builtin_amdgcn_sched_barrier(0);
       }
       negate_b(h1b);
+    };
+    if constexpr (NEG) {
+      // the negated core keeps one loop body with the slot offset in a
+      // register: two bodies with the flips raised the register demand past
+      // the file and the compiler moved accumulators in and out of it
+      for (int st = 1; st < n_st; ++st) {
+        const uint32_t base = (uint32_t)(st & 1) * G_SLOT;
+        gemm_wait_vm<0>();
+        wait_lgkm0();
+        __builtin_amdgcn_s_barrier();
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          read_pair(i, base, h0a, h0b);
+          if ((i & 1) == 0) {
+            issue_grp(st + 1, i >> 1);
+            issue_u(st + 1, i >> 1, std::integral_constant<int, 0>{});
+          } else {
+            issue_u(st + 1, i >> 1, std::integral_constant<int, 2>{});
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+          __builtin_amdgcn_sched_barrier(0);
+          if ((i & 1) == 0) {
+            issue_u(st + 1, i >> 1, std::integral_constant<int, 1>{});
+          } else {
+            issue_u(st + 1, i >> 1, std::integral_constant<int, 3>{});
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        negate_b(h0b);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          read_pair(i, base + HK1, h1a, h1b);
+          __builtin_amdgcn_sched_barrier(0);
+          mma_row(i, h0a, h0b);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        negate_b(h1b);
+      }
+    } else {
+      int st = 1;
+      for (; st + 1 < n_st; st += 2) {
+        stage(st, std::integral_constant<uint32_t, 1>{});
+        stage(st + 1, std::integral_constant<uint32_t, 0>{});
+      }
+      if (st < n_st) stage(st, std::integral_constant<uint32_t, 1>{});
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);

@@ -126,12 +126,12 @@ __global__ __launch_bounds__(256) void syrk_kernel(const T* __restrict__ X, int6
   if (j & 1) {
     GemmCoreT<Tag, true> core;
     core.zero();
-    core.run(sm, da, ldx, db, ldx, n_st);
+    core.run(sm, da, db, ldx, n_st);
     store(core.acc, -1.f);
   } else {
     GemmCoreT<Tag, false> core;
     core.zero();
-    core.run(sm, da, ldx, db, ldx, n_st);
+    core.run(sm, da, db, ldx, n_st);
     store(core.acc, 1.f);
   }
 }

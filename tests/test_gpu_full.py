@@ -48,6 +48,17 @@ def test_syrk_matches_oracle(n, D):
     assert err <= 1e-5
 
 
+@pytest.mark.parametrize("n", [1, 63, 64, 65, 128, 129, 192, 200, 320, 449])
+def test_syrk_short_slices(n):
+    """Row counts whose slices hold one to a few K-stages (ragged last stage;
+    odd and even stage counts reach both ends of the stage loop)."""
+    say(f"case: syrk short n={n} D=256")
+    X = (np.random.default_rng(1000 + n).standard_normal((n, 256)) * 2).astype(np.float16)
+    err = _check_upper(_syrk(X), O.accumulate_full(X))
+    say("max rel err", err)
+    assert err <= 1e-5
+
+
 def test_kfac_factors_from_packed_token_rows():
     """K-FAC factors (A = sum a a^T, Gamma = sum g g^T over the valid tokens)
     of two modules of a ragged batch: each is the FULL accumulate of the
