@@ -602,7 +602,7 @@ struct GemmCoreR {
 
 // The same block tile for K-major operands: C[m][n] += sum_k AT[k][m] BT[k][n]
 // with K-rows of the tile's 256 contiguous columns (A: rows of AT from the
-// tile's first column, stride lda; B likewise).  A stage is 64 K-rows of
+// tile's first column; B likewise; both with the row stride ld).  A stage is 64 K-rows of
 // 512 bytes per operand, loaded by the same direct-to-LDS instructions (two
 // K-rows per instruction); in LDS the 32-byte piece P of K-row r sits at
 // P ^ g(r), g(r) = (r & 3) | ((r >> 3) & 1) << 2, so that the 16 K-rows one
