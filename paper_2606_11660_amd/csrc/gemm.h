@@ -614,9 +614,9 @@ struct GemmCoreR {
 // 1024 bytes each) and needs no transposed copy of the operands.
 //
 // NEG: the sign bit of every 16-bit value of the B fragments is flipped (XOR
-// 0x80008000) between the loop that reads a K-half and the loop that uses
-// it, so the core accumulates -A B^T.  The second-moment accumulation alternates the sign of
-// its row slices this way to cancel the matrix core's rounding bias (see
+// 0x80008000, in place: flip_sign16) between the loop that reads a K-half
+// and the loop that uses it, so the core accumulates -A B^T.  The
+// second-moment accumulation alternates the sign of its row slices this way to cancel the matrix core's rounding bias (see
 // syrk.hip).  It is a compile-time choice: the non-negated core is the
 // plain loop, and a run-time mask or branch inside the loop raised the
 // scalar-register pressure or the instruction count of every slice.
@@ -627,6 +627,20 @@ __device__ inline i32x2 lds_read_tr16(uint32_t byte_addr) {
   return __builtin_bit_cast(i32x2, v);
 }
 __device__ inline int kmajor_swz(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
+
+// Flip the sign of the eight 16-bit values of an MFMA operand fragment, in
+// its own registers.  Written as plain code, the flipped values got fresh
+// registers, and in the negated core's paired stage loop the register file
+// ran short and the compiler moved accumulators in and out of it; inline
+// asm keeps them in place.  The asm is opaque to the compiler's hazard
+// checks, so a block of flips ends with s_nop 4 (five wait states; a VALU
+// write of a VGPR needs two before an MFMA reads it).
+__device__ inline void flip_sign16(i32x4& f) {
+  asm volatile("v_xor_b32 %0, 0x80008000, %0" : "+v"(f.x));
+  asm volatile("v_xor_b32 %0, 0x80008000, %0" : "+v"(f.y));
+  asm volatile("v_xor_b32 %0, 0x80008000, %0" : "+v"(f.z));
+  asm volatile("v_xor_b32 %0, 0x80008000, %0" : "+v"(f.w));
+}
 
 template <typename Tag, bool NEG = false>
 struct GemmCoreT {
@@ -643,7 +657,6 @@ struct GemmCoreT {
   // Byte offsets within a descriptor must fit 31 bits.
   __device__ inline void run(GemmSmem& sm, const i32x4& da, const i32x4& db, int64_t ld,
                              int n_st) {
-    constexpr int32_t neg_mask = NEG ? (int32_t)0x80008000 : 0;
     if (n_st <= 0) return;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = threadIdx.x & 63;
@@ -735,7 +748,8 @@ struct GemmCoreT {
     auto negate_b = [&](i32x4 (&fb)[8]) {
       if (NEG) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) fb[j] ^= neg_mask;
+        for (int j = 0; j < 8; ++j) flip_sign16(fb[j]);
+        asm volatile("s_nop 4");
       }
     };
     i32x4 h0a[8], h0b[8], h1a[8], h1b[8];
@@ -800,56 +814,12 @@ struct GemmCoreT {
       }
       negate_b(h1b);
     };
-    if constexpr (NEG) {
-      // the negated core keeps one loop body with the slot offset in a
-      // register: two bodies with the flips raised the register demand past
-      // the file and the compiler moved accumulators in and out of it
-      for (int st = 1; st < n_st; ++st) {
-        const uint32_t base = (uint32_t)(st & 1) * G_SLOT;
-        gemm_wait_vm<0>();
-        wait_lgkm0();
-        __builtin_amdgcn_s_barrier();
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          read_pair(i, base, h0a, h0b);
-          if ((i & 1) == 0) {
-            issue_grp(st + 1, i >> 1);
-            issue_u(st + 1, i >> 1, std::integral_constant<int, 0>{});
-          } else {
-            issue_u(st + 1, i >> 1, std::integral_constant<int, 2>{});
-          }
-          __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
-          __builtin_amdgcn_sched_barrier(0);
-          if ((i & 1) == 0) {
-            issue_u(st + 1, i >> 1, std::integral_constant<int, 1>{});
-          } else {
-            issue_u(st + 1, i >> 1, std::integral_constant<int, 3>{});
-          }
-          __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-          for (int j = 4; j < 8; ++j) acc[i][j] = mma16(Tag{}, h1a[i], h1b[j], acc[i][j]);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        negate_b(h0b);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          read_pair(i, base + HK1, h1a, h1b);
-          __builtin_amdgcn_sched_barrier(0);
-          mma_row(i, h0a, h0b);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-        negate_b(h1b);
-      }
-    } else {
-      int st = 1;
-      for (; st + 1 < n_st; st += 2) {
-        stage(st, std::integral_constant<uint32_t, 1>{});
-        stage(st + 1, std::integral_constant<uint32_t, 0>{});
-      }
-      if (st < n_st) stage(st, std::integral_constant<uint32_t, 1>{});
+    int st = 1;
+    for (; st + 1 < n_st; st += 2) {
+      stage(st, std::integral_constant<uint32_t, 1>{});
+      stage(st + 1, std::integral_constant<uint32_t, 0>{});
     }
+    if (st < n_st) stage(st, std::integral_constant<uint32_t, 1>{});
 #pragma unroll
     for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);
     gemm_wait_vm<0>();
