@@ -86,9 +86,8 @@ struct GemmCore {
     // offset moves the descriptors (desc_at), so the per-lane offsets are
     // fixed.  A stage past the end is issued with every lane out of range:
     // it fetches nothing and zero-fills a slot that is no longer read.
-    auto issue_grp = [&](int st, int g) {
-      const uint32_t sb = (uint32_t)(st & 1) * G_SLOT;
-      set_m0((g < 2 ? lds_a : lds_b) + sb + (uint32_t)(g & 1) * 4096u);
+    auto issue_grp = [&](int slot, int g) {
+      set_m0((g < 2 ? lds_a : lds_b) + (uint32_t)slot * G_SLOT + (uint32_t)(g & 1) * 4096u);
     };
     auto issue_u = [&](int st, int g, auto uc) {
       constexpr int u = decltype(uc)::value;
@@ -106,7 +105,7 @@ struct GemmCore {
     auto issue_all = [&](int st) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        issue_grp(st, g);
+        issue_grp(st & 1, g);
         issue_u(st, g, std::integral_constant<int, 0>{});
         issue_u(st, g, std::integral_constant<int, 1>{});
         issue_u(st, g, std::integral_constant<int, 2>{});
@@ -157,14 +156,17 @@ struct GemmCore {
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    for (int st = 1; st < n_st; ++st) {
+    // stage st in slot SLOT = st & 1, a compile-time constant (the loop runs
+    // in pairs), so the fragment reads carry the slot in their offset field
+    auto stage = [&](int st, auto slot_c) {
+      constexpr int SLOT = decltype(slot_c)::value;
       // stage st landed (nothing later is in flight); this wave's reads of
       // stage st - 1 are complete
       gemm_wait_vm<0>();
       wait_lgkm0();
       __builtin_amdgcn_s_barrier();
-      const i32x4* pa = sm.a[st & 1];
-      const i32x4* pb = sm.b[st & 1];
+      const i32x4* pa = sm.a[SLOT];
+      const i32x4* pb = sm.b[SLOT];
       // h1 of stage st - 1, reading h0 of stage st, loading stage st + 1
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -172,7 +174,7 @@ struct GemmCore {
         // loads 2 i and 2 i + 1 of stage st + 1: group i / 2, members
         // 2 (i % 2) and 2 (i % 2) + 1
         if ((i & 1) == 0) {
-          issue_grp(st + 1, i >> 1);
+          issue_grp(1 - SLOT, i >> 1);
           issue_u(st + 1, i >> 1, std::integral_constant<int, 0>{});
         } else {
           issue_u(st + 1, i >> 1, std::integral_constant<int, 2>{});
@@ -199,7 +201,13 @@ struct GemmCore {
         mma_row(i, h0a, h0b);
         __builtin_amdgcn_sched_barrier(0);
       }
+    };
+    int st = 1;
+    for (; st + 1 < n_st; st += 2) {
+      stage(st, std::integral_constant<int, 1>{});
+      stage(st + 1, std::integral_constant<int, 0>{});
     }
+    if (st < n_st) stage(st, std::integral_constant<int, 1>{});
     // h1 of the last stage
 #pragma unroll
     for (int i = 0; i < 8; ++i) mma_row(i, h1a, h1b);
