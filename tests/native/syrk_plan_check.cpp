@@ -1,8 +1,11 @@
 // CPU check of the SYRK planner's arithmetic (host-only header): for row
 // strides up to the accepted maximum, every K-slice spans at most 2^31 bytes
-// (the GEMM core's past-the-end loads rely on it), the chunks cover the rows,
-// and the workspace query (no stride limit) is large enough for every
-// stride's plan.  Prints "ok" or the first violation and exits non-zero.
+// (descriptor ranges and stage offsets are 32-bit), the chunks cover the
+// rows, and the workspace query (no stride limit) is large enough for every
+// stride's plan; and for the slices at the end of every chunk, the last
+// stage that holds rows starts inside the slice's descriptor range (the
+// per-stage descriptor advance subtracts the stage offset from the range
+// without clamping).  Prints "ok" or the first violation and exits non-zero.
 #include <cstdio>
 #include <cstdlib>
 
@@ -28,6 +31,26 @@ int main() {
                   P.C == P.Cs * P.J && n_chunks * P.C >= n && P.part_bytes <= Q.part_bytes &&
                   P.h64_bytes == Q.h64_bytes;
         if (ldx) ok = ok && P.Cs * ld * 2 <= (1ll << 31);
+        // the kernel's slice range (bytes from the tile's first column) for
+        // the first and the last column tile, at the first and the last
+        // slice of every chunk (plans that launch: a given stride)
+        for (long long r0 = 0; ok && ldx && r0 < n; r0 += P.C) {
+          const long long rows_c = n - r0 < P.C ? n - r0 : P.C;
+          const long long Jc = (rows_c + P.Cs - 1) / P.Cs;
+          for (long long j : {0ll, Jc - 1}) {
+            const long long rs = r0 + j * P.Cs;
+            long long nr = n - rs;
+            nr = nr > P.Cs ? P.Cs : nr;
+            if (nr <= 0) continue;
+            const long long n_st = (nr + 63) / 64;
+            for (long long c0 : {0ll, (D - 1) / 256 * 256}) {
+              const long long lim_slice = nr * ld, lim_mat = (n - 1 - rs) * ld + (D - c0);
+              const long long range = 2 * (lim_slice < lim_mat ? lim_slice : lim_mat);
+              const long long off = (n_st - 1) * 64 * ld * 2;
+              ok = ok && off < range && range < (1ll << 32);
+            }
+          }
+        }
         if (!ok) {
           std::printf("violation: n=%lld D=%lld ldx=%lld -> J=%d Cs=%lld C=%lld part=%zu (query %zu)\n",
                       n, D, ldx, P.J, (long long)P.Cs, (long long)P.C, P.part_bytes, Q.part_bytes);

@@ -278,8 +278,9 @@ def test_built_device_code_passes_the_hazard_scan():
 def test_syrk_plan_slices_fit_their_buffer_range(tmp_path):
     """Compile the host-only SYRK planner with g++ and check its arithmetic
     over row counts, widths and strides up to the accepted maximum (65536):
-    no K-slice spans more than 2^31 bytes, chunks cover the rows, and the
-    workspace query covers every stride's plan."""
+    no K-slice spans more than 2^31 bytes, chunks cover the rows, the
+    workspace query covers every stride's plan, and the last stage holding
+    rows starts inside its slice's descriptor range."""
     import shutil
     import subprocess
     gxx = shutil.which("g++")
