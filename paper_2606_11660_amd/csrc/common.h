@@ -104,18 +104,6 @@ __device__ inline void lds_dma16_m0(const i32x4& desc, uint32_t voff) {
                : "v"(voff), "s"(uniform_desc(desc)), "n"(OFF)
                : "memory");
 }
-// The same preceded by five wait states, for a load whose descriptor the
-// compiler may have just moved from VGPRs into SGPRs (v_readfirstlane): a
-// VALU write of an SGPR needs five wait states before a buffer load reads
-// it, and the compiler does not see that the asm holds a buffer load.
-template <int OFF>
-__device__ inline void lds_dma16_m0_guarded(const i32x4& desc, uint32_t voff) {
-  static_assert(OFF >= 0 && OFF < 4096, "12-bit instruction offset");
-  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds"
-               :
-               : "v"(voff), "s"(uniform_desc(desc)), "n"(OFF)
-               : "memory");
-}
 // The same with the non-temporal cache policy (data read once).
 template <int OFF>
 __device__ inline void lds_dma16_m0_nt(const i32x4& desc, uint32_t voff) {

@@ -274,16 +274,13 @@ struct GemmCoreHL {
     // load n (0..7) of A block s (slot s & 1) or of B step t (slot t & 1):
     // group n / 4 covers rows 32 (n / 4) .. + 31 of the wave's 64, member
     // n % 4 lands at M0 + 1024 (n % 4); past the end nothing is fetched.
-    // The first load of a group is guarded: this core's register pressure
-    // leads the compiler to keep the descriptors in VGPRs and move them into
-    // SGPRs right before it.
     auto load_a = [&](int s, int n) {
       const int g = n >> 2, u = n & 3;
       const i32x4 d = desc_at(da, (uint32_t)s * 128u, s < n_k);
       if (u == 0) set_m0(lds_a + (uint32_t)(s & 1) * G_SLOT + (uint32_t)g * 4096u);
       const uint32_t voff = a_off + (uint32_t)(4 * g + u) * a8;
       switch (u) {
-        case 0: lds_dma16_m0_guarded<0>(d, voff); break;
+        case 0: lds_dma16_m0<0>(d, voff); break;
         case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
         case 2: lds_dma16_m0<2048>(d, voff - 2048u); break;
         default: lds_dma16_m0<3072>(d, voff - 3072u); break;
@@ -298,7 +295,7 @@ struct GemmCoreHL {
       if (u == 0) set_m0(lds_b + (uint32_t)(t & 1) * G_SLOT + (uint32_t)g * 4096u);
       const uint32_t voff = b_off + (uint32_t)(4 * g + u) * b8;
       switch (u) {
-        case 0: lds_dma16_m0_guarded<0>(d, voff); break;
+        case 0: lds_dma16_m0<0>(d, voff); break;
         case 1: lds_dma16_m0<1024>(d, voff - 1024u); break;
         case 2: lds_dma16_m0<2048>(d, voff - 2048u); break;
         default: lds_dma16_m0<3072>(d, voff - 3072u); break;
