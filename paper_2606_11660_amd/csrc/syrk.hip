@@ -225,6 +225,25 @@ __global__ __launch_bounds__(256) void syrk_reduce_store_kernel(const float* __r
   }
   int tp, tq;
   upper_tile(u, nt, tp, tq);
+  // the thread's four elements share row p and take columns q0 .. q0 + 3
+  // (f0 is a multiple of 4): one 16-byte access where all four are stored
+  {
+    const int th = (int)(f0 & 255), w = th >> 6, lane = th & 63;
+    const int irj = (int)(f0 >> 8);
+    const int r = irj & 3, jj = (irj >> 2) & 7, i = irj >> 5;
+    const int64_t p = (int64_t)tp * GT + 128 * (w >> 1) + 16 * i + 4 * (lane >> 4) + r;
+    const int64_t q0 = (int64_t)tq * GT + 128 * (w & 1) + 16 * jj + (lane & 15);
+    if ((D & 3) == 0 && p < D && q0 + 3 < D && p <= q0) {
+      f32x4* hp = reinterpret_cast<f32x4*>(H + p * D + q0);
+      f32x4 hv = *hp;
+      hv.x = (float)((double)hv.x + s[0]);
+      hv.y = (float)((double)hv.y + s[1]);
+      hv.z = (float)((double)hv.z + s[2]);
+      hv.w = (float)((double)hv.w + s[3]);
+      *hp = hv;
+      return;
+    }
+  }
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     const int64_t f = f0 + c;
