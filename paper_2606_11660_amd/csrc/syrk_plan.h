@@ -18,9 +18,9 @@ constexpr int kSyrkSlices = 16;         // K-slices per full chunk (whole rounds
 constexpr int kSyrkSliceRows = ATTR_SYRK_SLICE_ROWS;        // longest fp32 accumulation
 constexpr int kSyrkChunkRows = kSyrkSlices * kSyrkSliceRows;  // rows per launch
 
-// Rows of one K-slice must span at most 2^31 bytes: the GEMM core marks its
-// loads past the last stage by adding 2^31 to their offset, which lands out
-// of the slice's buffer range only when that range is at most 2^31 bytes.
+// Rows of one K-slice must span at most 2^31 bytes: the GEMM core's buffer
+// descriptor range, its per-lane offsets and its per-stage descriptor
+// advance are 32-bit quantities.
 inline int64_t syrk_max_slice_rows(int64_t ldx) {
   if (ldx <= 0) return INT64_MAX;
   int64_t r = ((int64_t)1 << 30) / ldx;  // rows of 2 * ldx bytes in 2^31 bytes
