@@ -1,0 +1,100 @@
+"""Operands whose row stride exceeds their width (views into wider buffers
+whose extra columns hold NaN) on the entry points that take a stride: the
+GEMM-plan and streaming-plan store scans (Q and G), the FULL accumulate
+(X), the FULL and DIAG applies (X in, Y out: the padding of Y stays
+untouched) and the DIAG accumulate.  A kernel that read or wrote past a
+row's width would turn results into NaN or overwrite the sentinel."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2606_11660_amd as P
+import synth
+from tests._util import check_topk, dev, host, row_rel_l2, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _wide(x: np.ndarray, pad: int) -> torch.Tensor:
+    """Device view of x inside a buffer pad columns wider, padding NaN."""
+    n, d = x.shape
+    buf = np.full((n, d + pad), np.nan, dtype=x.dtype)
+    buf[:, :d] = x
+    return dev(buf)[:, :d]
+
+
+def _topk(Q, G, k):
+    ts = torch.full((Q.shape[0], k), 5.0, dtype=torch.float32, device="cuda")
+    ti = torch.full((Q.shape[0], k), 7, dtype=torch.int64, device="cuda")
+    P.attr_score_topk(Q, G, k, ts, ti)
+    torch.cuda.synchronize()
+    return host(ts), host(ti)
+
+
+@pytest.mark.parametrize("nq,ng,D,k,qpad,gpad", [(300, 9000, 256, 10, 64, 192),
+                                                 (128, 5000, 192, 20, 8, 72),
+                                                 (40, 9000, 256, 10, 64, 128)])
+def test_scan_strided(nq, ng, D, k, qpad, gpad):
+    """GEMM plan (300 queries: 256 x 256 tiles; 128: the ring) and the
+    streaming plan (40 queries) on strided Q and G."""
+    say(f"case: strided scan nq={nq} ng={ng} D={D} k={k} pads {qpad},{gpad}")
+    Q = synth.unit_rows(nq, D, seed=51)
+    G = synth.unit_rows(ng, D, seed=52)
+    Qd, Gd = _wide(Q, qpad), _wide(G, gpad)
+    assert Qd.stride(0) == D + qpad and Gd.stride(0) == D + gpad
+    ts, ti = _topk(Qd, Gd, k)
+    check_topk(ts, ti, O.scores(Q, G), k)
+
+
+@pytest.mark.parametrize("n,D,pad", [(5000, 320, 64), (700, 256, 8)])
+def test_full_accumulate_strided(n, D, pad):
+    """X with row stride D + pad (a ragged last column tile at D = 320)."""
+    say(f"case: strided syrk n={n} D={D} pad={pad}")
+    X = (np.random.default_rng(n).standard_normal((n, D)) * 2).astype(np.float16)
+    H = torch.zeros((D, D), dtype=torch.float32, device="cuda")
+    P.attr_precond_accumulate(_wide(X, pad), P.PRECOND_FULL, H)
+    torch.cuda.synchronize()
+    ref = O.accumulate_full(X)
+    iu = np.triu_indices(D)
+    got = host(H)
+    err = np.abs(got[iu] - ref[iu]).max() / np.abs(ref).max()
+    say("max rel err", err)
+    assert np.isfinite(got[iu]).all() and err <= 1e-5
+
+
+@pytest.mark.parametrize("mode", ["full", "diag"])
+def test_apply_strided(mode):
+    """X in and Y out both strided; Y's padding keeps its sentinel."""
+    n, D, xpad, ypad = 777, 320, 64, 128
+    say(f"case: strided apply {mode} n={n} D={D}")
+    rng = np.random.default_rng(8)
+    X = (rng.standard_normal((n, D)) * 3).astype(np.float16)
+    if mode == "full":
+        B = rng.standard_normal((D, D)) / np.sqrt(D)
+        M = (B @ B.T + 0.5 * np.eye(D)).astype(np.float32)
+    else:
+        M = (rng.random(D) + 0.5).astype(np.float32)
+    Ybuf = torch.full((n, D + ypad), 12345.0, dtype=torch.float32, device="cuda")
+    Y = Ybuf[:, :D]
+    P.attr_precond_apply(_wide(X, xpad), P.PRECOND_FULL if mode == "full" else P.PRECOND_DIAG,
+                         dev(M), True, Y)
+    torch.cuda.synchronize()
+    ref = O.precond_apply(X, mode, M.astype(np.float64), unit_norm=True)
+    err = row_rel_l2(host(Y), ref)
+    say("max row rel-L2", err.max())
+    assert err.max() <= 1e-5
+    assert (host(Ybuf)[:, D:] == 12345.0).all(), "padding of Y was written"
+
+
+def test_diag_accumulate_strided():
+    n, D, pad = 3001, 512, 64
+    say(f"case: strided diag accumulate n={n} D={D}")
+    X = (np.random.default_rng(9).standard_normal((n, D))).astype(np.float16)
+    h = torch.zeros(D, dtype=torch.float32, device="cuda")
+    P.attr_precond_accumulate(_wide(X, pad), P.PRECOND_DIAG, h)
+    torch.cuda.synchronize()
+    ref = O.accumulate_diag(X)
+    rel = np.abs(host(h) - ref) / ref
+    say("max rel err", rel.max())
+    assert rel.max() <= 1e-6
