@@ -2,7 +2,8 @@
 whose extra columns hold NaN) on the entry points that take a stride: the
 GEMM-plan and streaming-plan store scans (Q and G), the FULL accumulate
 (X), the FULL and DIAG applies (X in, Y out: the padding of Y stays
-untouched) and the DIAG accumulate.  A kernel that read or wrote past a
+untouched), the DIAG accumulate and the projection (every module's a and g
+rows).  A kernel that read or wrote past a
 row's width would turn results into NaN or overwrite the sentinel."""
 import numpy as np
 import pytest
@@ -98,3 +99,43 @@ def test_diag_accumulate_strided():
     rel = np.abs(host(h) - ref) / ref
     say("max rel err", rel.max())
     assert rel.max() <= 1e-6
+
+
+def _wide_any(x: np.ndarray, pad: int) -> torch.Tensor:
+    """_wide for fp32 arrays and for bf16 bit patterns (uint16: NaN 0x7fc0)."""
+    if x.dtype == np.uint16:
+        n, d = x.shape
+        buf = np.full((n, d + pad), 0x7FC0, dtype=np.uint16)
+        buf[:, :d] = x
+        return dev(buf)[:, :d]
+    return _wide(x, pad)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_project_strided(dtype):
+    """Projection with every module's a and g rows as views of wider buffers
+    (NaN in the extra columns), two 256-token chunks per example."""
+    n, T, k = 5, 300, 16
+    shapes = [(64, 192), (128, 64)]
+    say(f"case: strided projection {dtype} n={n} T={T} k={k}")
+    rng = np.random.default_rng(77)
+    cast = synth.to_bf16_bits if dtype == "bf16" else (lambda v: v.astype(np.float32))
+    host_mods, mods = [], []
+    for m, (d_in, d_out) in enumerate(shapes):
+        a = cast(rng.standard_normal((n * T, d_in)))
+        g = cast(rng.standard_normal((n * T, d_out)) * 1e-2)
+        R = cast(rng.standard_normal((d_out, k)) / np.sqrt(k))
+        S = cast(rng.standard_normal((d_in, k)) / np.sqrt(k))
+        host_mods.append((a, g, R, S))
+        mods.append(P.Module(_wide_any(a, 64), _wide_any(g, 32), dev(R), dev(S), out_col=m * k * k))
+    D = len(shapes) * k * k
+    out = torch.full((n, D), -7.0, dtype=torch.float32, device="cuda")
+    P.attr_project(mods, k, n, T, out)
+    torch.cuda.synchronize()
+    ref = O.project_concat([O.project(a.reshape(n, T, -1), g.reshape(n, T, -1), R, S)
+                            for (a, g, R, S) in host_mods])
+    got = host(out)
+    err = row_rel_l2(got, ref)
+    say("max row rel-L2", err.max())
+    assert np.isfinite(got).all()
+    assert err.max() <= (1e-4 if dtype == "bf16" else 1e-5)
