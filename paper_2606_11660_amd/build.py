@@ -159,6 +159,62 @@ def lds_dma_hazards(asm: str) -> list:
     return sorted(set(found))
 
 
+def _vgprs(tok: str) -> set:
+    m = re.match(r"v\[(\d+):(\d+)\]", tok)
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    m = re.match(r"v(\d+)$", tok)
+    return {int(m.group(1))} if m else set()
+
+
+def asm_valu_mfma_hazards(asm: str, need: int = 2) -> list:
+    """A VALU instruction written in inline asm (the GEMM core's in-place
+    sign flips of MFMA operand fragments) is invisible to the compiler's
+    hazard recognizer, which would otherwise separate a VALU write of a VGPR
+    from an MFMA that reads it by `need` wait states.  Following the
+    fall-through path from each such write, with one wait state per
+    instruction and N + 1 per s_nop N, an MFMA that reads the written VGPR
+    (any source operand) before `need` wait states is a violation, and so is
+    reaching a label or a branch first (the scan does not follow control
+    flow).  Returns a description of every violation in `asm`."""
+    lines = [l.strip() for l in asm.splitlines()]
+    found, kernel, in_asm = [], "?", False
+    for idx, line in enumerate(lines):
+        if re.match(r"^_Z\S+:", line):
+            kernel = line[:-1]
+        if line.startswith(";;#ASMSTART"):
+            in_asm = True
+            continue
+        if line.startswith(";;#ASMEND"):
+            in_asm = False
+            continue
+        if not in_asm or not line.startswith("v_") or line.startswith("v_mfma"):
+            continue
+        ops = _operands(line)
+        dst = _vgprs(ops[0]) if ops else set()
+        if not dst:
+            continue
+        ws, j = 0, idx + 1
+        while ws < need and j < len(lines):
+            nxt = lines[j]
+            j += 1
+            if not nxt or nxt.startswith(";") or (nxt.startswith(".") and not nxt.endswith(":")):
+                continue
+            if nxt.endswith(":") or _BRANCH.match(nxt) or nxt.split()[0] in _NO_FALLTHROUGH:
+                found.append(f"{kernel}: '{line}' reaches '{nxt}' before {need} wait states")
+                break
+            op = nxt.split()[0]
+            if op == "s_nop":
+                ws += int(nxt.split()[1], 0) + 1
+                continue
+            if op.startswith("v_mfma"):
+                srcs = set().union(*(_vgprs(t) for t in _operands(nxt)[1:]))
+                if srcs & dst:
+                    found.append(f"{kernel}: '{line}' {ws} wait states before '{nxt}'")
+            ws += 1
+    return sorted(set(found))
+
+
 def build(verbose: bool = False) -> str:
     hipcc = _hipcc()
     os.makedirs(BUILD, exist_ok=True)
@@ -188,9 +244,10 @@ def build(verbose: bool = False) -> str:
     hazards = []
     for j in asm_jobs:
         with open(j[-1]) as f:
-            hazards += lds_dma_hazards(f.read())
+            asm = f.read()
+        hazards += lds_dma_hazards(asm) + asm_valu_mfma_hazards(asm)
     if hazards:
-        raise RuntimeError("direct-to-LDS loads without the SGPR wait states:\n" + "\n".join(hazards))
+        raise RuntimeError("inline asm without the wait states it needs:\n" + "\n".join(hazards))
     tmp = LIB + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)

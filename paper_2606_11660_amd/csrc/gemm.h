@@ -639,7 +639,8 @@ __device__ inline int kmajor_swz(int r) { return (r & 3) | (((r >> 3) & 1) << 2)
 // ran short and the compiler moved accumulators in and out of it; inline
 // asm keeps them in place.  The asm is opaque to the compiler's hazard
 // checks, so a block of flips ends with s_nop 4 (five wait states; a VALU
-// write of a VGPR needs two before an MFMA reads it).
+// write of a VGPR needs two before an MFMA reads it), and the build scans
+// the assembly for an MFMA that reads a flipped register too soon.
 __device__ inline void flip_sign16(i32x4& f) {
   asm volatile("v_xor_b32 %0, 0x80008000, %0" : "+v"(f.x));
   asm volatile("v_xor_b32 %0, 0x80008000, %0" : "+v"(f.y));

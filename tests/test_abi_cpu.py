@@ -259,6 +259,25 @@ def test_lds_dma_hazards_compiler_m0_write():
     assert lds_dma_hazards(other) == []
 
 
+def test_asm_valu_write_before_mfma_read():
+    """An inline-asm VALU write (the sign flips of MFMA fragments) needs two
+    wait states before an MFMA reads the VGPR; other MFMAs, s_nop and
+    unrelated VGPRs do not trip it; a label or branch inside the window is
+    refused (the scan does not follow control flow)."""
+    from paper_2606_11660_amd.build import asm_valu_mfma_hazards
+    flip = [";;#ASMSTART", "\tv_xor_b32 v5, 0x80008000, v5", ";;#ASMEND"]
+    mf = "\tv_mfma_f32_16x16x32_f16 a[0:3], v[8:11], v[4:7], a[0:3]"
+    assert len(asm_valu_mfma_hazards(_asm(*flip, mf))) == 1
+    assert len(asm_valu_mfma_hazards(_asm(*flip, "\ts_nop 0", mf))) == 1
+    assert asm_valu_mfma_hazards(_asm(*flip, "\ts_nop 1", mf)) == []
+    other = "\tv_mfma_f32_16x16x32_f16 a[4:7], v[8:11], v[12:15], a[4:7]"
+    assert len(asm_valu_mfma_hazards(_asm(*flip, other, mf))) == 1
+    assert asm_valu_mfma_hazards(_asm(*flip, other, other, mf)) == []
+    assert len(asm_valu_mfma_hazards(_asm(*flip, ".LBB0_1:", "\ts_nop 7", mf))) == 1
+    # the same write by compiler-generated code is the compiler's to protect
+    assert asm_valu_mfma_hazards(_asm("\tv_xor_b32_e32 v5, 0x80008000, v5", mf)) == []
+
+
 def test_built_device_code_passes_the_hazard_scan():
     """Every device assembly file of the last build passes the scan (the
     build itself refuses to link otherwise); the scan sees the loads."""
@@ -267,12 +286,15 @@ def test_built_device_code_passes_the_hazard_scan():
     files = glob.glob(os.path.join(ROOT, "paper_2606_11660_amd", "_build", "*.s"))
     if not files:
         pytest.skip("no device assembly: build first")
-    n_loads = 0
+    from paper_2606_11660_amd.build import asm_valu_mfma_hazards
+    n_loads = n_flips = 0
     for f in files:
         asm = open(f).read()
         n_loads += sum(1 for l in asm.splitlines() if "buffer_load_dword" in l and " lds" in l)
+        n_flips += sum(1 for l in asm.splitlines() if l.strip().startswith("v_xor_b32 v"))
         assert lds_dma_hazards(asm) == [], f
-    assert n_loads > 0
+        assert asm_valu_mfma_hazards(asm) == [], f
+    assert n_loads > 0 and n_flips > 0
 
 
 def test_syrk_plan_slices_fit_their_buffer_range(tmp_path):
