@@ -25,6 +25,16 @@ def _wide(x: np.ndarray, pad: int) -> torch.Tensor:
     return dev(buf)[:, :d]
 
 
+def _wide_any(x: np.ndarray, pad: int) -> torch.Tensor:
+    """_wide for fp32 arrays and for bf16 bit patterns (uint16: NaN 0x7fc0)."""
+    if x.dtype == np.uint16:
+        n, d = x.shape
+        buf = np.full((n, d + pad), 0x7FC0, dtype=np.uint16)
+        buf[:, :d] = x
+        return dev(buf)[:, :d]
+    return _wide(x, pad)
+
+
 def _topk(Q, G, k):
     ts = torch.full((Q.shape[0], k), 5.0, dtype=torch.float32, device="cuda")
     ti = torch.full((Q.shape[0], k), 7, dtype=torch.int64, device="cuda")
@@ -33,28 +43,32 @@ def _topk(Q, G, k):
     return host(ts), host(ti)
 
 
-@pytest.mark.parametrize("nq,ng,D,k,qpad,gpad", [(300, 9000, 256, 10, 64, 192),
-                                                 (128, 5000, 192, 20, 8, 72),
-                                                 (40, 9000, 256, 10, 64, 128)])
-def test_scan_strided(nq, ng, D, k, qpad, gpad):
+@pytest.mark.parametrize("nq,ng,D,k,qpad,gpad,dt", [(300, 9000, 256, 10, 64, 192, np.float16),
+                                                    (128, 5000, 192, 20, 8, 72, np.float16),
+                                                    (40, 9000, 256, 10, 64, 128, np.float16),
+                                                    (40, 9000, 96, 10, 4, 36, np.float32)])
+def test_scan_strided(nq, ng, D, k, qpad, gpad, dt):
     """GEMM plan (300 queries: 256 x 256 tiles; 128: the ring) and the
-    streaming plan (40 queries) on strided Q and G."""
-    say(f"case: strided scan nq={nq} ng={ng} D={D} k={k} pads {qpad},{gpad}")
-    Q = synth.unit_rows(nq, D, seed=51)
-    G = synth.unit_rows(ng, D, seed=52)
+    streaming plan (40 queries, fp16 and fp32) on strided Q and G."""
+    say(f"case: strided scan nq={nq} ng={ng} D={D} k={k} pads {qpad},{gpad} {dt.__name__}")
+    Q = synth.unit_rows(nq, D, seed=51, dtype=dt)
+    G = synth.unit_rows(ng, D, seed=52, dtype=dt)
     Qd, Gd = _wide(Q, qpad), _wide(G, gpad)
     assert Qd.stride(0) == D + qpad and Gd.stride(0) == D + gpad
     ts, ti = _topk(Qd, Gd, k)
     check_topk(ts, ti, O.scores(Q, G), k)
 
 
-@pytest.mark.parametrize("n,D,pad", [(5000, 320, 64), (700, 256, 8)])
-def test_full_accumulate_strided(n, D, pad):
-    """X with row stride D + pad (a ragged last column tile at D = 320)."""
-    say(f"case: strided syrk n={n} D={D} pad={pad}")
-    X = (np.random.default_rng(n).standard_normal((n, D)) * 2).astype(np.float16)
+@pytest.mark.parametrize("n,D,pad,bf16", [(5000, 320, 64, False), (700, 256, 8, False),
+                                          (3000, 320, 32, True)])
+def test_full_accumulate_strided(n, D, pad, bf16):
+    """X with row stride D + pad (a ragged last column tile at D = 320), fp16
+    and bf16."""
+    say(f"case: strided syrk n={n} D={D} pad={pad} bf16={bf16}")
+    Xf = np.random.default_rng(n).standard_normal((n, D)) * 2
+    X = synth.to_bf16_bits(Xf) if bf16 else Xf.astype(np.float16)
     H = torch.zeros((D, D), dtype=torch.float32, device="cuda")
-    P.attr_precond_accumulate(_wide(X, pad), P.PRECOND_FULL, H)
+    P.attr_precond_accumulate(_wide_any(X, pad), P.PRECOND_FULL, H)
     torch.cuda.synchronize()
     ref = O.accumulate_full(X)
     iu = np.triu_indices(D)
@@ -99,16 +113,6 @@ def test_diag_accumulate_strided():
     rel = np.abs(host(h) - ref) / ref
     say("max rel err", rel.max())
     assert rel.max() <= 1e-6
-
-
-def _wide_any(x: np.ndarray, pad: int) -> torch.Tensor:
-    """_wide for fp32 arrays and for bf16 bit patterns (uint16: NaN 0x7fc0)."""
-    if x.dtype == np.uint16:
-        n, d = x.shape
-        buf = np.full((n, d + pad), 0x7FC0, dtype=np.uint16)
-        buf[:, :d] = x
-        return dev(buf)[:, :d]
-    return _wide(x, pad)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
